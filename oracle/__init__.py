@@ -1,0 +1,143 @@
+"""CPU oracle of the speculative verification step -- TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The product path (the HIP library and its Python
+binding) never does, and shares no code with it: ``spexis_oracle.c`` restates the cache
+layout, the fp64 attention, the fp64 softmax and the exact-arithmetic acceptance rule from
+their definitions (see the header of that file for the passages each function follows).
+
+Everything here takes and returns numpy arrays on the host.  bf16 tensors are passed as
+their uint16 bit patterns.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "spexis_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "libspexis_oracle.so")
+
+# row_status codes of the acceptance rule
+OK, EMPTY_ROW, BAD_ROW, BAD_TOKEN = 0, 1, 2, 3
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (plain C11 + OpenMP, no fast-math, no FMA contraction)."""
+    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+                               "-Wall", "-shared", "-fPIC", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        build()
+        L = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        i32, i64, f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+        L.oracle_append_kv.argtypes = [P, P, i32, i32, i32, i32, i32, P, P, P, i32, P, P]
+        L.oracle_append_kv.restype = ctypes.c_int
+        L.oracle_attention.argtypes = [P, P, i32, i32, i32, i32, i32, P, P, P, i32, P, i32, f32, P, i32, P]
+        L.oracle_attention.restype = ctypes.c_int
+        L.oracle_softmax.argtypes = [P, i64, i32, f32, P]
+        L.oracle_softmax.restype = None
+        L.oracle_accept.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, P, P]
+        L.oracle_accept.restype = None
+        L.oracle_num_threads.argtypes = []
+        L.oracle_num_threads.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _c(a: np.ndarray, dtype) -> np.ndarray:
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a
+
+
+def _p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def num_threads() -> int:
+    return int(lib().oracle_num_threads())
+
+
+def append_kv(k_pool: np.ndarray, v_pool: np.ndarray, num_blocks: int, num_kv_heads: int, block_size: int,
+              head_dim: int, qsl, seq_lens, block_tables, new_k: np.ndarray, new_v: np.ndarray) -> None:
+    """Write new K/V rows [T, Hkv, D] (uint16 bf16 bits) into the pools, in place."""
+    assert k_pool.dtype == np.uint16 and v_pool.dtype == np.uint16
+    assert k_pool.flags.c_contiguous and v_pool.flags.c_contiguous
+    qsl, seq_lens = _c(qsl, np.int32), _c(seq_lens, np.int32)
+    bt = _c(block_tables, np.int32)
+    nk, nv = _c(new_k, np.uint16), _c(new_v, np.uint16)
+    B = len(seq_lens)
+    rc = lib().oracle_append_kv(_p(k_pool), _p(v_pool), num_blocks, num_kv_heads, block_size, head_dim, B,
+                                _p(qsl), _p(seq_lens), _p(bt), bt.shape[1], _p(nk), _p(nv))
+    if rc != 0:
+        raise ValueError("oracle_append_kv: index out of range")
+
+
+def attention(k_pool: np.ndarray, v_pool: np.ndarray, num_blocks: int, num_kv_heads: int, block_size: int,
+              head_dim: int, qsl, seq_lens, block_tables, q: np.ndarray, num_q_heads: int, scale: float,
+              seqs=None, out: np.ndarray = None) -> np.ndarray:
+    """fp64 attention output [T, Hq, D]; only rows of ``seqs`` (default: all) are computed."""
+    qsl, seq_lens = _c(qsl, np.int32), _c(seq_lens, np.int32)
+    bt = _c(block_tables, np.int32)
+    qq = _c(q, np.uint16)
+    B = len(seq_lens)
+    T = int(qsl[-1])
+    seqs = _c(np.arange(B) if seqs is None else seqs, np.int32)
+    if out is None:
+        out = np.full((T, num_q_heads, head_dim), np.nan, dtype=np.float64)
+    assert out.dtype == np.float64 and out.flags.c_contiguous
+    rc = lib().oracle_attention(_p(k_pool), _p(v_pool), num_blocks, num_kv_heads, block_size, head_dim, B,
+                                _p(qsl), _p(seq_lens), _p(bt), bt.shape[1], _p(qq), num_q_heads,
+                                ctypes.c_float(scale), _p(seqs), len(seqs), _p(out))
+    if rc != 0:
+        raise ValueError("oracle_attention: bad arguments or index out of range")
+    return out
+
+
+def softmax(logits: np.ndarray, temperature: float = 1.0) -> np.ndarray:
+    """fp32 probabilities of fp32 logits [rows, V], computed in fp64."""
+    x = _c(logits, np.float32)
+    rows, V = x.shape
+    out = np.empty_like(x)
+    lib().oracle_softmax(_p(x), rows, V, ctypes.c_float(temperature), _p(out))
+    return out
+
+
+def accept(qsl, target: np.ndarray, draft: np.ndarray, draft_ids, u_accept, u_sample, max_k: int = None,
+           seq_lens=None):
+    """Acceptance on fp32 probability rows.
+
+    Returns (accepted_len [B], out_tokens [B, max_k+1], row_status [B], new_seq_lens or None).
+    """
+    qsl = _c(qsl, np.int32)
+    B = len(qsl) - 1
+    tg = _c(target, np.float32)
+    V = tg.shape[1]
+    nd = int(qsl[-1]) - B
+    dr = _c(draft, np.float32).reshape(nd, V) if nd > 0 else np.zeros((1, V), np.float32)
+    ids = _c(draft_ids, np.int32) if nd > 0 else np.zeros(1, np.int32)
+    ua = _c(u_accept, np.float32) if nd > 0 else np.zeros(1, np.float32)
+    us = _c(u_sample, np.float32)
+    if max_k is None:
+        max_k = int((np.diff(qsl) - 1).max())
+    acc = np.empty(B, np.int32)
+    toks = np.empty((B, max_k + 1), np.int32)
+    status = np.empty(B, np.int32)
+    sl = _c(seq_lens, np.int32).copy() if seq_lens is not None else None
+    lib().oracle_accept(B, V, max_k, _p(qsl), _p(tg), _p(dr), _p(ids), _p(ua), _p(us), _p(acc), _p(toks),
+                        _p(status), _p(sl) if sl is not None else None)
+    return acc, toks, status, sl

@@ -1,0 +1,324 @@
+/*
+ * spexis_oracle.c -- plain, slow CPU reference of the speculative verification step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may call, link or load this
+ * file or the library built from it; only the test suite, the smoke check and the
+ * CPU-baseline leg of the benchmark do.  It shares no code, header, table or helper
+ * with the HIP implementation: the cache layout, the softmax and the acceptance rule are
+ * written out here again from their definitions.
+ *
+ * What it computes (Spexis, "Speculative-Parallel Execution" and Related Work, which cite
+ * speculative decoding [sd]: the draft proposes k tokens, the full model verifies them in
+ * one pass):
+ *   oracle_append_kv   -- write the k+1 new K/V rows of every sequence into the paged cache
+ *                         (the cache is shared by speculative and normal execution, Sec. 4).
+ *   oracle_attention   -- causal, grouped-query attention of the k+1 query tokens of each
+ *                         sequence over its paged KV, in fp64, straight from the definition.
+ *   oracle_softmax     -- temperature softmax of fp32 logits, in fp64, rounded to fp32.
+ *   oracle_accept      -- speculative-sampling acceptance (accept x_i with probability
+ *                         min(1, p_i(x_i)/q_i(x_i)); on the first rejection sample from the
+ *                         normalised residual max(0, p - q); otherwise sample the bonus token
+ *                         from p_k), with every decision taken in exact arithmetic so that any
+ *                         correct implementation reaches the same integers.
+ *
+ * Cache layout (the library's documented format, restated here independently):
+ *   K pool: bf16 [num_blocks][Hkv][D/8][bs][8]
+ *           element (blk, h, slot, d) at ((((blk*Hkv + h)*(D/8) + d/8)*bs + slot)*8 + d%8)
+ *   V pool: bf16 [num_blocks][Hkv][D][bs], the slot index stored with bits 2 and 3 swapped
+ *           element (blk, h, slot, d) at (((blk*Hkv + h)*D + d)*bs + swap23(slot))
+ *
+ * Build: gcc -O2 -std=c11 -fopenmp -ffp-contract=off -shared -fPIC (no fast-math).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* ---------------------------------------------------------------- helpers */
+
+/* bf16 bit pattern -> double (exact: bf16 is the top half of an fp32). */
+static double bf16_to_double(uint16_t bits) {
+  uint32_t u = (uint32_t)bits << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+static int64_t swap23(int64_t slot) {
+  int64_t b2 = (slot >> 2) & 1, b3 = (slot >> 3) & 1;
+  return (slot & ~(int64_t)12) | (b2 << 3) | (b3 << 2);
+}
+
+static int64_t k_index(int64_t blk, int64_t h, int64_t slot, int64_t d, int64_t hkv, int64_t bs,
+                       int64_t D) {
+  return (((blk * hkv + h) * (D / 8) + d / 8) * bs + slot) * 8 + d % 8;
+}
+
+static int64_t v_index(int64_t blk, int64_t h, int64_t slot, int64_t d, int64_t hkv, int64_t bs,
+                       int64_t D) {
+  return ((blk * hkv + h) * D + d) * bs + swap23(slot);
+}
+
+/* ------------------------------------------------------------- append KV */
+
+/*
+ * For sequence b with n_b = qsl[b+1]-qsl[b] new tokens and post-append length S_b,
+ * new token j sits at position L_b + j with L_b = S_b - n_b; its row goes to block
+ * block_tables[b][pos/bs], slot pos%bs.  Returns 0, or -1 if an index is out of range
+ * (a sequence with inconsistent lengths, or a token whose block id is out of range, is
+ * skipped).
+ */
+int oracle_append_kv(uint16_t* k_pool, uint16_t* v_pool, int32_t num_blocks, int32_t hkv,
+                     int32_t bs, int32_t D, int32_t B, const int32_t* qsl,
+                     const int32_t* seq_lens, const int32_t* block_tables,
+                     int32_t max_blocks_per_seq, const uint16_t* new_k, const uint16_t* new_v) {
+  int rc = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    int32_t n = qsl[b + 1] - qsl[b];
+    int32_t L = seq_lens[b] - n;
+    if (n < 1 || L < 0 || (seq_lens[b] + bs - 1) / bs > max_blocks_per_seq) { rc = -1; continue; }
+    for (int32_t j = 0; j < n; ++j) {
+      int64_t pos = (int64_t)L + j;
+      int32_t blk = block_tables[(int64_t)b * max_blocks_per_seq + pos / bs];
+      if (blk < 0 || blk >= num_blocks) { rc = -1; continue; }
+      int64_t slot = pos % bs;
+      int64_t row = (int64_t)qsl[b] + j;
+      for (int32_t h = 0; h < hkv; ++h)
+        for (int32_t d = 0; d < D; ++d) {
+          int64_t src = (row * hkv + h) * D + d;
+          k_pool[k_index(blk, h, slot, d, hkv, bs, D)] = new_k[src];
+          v_pool[v_index(blk, h, slot, d, hkv, bs, D)] = new_v[src];
+        }
+    }
+  }
+  return rc;
+}
+
+/* ------------------------------------------------------------- attention */
+
+/*
+ * out[(qsl[b]+j)*Hq + h][d] = sum_t softmax_t(s) v[b,t,g][d], fp64, for every sequence b
+ * listed in seqs[0..nseqs), query token j < n_b and query head h, where
+ *   g = h / (Hq/Hkv)                     (contiguous query-head groups share a KV head)
+ *   t ranges over 0 .. L_b + j           (a query sees the cache and itself, not later drafts)
+ *   s_t = scale * <q[qsl[b]+j][h], k[b,t,g]>
+ * Rows of sequences not listed are left untouched.  Returns -1 on an index out of range.
+ */
+int oracle_attention(const uint16_t* k_pool, const uint16_t* v_pool, int32_t num_blocks,
+                     int32_t hkv, int32_t bs, int32_t D, int32_t B, const int32_t* qsl,
+                     const int32_t* seq_lens, const int32_t* block_tables,
+                     int32_t max_blocks_per_seq, const uint16_t* q, int32_t hq, float scale,
+                     const int32_t* seqs, int32_t nseqs, double* out) {
+  if (hkv <= 0 || hq % hkv != 0) return -1;
+  int32_t G = hq / hkv;
+  int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+  for (int32_t si = 0; si < nseqs; ++si) {
+    int32_t b = seqs[si];
+    if (b < 0 || b >= B) { bad |= 1; continue; }
+    int32_t n = qsl[b + 1] - qsl[b];
+    int32_t S = seq_lens[b];
+    int32_t L = S - n;
+    if (n < 1 || L < 0 || (S + bs - 1) / bs > max_blocks_per_seq) { bad |= 1; continue; }
+    double* s = (double*)malloc(sizeof(double) * (size_t)S);
+    for (int32_t j = 0; j < n; ++j) {
+      for (int32_t h = 0; h < hq; ++h) {
+        int32_t g = h / G;
+        const uint16_t* qrow = q + ((int64_t)(qsl[b] + j) * hq + h) * D;
+        int32_t last = L + j; /* keys 0..last are visible */
+        double m = -INFINITY;
+        for (int32_t t = 0; t <= last; ++t) {
+          int32_t blk = block_tables[(int64_t)b * max_blocks_per_seq + t / bs];
+          if (blk < 0 || blk >= num_blocks) { bad |= 1; blk = 0; }
+          double dot = 0.0;
+          for (int32_t d = 0; d < D; ++d)
+            dot += bf16_to_double(qrow[d]) * bf16_to_double(k_pool[k_index(blk, g, t % bs, d, hkv, bs, D)]);
+          s[t] = (double)scale * dot;
+          if (s[t] > m) m = s[t];
+        }
+        double z = 0.0;
+        for (int32_t t = 0; t <= last; ++t) { s[t] = exp(s[t] - m); z += s[t]; }
+        double* o = out + ((int64_t)(qsl[b] + j) * hq + h) * D;
+        for (int32_t d = 0; d < D; ++d) o[d] = 0.0;
+        for (int32_t t = 0; t <= last; ++t) {
+          int32_t blk = block_tables[(int64_t)b * max_blocks_per_seq + t / bs];
+          if (blk < 0 || blk >= num_blocks) blk = 0;
+          double w = s[t] / z;
+          for (int32_t d = 0; d < D; ++d)
+            o[d] += w * bf16_to_double(v_pool[v_index(blk, g, t % bs, d, hkv, bs, D)]);
+        }
+      }
+    }
+    free(s);
+  }
+  return bad ? -1 : 0;
+}
+
+/* --------------------------------------------------------------- softmax */
+
+/*
+ * probs[r][v] = exp((l_v - max l)/T) / sum_u exp((l_u - max l)/T), evaluated in fp64 from
+ * the fp32 logits and fp32 temperature, then rounded to fp32.  Temperature divides the
+ * logits of both the target and the draft rows before the softmax.
+ */
+void oracle_softmax(const float* logits, int64_t rows, int32_t V, float temperature, float* probs) {
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < rows; ++r) {
+    const float* x = logits + r * V;
+    double m = -INFINITY;
+    for (int32_t v = 0; v < V; ++v) if ((double)x[v] > m) m = (double)x[v];
+    double* e = (double*)malloc(sizeof(double) * (size_t)V);
+    double z = 0.0;
+    for (int32_t v = 0; v < V; ++v) { e[v] = exp(((double)x[v] - m) / (double)temperature); z += e[v]; }
+    for (int32_t v = 0; v < V; ++v) probs[r * V + v] = (float)(e[v] / z);
+    free(e);
+  }
+}
+
+/* ---------------------------------------------------------------- accept */
+
+/* row_status codes */
+#define ORACLE_OK 0
+#define ORACLE_EMPTY_ROW 1   /* sampled row had no positive weight, even after the fallback */
+#define ORACLE_BAD_ROW 2     /* sampled row held a NaN, an infinity or a negative value */
+#define ORACLE_BAD_TOKEN 3   /* a draft token id outside [0, V) */
+
+static int bad_value(float x) { return isnan(x) || isinf(x) || x < 0.0f; }
+
+/*
+ * Exact threshold t = floor(u * S) for an fp32 uniform u and an integer S < 2^63.
+ * u = f * 2^e with f in [0.5, 1) (frexp); f * 2^24 is an integer m < 2^24, so
+ * u * S = m * S / 2^(24 - e) and the floor is a right shift of the 128-bit product.
+ * u <= 0 or NaN gives 0; u >= 1 gives S - 1; the result is clamped to S - 1.
+ */
+static uint64_t exact_threshold(float u, uint64_t S) {
+  if (!(u > 0.0f)) return 0;
+  if (u >= 1.0f) return S - 1;
+  int e;
+  float f = frexpf(u, &e);
+  uint64_t m = (uint64_t)ldexpf(f, 24);
+  int shift = 24 - e; /* >= 25 */
+  unsigned __int128 prod = (unsigned __int128)m * (unsigned __int128)S;
+  uint64_t t = shift >= 128 ? 0 : (uint64_t)(prod >> shift);
+  return t < S ? t : S - 1;
+}
+
+/*
+ * Inverse-CDF sample of the fp32 weight row w[0..V) with the uniform u, in fixed point:
+ *   M = max w; e such that M in [2^e, 2^(e+1)); s = 40 - e;
+ *   W_v = floor(w_v * 2^s)  (exact: a power-of-two scaling of an fp32 value, then floor);
+ *   S = sum W_v;  t = floor(u * S) exactly;
+ *   token = the smallest m with W_0 + ... + W_m > t.
+ * Returns -1 if M == 0.
+ */
+static int32_t sample_fixed_point(const float* w, int32_t V, float u) {
+  float M = 0.0f;
+  for (int32_t v = 0; v < V; ++v) if (w[v] > M) M = w[v];
+  if (M == 0.0f) return -1;
+  int E;
+  frexp((double)M, &E); /* M = f * 2^E, f in [0.5,1)  =>  M in [2^(E-1), 2^E) */
+  int s = 40 - (E - 1);
+  uint64_t S = 0;
+  for (int32_t v = 0; v < V; ++v) S += (uint64_t)floor(ldexp((double)w[v], s));
+  uint64_t t = exact_threshold(u, S);
+  uint64_t prefix = 0;
+  for (int32_t v = 0; v < V; ++v) {
+    prefix += (uint64_t)floor(ldexp((double)w[v], s));
+    if (prefix > t) return v;
+  }
+  return V - 1; /* unreachable: prefix reaches S > t */
+}
+
+/*
+ * Speculative-sampling acceptance on fp32 probability rows.
+ *   Sequence b has k_b = qsl[b+1]-qsl[b]-1 drafts x_i = draft_ids[qsl[b]-b+i].
+ *   Target row i of b is target[(qsl[b]+i)*V ...] (i = 0..k_b); draft row i is
+ *   draft[(qsl[b]-b+i)*V ...] (i = 0..k_b-1).
+ * Steps, for each b:
+ *   1. any x_i outside [0, V): status 3, a_b = 0, every token -1.
+ *   2. for i = 0..k_b-1: accept iff (double)u_i * (double)q_i(x_i) < (double)p_i(x_i)
+ *      (exact: a product of two fp32 values is exact in fp64, so this is u < p/q, i.e. the
+ *      test u < min(1, p/q) for u in [0,1)); a_b = the number of leading accepts.
+ *   3. a_b < k_b: weights w_v = max(0, fp32(p_a(v) - q_a(v))); if every w_v is 0, fall
+ *      back to w = p_a.  a_b = k_b: w = p_k (bonus token).
+ *      The row(s) read here must be finite and non-negative, else status 2.
+ *   4. token = sample_fixed_point(w, u_sample[b]); if no weight is positive, status 1.
+ *   Outputs: accepted_len[b] = a_b; out_tokens[b][0..a_b) = x_0..x_{a_b-1};
+ *   out_tokens[b][a_b] = token (-1 on status 1/2); later positions -1.
+ *   If seq_lens_inout is not NULL, seq_lens_inout[b] = S_b - k_b + a_b (the rows of
+ *   rejected drafts become stale) unless status is 3.
+ */
+void oracle_accept(int32_t B, int32_t V, int32_t max_k, const int32_t* qsl, const float* target,
+                   const float* draft, const int32_t* draft_ids, const float* u_accept,
+                   const float* u_sample, int32_t* accepted_len, int32_t* out_tokens,
+                   int32_t* row_status, int32_t* seq_lens_inout) {
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int32_t b = 0; b < B; ++b) {
+    int32_t k = qsl[b + 1] - qsl[b] - 1;
+    int64_t t0 = qsl[b];       /* first target row of b */
+    int64_t d0 = qsl[b] - b;   /* first draft row of b */
+    int32_t* tok = out_tokens + (int64_t)b * (max_k + 1);
+    for (int32_t i = 0; i <= max_k; ++i) tok[i] = -1;
+    accepted_len[b] = 0;
+    row_status[b] = ORACLE_OK;
+
+    int ids_ok = 1;
+    for (int32_t i = 0; i < k; ++i)
+      if (draft_ids[d0 + i] < 0 || draft_ids[d0 + i] >= V) ids_ok = 0;
+    if (!ids_ok) { row_status[b] = ORACLE_BAD_TOKEN; continue; }
+
+    int32_t a = 0;
+    while (a < k) {
+      int32_t x = draft_ids[d0 + a];
+      double p = (double)target[(t0 + a) * V + x];
+      double q = (double)draft[(d0 + a) * V + x];
+      double u = (double)u_accept[d0 + a];
+      if (u * q < p) ++a; else break;
+    }
+    accepted_len[b] = a;
+    for (int32_t i = 0; i < a; ++i) tok[i] = draft_ids[d0 + i];
+    if (seq_lens_inout) seq_lens_inout[b] = seq_lens_inout[b] - k + a;
+
+    const float* P = target + (t0 + a) * V;
+    const float* Q = a < k ? draft + (d0 + a) * V : NULL;
+    int bad = 0;
+    for (int32_t v = 0; v < V; ++v) {
+      if (bad_value(P[v])) bad = 1;
+      if (Q && bad_value(Q[v])) bad = 1;
+    }
+    if (bad) { row_status[b] = ORACLE_BAD_ROW; continue; }
+
+    float* w = (float*)malloc(sizeof(float) * (size_t)V);
+    int any = 0;
+    for (int32_t v = 0; v < V; ++v) {
+      if (Q) {
+        float diff = P[v] - Q[v]; /* one IEEE fp32 subtraction, round to nearest */
+        w[v] = diff > 0.0f ? diff : 0.0f;
+      } else {
+        w[v] = P[v];
+      }
+      if (w[v] > 0.0f) any = 1;
+    }
+    if (!any && Q) for (int32_t v = 0; v < V; ++v) w[v] = P[v];
+    int32_t token = sample_fixed_point(w, V, u_sample[b]);
+    free(w);
+    if (token < 0) row_status[b] = ORACLE_EMPTY_ROW;
+    tok[a] = token;
+  }
+}
+
+/* Number of OpenMP threads the parallel loops above use (for reporting). */
+int oracle_num_threads(void) {
+  int n = 1;
+#ifdef _OPENMP
+#pragma omp parallel
+  {
+#pragma omp single
+    n = omp_get_num_threads();
+  }
+#endif
+  return n;
+}
