@@ -1,0 +1,199 @@
+"""Benchmark of the speculative verification step on one MI355X.
+
+A step is one pass of the whole hot path over one synthetic batch already resident in HBM:
+spexis_append_kv -> spexis_verify_attention -> spexis_accept (logits mode, temperature as
+the workload sets).  Throughput is verified tokens per second: sum_b (a_b + 1) emitted tokens
+(accepted drafts plus the resampled or bonus token) over the step time.
+
+Prints ONE JSON line.  Also reports the attention kernel against the HBM roofline (algorithmic
+bytes over its event-timed duration) and the CPU oracle timed on the host cores.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 2] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "verified tokens/sec (verify-attn + accept) at 1 GPU; achieved HBM GB/s"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def attention_bytes(batch, spec) -> int:
+    """Algorithmic bytes of one verify-attention launch: every cached K and V element once,
+    Q in and O out once, and the block-table entries the sequences use."""
+    D, hkv, hq = spec.head_dim, spec.num_kv_heads, spec.num_q_heads
+    kv = int(batch.seq_lens.astype(np.int64).sum()) * hkv * D * 2 * 2
+    qo = batch.T * hq * D * 2 * 2
+    tables = int(((batch.seq_lens + spec.block_size - 1) // spec.block_size).sum()) * 4
+    return kv + qo + tables
+
+
+def attention_flops(batch, spec) -> int:
+    D, hq = spec.head_dim, spec.num_q_heads
+    f = 0
+    for b in range(batch.B):
+        n, L = int(batch.k[b]) + 1, int(batch.ctx_lens[b])
+        f += hq * 4 * D * sum(L + j + 1 for j in range(n))
+    return f
+
+
+def cpu_baseline(spec, batch, attn, acc, min_seconds=10.0, max_reps=40):
+    """Time the oracle on the whole step (attention of every sequence, softmax of every target
+    and draft row, acceptance) on the host cores; returns the verified tokens/s it reaches."""
+    import oracle
+    from paper_2609_34370_amd.step import bf16_to_u16
+
+    kp, vp = bf16_to_u16(attn.k_pool).copy(), bf16_to_u16(attn.v_pool).copy()
+    q = bf16_to_u16(attn.q)
+    nk, nv = bf16_to_u16(attn.new_k), bf16_to_u16(attn.new_v)
+    tl, dl = acc.target_logits.cpu().numpy(), acc.draft_logits.cpu().numpy()
+    ids, ua, us = acc.draft_ids.cpu().numpy(), acc.u_accept.cpu().numpy(), acc.u_sample.cpu().numpy()
+    scale = float(np.float32(1.0 / math.sqrt(spec.head_dim)))
+    reps, emitted, t_total = 0, 0, 0.0
+    while reps < max_reps and (reps == 0 or t_total < min_seconds):
+        t0 = time.perf_counter()
+        oracle.append_kv(kp, vp, batch.num_blocks, spec.num_kv_heads, spec.block_size, spec.head_dim, batch.qsl,
+                         batch.seq_lens, batch.block_tables, nk, nv)
+        oracle.attention(kp, vp, batch.num_blocks, spec.num_kv_heads, spec.block_size, spec.head_dim, batch.qsl,
+                         batch.seq_lens, batch.block_tables, q, spec.num_q_heads, scale)
+        p = oracle.softmax(tl, acc.temperature)
+        qq = oracle.softmax(dl, acc.temperature)
+        a, _, _, _ = oracle.accept(batch.qsl, p, qq, ids, ua, us, max_k=batch.max_k)
+        t_total += time.perf_counter() - t0
+        emitted += int((a.astype(np.int64) + 1).sum())
+        reps += 1
+    return {"value": round(emitted / t_total, 2), "unit": "tokens/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"the full {spec.name} step ({batch.B} sequences: append, fp64 attention, fp64 softmax of "
+                      f"{batch.T}+{batch.T - batch.B} rows, exact acceptance) x{reps}, {t_total:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--kv-chunk", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_34370_amd import spexis as sx
+    from paper_2609_34370_amd import workloads as wl
+    from paper_2609_34370_amd.step import VerifyStep
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    spec = wl.WORKLOADS[args.workload]
+    log(f"[bench] workload {spec.wid} ({spec.name}): generating inputs on the GPU")
+    batch = wl.make_batch(spec, seed=args.seed)
+    attn = wl.make_attention_inputs(spec, batch, device="cuda", seed=args.seed)
+    acc = wl.make_accept_inputs(spec, batch, device="cuda", seed=args.seed)
+    torch.cuda.synchronize()
+    # host copies for the oracle baseline are taken before the GPU appends (same bytes it saw)
+    baseline_inputs = None
+    if not args.no_cpu_baseline:
+        baseline_inputs = wl.AttentionInputs(attn.k_pool.cpu(), attn.v_pool.cpu(), attn.q.cpu(), attn.new_k.cpu(),
+                                             attn.new_v.cpu())
+    step = VerifyStep(batch, attn, acc, kv_chunk_tokens=args.kv_chunk, kind=sx.SPEXIS_INPUT_LOGITS)
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        step.run()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        ev[i][0].record(stream)
+        step.append()
+        ev[i][1].record(stream)
+        step.attention()
+        ev[i][2].record(stream)
+        step.accept()
+        ev[i][3].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    a, toks, status = step.accept_outputs()
+    emitted = int((a.astype(np.int64) + 1).sum())
+    ms_append = float(np.mean([ev[i][0].elapsed_time(ev[i][1]) for i in range(K)]))
+    ms_attn = float(np.mean([ev[i][1].elapsed_time(ev[i][2]) for i in range(K)]))
+    ms_accept = float(np.mean([ev[i][2].elapsed_time(ev[i][3]) for i in range(K)]))
+    ms_step = elapsed * 1e3 / K
+    value = emitted / (ms_step * 1e-3)
+    abytes = attention_bytes(batch, spec)
+    achieved = abytes / (ms_attn * 1e-3) / 1e9
+    log(f"[bench] append {ms_append * 1e3:.1f} us  attention {ms_attn * 1e3:.1f} us  accept {ms_accept * 1e3:.1f} us"
+        f"  step {ms_step * 1e3:.1f} us  emitted {emitted}/step  accepted mean {a.mean():.3f}  status!=0 "
+        f"{int((status != 0).sum())}")
+    log(f"[bench] attention {abytes / 1e9:.3f} GB algorithmic -> {achieved:.0f} GB/s "
+        f"({achieved / HBM_PEAK_GBS:.1%} of 8 TB/s); {attention_flops(batch, spec) / (ms_attn * 1e-3) / 1e12:.1f} "
+        f"TFLOP/s")
+
+    cpu = None
+    if baseline_inputs is not None and int(os.environ.get("RANK", "0")) == 0:
+        log("[bench] timing the CPU oracle on the host cores")
+        cpu = cpu_baseline(spec, batch, baseline_inputs, acc)
+        log(f"[bench] oracle: {cpu}")
+
+    traffic = None
+    prof = os.path.join(ROOT, "profiles", "traffic.json")
+    if os.path.exists(prof):
+        with open(prof) as f:
+            t = json.load(f).get(f"workload{spec.wid}")
+        if t and t.get("source_digest") == _kernel_digest():
+            traffic = t["bytes_per_launch"]
+
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": spec.name, "batch": batch.B, "q_heads": spec.num_q_heads,
+                   "kv_heads": spec.num_kv_heads, "head_dim": spec.head_dim, "block_size": spec.block_size,
+                   "context": list(spec.ctx), "draft_tokens": list(spec.k), "vocab": spec.vocab,
+                   "temperature": spec.temperature, "accept_input": "logits", "parallelism": "none"},
+        "phases_us": {"append": round(ms_append * 1e3, 2), "verify_attention": round(ms_attn * 1e3, 2),
+                      "accept": round(ms_accept * 1e3, 2)},
+        "emitted_tokens_per_step": emitted,
+        "roofline": {"bound": "hbm", "kernel": "spexis_verify_attention", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "algorithmic_bytes": abytes},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def _kernel_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    with open(os.path.join(ROOT, "paper_2609_34370_amd", "csrc", "attention.hip"), "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,207 @@
+/*
+ * spexis.h -- C ABI of the speculative-verification hot path on one MI355X (gfx950).
+ *
+ * Spexis (speculative-parallel execution, Sec. 4) verifies the k tokens a self-speculative
+ * draft proposes with one pass of the full model: the k+1 query tokens of a sequence (its
+ * last accepted token and the k drafts) are appended to the paged KV cache that speculative
+ * and normal execution share, attend causally over that cache, and the speculative-sampling
+ * rule the paper adopts from [sd] (Related Work) decides how many drafts survive.  This
+ * library computes exactly that step:
+ *
+ *   spexis_append_kv         write the k+1 new K/V rows of every sequence into the cache
+ *   spexis_verify_attention  causal grouped-query attention of those rows over the cache
+ *   spexis_accept            ratio tests, residual / bonus sampling, outputs
+ *   spexis_softmax_rows      temperature softmax of logit rows (probability inputs)
+ *
+ * Conventions shared by every entry point
+ *   - Pointers are DEVICE pointers unless a parameter says "host".  Every call is
+ *     asynchronous on `stream` (a hipStream_t passed as void*; NULL = the null stream);
+ *     the library never synchronises and never reads device data on the host.
+ *   - The caller owns all memory: cache pools, block tables, outputs and workspaces.  The
+ *     library allocates nothing and holds no device state between calls.
+ *   - Scalars are validated on the host before any launch.  Device data (block ids, lengths,
+ *     token ids) is trusted for correctness but clamped for memory safety: an inconsistent
+ *     value gives an unspecified result, never an access outside the buffers described here.
+ *   - Return codes: SPEXIS_OK, or a negative code with a message in spexis_last_error().
+ *   - Calls on one stream run in order; calls that share a workspace or an output and run
+ *     concurrently on different streams race.
+ *
+ * Batch description (append, attention)
+ *   num_seqs        B, sequences in the step
+ *   query_start_loc [B+1] int32: sequence b owns query rows qsl[b] .. qsl[b+1]-1;
+ *                   n_b = qsl[b+1]-qsl[b] = k_b + 1 >= 1, qsl[0] = 0, qsl[B] = total_tokens
+ *   seq_lens        [B] int32: S_b, tokens of sequence b in the cache AFTER the append;
+ *                   L_b = S_b - n_b are the tokens cached before this step
+ *   block_tables    [B][max_blocks_per_seq] int32 physical block ids; token t of sequence b
+ *                   lives in block block_tables[b][t / block_size], slot t % block_size
+ *   total_tokens    host: T = qsl[B], rows of q / out / new_k / new_v
+ *   max_query_len   host: >= max_b n_b
+ *
+ * Paged cache layout (bf16, one pool for K and one for V, num_blocks blocks each)
+ *   K pool  [num_blocks][Hkv][D/8][block_size][8]
+ *           element (blk, h, slot, d) at ((((blk*Hkv + h)*(D/8) + d/8)*bs + slot)*8 + d%8)
+ *   V pool  [num_blocks][Hkv][D][block_size], slot index stored with bits 2 and 3 swapped
+ *           element (blk, h, slot, d) at (((blk*Hkv + h)*D + d)*bs + swap23(slot)),
+ *           swap23(s) = (s & ~12) | ((s >> 2 & 1) << 3) | ((s >> 3 & 1) << 2)
+ *   Each (block, head) is one contiguous 4 KB (bs 16) or 8 KB (bs 32) chunk of each pool.
+ *   The layout lets the attention kernel load both matrix-core operands straight from HBM
+ *   with fully coalesced 16-byte loads (K: eight head-dim values of one slot; V: eight
+ *   slots of one head-dim index, in the order the score tile produces them).
+ */
+#ifndef SPEXIS_H
+#define SPEXIS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPEXIS_VERSION 100
+
+#define SPEXIS_OK 0
+#define SPEXIS_ERR_INVALID_ARGUMENT (-1)  /* null pointer, non-positive size, Hq % Hkv != 0 ... */
+#define SPEXIS_ERR_UNSUPPORTED (-2)       /* a shape outside the supported set (see each call) */
+#define SPEXIS_ERR_WORKSPACE_TOO_SMALL (-3)
+#define SPEXIS_ERR_HIP (-4)               /* a HIP launch failed; message has hipGetErrorString */
+
+/* row_status codes written by spexis_accept */
+#define SPEXIS_ROW_OK 0
+#define SPEXIS_ROW_EMPTY 1      /* the sampled row had no positive weight, even after fallback */
+#define SPEXIS_ROW_BAD_VALUE 2  /* the sampled row held a NaN, an infinity or a negative value */
+#define SPEXIS_ROW_BAD_TOKEN 3  /* a draft token id outside [0, vocab) */
+
+/* input kinds of spexis_accept */
+#define SPEXIS_INPUT_PROBS 0
+#define SPEXIS_INPUT_LOGITS 1
+
+/* Library version (SPEXIS_VERSION). */
+int spexis_version(void);
+
+/* Message of the last failed call on this host thread ("" if none).  Host memory owned by
+ * the library, valid until the next call on the same thread. */
+const char* spexis_last_error(void);
+
+/*
+ * spexis_append_kv -- write the n_b = k_b + 1 new K/V rows of every sequence into the cache.
+ *
+ * Defined by the shared-cache design of speculative-parallel execution (Sec. 4): verified
+ * and speculative tokens live in one paged cache, so a step's rows go to positions
+ * L_b .. S_b-1 of their sequence, overwriting whatever a rejected speculation left there.
+ * For every b, j < n_b and KV head h: token position L_b + j receives
+ * new_k[qsl[b]+j][h][:] and new_v[qsl[b]+j][h][:].  Nothing else in the pools changes.
+ *
+ *   k_cache, v_cache   bf16 pools in the layout above (written)
+ *   num_blocks         blocks per pool; num_kv_heads Hkv >= 1; block_size in {16, 32};
+ *                      head_dim in {64, 128}
+ *   new_k, new_v       [total_tokens][Hkv][head_dim] bf16, row-major (read)
+ * Errors: INVALID_ARGUMENT for null pointers or non-positive sizes; UNSUPPORTED for other
+ * block sizes or head dims.
+ */
+int spexis_append_kv(void* k_cache, void* v_cache, int32_t num_blocks, int32_t num_kv_heads,
+                     int32_t block_size, int32_t head_dim, int32_t num_seqs,
+                     const int32_t* query_start_loc, const int32_t* seq_lens,
+                     const int32_t* block_tables, int32_t max_blocks_per_seq,
+                     int32_t total_tokens, int32_t max_query_len, const void* new_k,
+                     const void* new_v, void* stream);
+
+/*
+ * Bytes of workspace spexis_verify_attention needs for these host-side bounds (0 when no
+ * sequence is split across KV chunks).  kv_chunk_tokens as in spexis_verify_attention.
+ */
+size_t spexis_verify_attention_workspace_size(int32_t num_seqs, int32_t num_q_heads,
+                                              int32_t num_kv_heads, int32_t head_dim,
+                                              int32_t max_query_len, int32_t max_seq_len,
+                                              int32_t kv_chunk_tokens);
+
+/*
+ * spexis_verify_attention -- the target model's joint verification pass over the drafts
+ * (Sec. 4: drafts are verified together by the full model; Related Work: the base model
+ * verifies the draft model's tokens in parallel).
+ *
+ * For every b, query token j < n_b and query head h, with G = Hq/Hkv and g = h / G:
+ *   out[qsl[b]+j][h][:] = sum_{t <= L_b + j} softmax_t(scale * <q[qsl[b]+j][h], k[b,t,g]>)
+ *                         * v[b,t,g][:]
+ * i.e. a query token sees the cached prefix and itself but not later drafts.  bf16 inputs,
+ * fp32 accumulation, bf16 output.
+ *
+ *   q       [total_tokens][Hq][head_dim] bf16 (read);  out: same shape, bf16 (written;
+ *           must not alias q)
+ *   scale   softmax scale, usually 1/sqrt(head_dim)
+ *   max_seq_len      host: >= max_b S_b, and S_b <= max_blocks_per_seq * block_size
+ *   kv_chunk_tokens  host: KV tokens per work item when a sequence is split across
+ *                    workgroups (0 = automatic; otherwise rounded up to a multiple of 32)
+ *   workspace        fp32 partials, >= spexis_verify_attention_workspace_size(...) bytes
+ * Supported: head_dim in {64, 128}, block_size in {16, 32}, (Hq/Hkv) * max_query_len <= 64.
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED, WORKSPACE_TOO_SMALL, HIP.
+ */
+int spexis_verify_attention(const void* k_cache, const void* v_cache, int32_t num_blocks,
+                            int32_t num_kv_heads, int32_t block_size, int32_t head_dim,
+                            int32_t num_seqs, const int32_t* query_start_loc,
+                            const int32_t* seq_lens, const int32_t* block_tables,
+                            int32_t max_blocks_per_seq, int32_t total_tokens,
+                            int32_t max_query_len, int32_t max_seq_len, const void* q,
+                            int32_t num_q_heads, float scale, void* out,
+                            int32_t kv_chunk_tokens, void* workspace, size_t workspace_bytes,
+                            void* stream);
+
+/*
+ * spexis_softmax_rows -- probs[r][v] = exp((logits[r][v] - max_u logits[r][u]) / T) /
+ * sum_u exp(...), fp32, for rows r < rows (the temperature divides the logits of target and
+ * draft rows alike).  logits and probs are [rows][vocab] fp32 and may alias.
+ * Errors: INVALID_ARGUMENT (null, rows < 0, vocab <= 0, temperature <= 0 or not finite).
+ */
+int spexis_softmax_rows(const float* logits, float* probs, int64_t rows, int32_t vocab,
+                        float temperature, void* stream);
+
+/* Bytes of workspace spexis_accept needs. */
+size_t spexis_accept_workspace_size(int32_t num_seqs, int32_t vocab, int32_t max_k);
+
+/*
+ * spexis_accept -- speculative-sampling acceptance, the rule of [sd] (Related Work) that
+ * decides how many drafts survive verification (Sec. 4, Fig. 3: accepted tokens continue,
+ * rejected ones are re-executed).
+ *
+ * Sequence b has k_b = qsl[b+1]-qsl[b]-1 drafts x_i = draft_ids[qsl[b]-b+i].  Its target
+ * rows are target[qsl[b]+i] (i = 0..k_b), its draft rows draft[qsl[b]-b+i] (i < k_b).
+ * kind = SPEXIS_INPUT_PROBS: rows are fp32 probabilities p_i, q_i.
+ * kind = SPEXIS_INPUT_LOGITS: rows are fp32 logits; p_i = softmax(target_i / T) and
+ *        q_i = softmax(draft_i / T) are formed on the fly (temperature > 0).
+ * For every b:
+ *   1. any x_i outside [0, vocab): row_status = BAD_TOKEN, accepted_len = 0, tokens -1.
+ *   2. draft i is accepted iff (double)u_accept[qsl[b]-b+i] * (double)q_i(x_i)
+ *      < (double)p_i(x_i), an exact comparison equal to u < min(1, p/q) for u in [0,1);
+ *      a_b = number of leading accepts.
+ *   3. a_b < k_b: weights w = max(0, fp32(p_a - q_a)), falling back to w = p_a if all are
+ *      zero; a_b = k_b: w = p_k (bonus).  Rows read here must be finite and >= 0, else
+ *      row_status = BAD_VALUE and the token at position a_b is -1.
+ *   4. the token at position a_b is the inverse-CDF sample of w with u_sample[b], taken in
+ *      exact fixed point: M = max w in [2^e, 2^(e+1)), W_v = floor(w_v * 2^(40-e)),
+ *      S = sum W_v, t = floor(u_sample[b] * S) (exact), token = smallest m with
+ *      W_0 + ... + W_m > t.  No positive weight: row_status = EMPTY, token -1.
+ * Outputs: accepted_len[b] = a_b; out_tokens[b][0..a_b) = x_0..x_{a_b-1};
+ *   out_tokens[b][a_b] = the sampled token; out_tokens[b][i > a_b] = -1 (out_tokens is
+ *   [B][max_k+1] int32); row_status[b]; if seq_lens_inout != NULL,
+ *   seq_lens_inout[b] -= k_b - a_b (rows of rejected drafts become stale), except for
+ *   BAD_TOKEN rows.
+ *
+ *   total_tokens  host: T = qsl[B]; target has T rows, draft T - B rows of `vocab` fp32
+ *   max_k         host: >= max_b k_b, <= 32
+ *   u_accept      [T-B] fp32, u_sample [B] fp32, in [0,1)
+ *   workspace     >= spexis_accept_workspace_size(num_seqs, vocab, max_k) bytes
+ * Supported: vocab <= 4194304.  Errors: INVALID_ARGUMENT, UNSUPPORTED,
+ * WORKSPACE_TOO_SMALL, HIP.
+ */
+int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k,
+                  float temperature, int32_t total_tokens, const int32_t* query_start_loc,
+                  const float* target, const float* draft, const int32_t* draft_ids,
+                  const float* u_accept, const float* u_sample, int32_t* accepted_len,
+                  int32_t* out_tokens, int32_t* row_status, int32_t* seq_lens_inout,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPEXIS_H */

@@ -1,0 +1,270 @@
+// extern "C" entry points of libspexis: host-side validation of scalar arguments, workspace
+// carving and kernel launches on the caller's stream.  No entry point allocates, frees or
+// synchronises.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "kernels.h"
+#include "spexis.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int ok() {
+  g_last_error.clear();
+  return SPEXIS_OK;
+}
+
+int hip_result(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(SPEXIS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+constexpr int kMaxChunks = 64;     // split-KV chunks per sequence (merge kernel's LDS table)
+constexpr int kMaxRows = 64;       // query rows per (sequence, KV head)
+constexpr int kMaxK = 32;
+constexpr int kMaxVocab = 1 << 22; // keeps sum W_v < 2^63 (W_v < 2^41)
+
+bool bad_cache_shape(int32_t bs, int32_t d) { return !((bs == 16 || bs == 32) && (d == 64 || d == 128)); }
+
+// KV tokens per split-KV work item and the number of items per sequence.
+void attn_chunking(int32_t max_seq_len, int32_t req, int* chunk, int* nch) {
+  int64_t c = req > 0 ? round_up(req, 32) : std::max<int64_t>(512, round_up((max_seq_len + 15) / 16, 32));
+  int64_t n = (max_seq_len + c - 1) / c;
+  if (n > kMaxChunks) {
+    c = round_up((max_seq_len + kMaxChunks - 1) / kMaxChunks, 32);
+    n = (max_seq_len + c - 1) / c;
+  }
+  *chunk = (int)c;
+  *nch = (int)std::max<int64_t>(n, 1);
+}
+
+struct AcceptLayout {
+  size_t st_a, st_mode, ctr, counts, lists, lse, row_stats, max_part, bad_part, sum_part, total;
+};
+
+int64_t accept_nsub(int64_t V) { return (V + spexis::kAcceptSub - 1) / spexis::kAcceptSub; }
+
+AcceptLayout accept_layout(int64_t B, int64_t V, int64_t max_k) {
+  const int64_t ns = accept_nsub(V);
+  AcceptLayout l{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off += (size_t)round_up((int64_t)bytes, 256);
+    return at;
+  };
+  l.st_a = take(B * 4);
+  l.st_mode = take(B * 4);
+  l.ctr = take(B * 4);
+  l.counts = take((max_k + 2) * 4);
+  l.lists = take((max_k + 1) * B * 4);
+  l.lse = take(2 * B * ns * 2 * 4);
+  l.row_stats = take(B * (max_k + 1) * 4 * 4);
+  l.max_part = take(B * ns * 2 * 4);
+  l.bad_part = take(B * ns * 4);
+  l.sum_part = take(B * ns * 8);
+  l.total = off;
+  return l;
+}
+
+}  // namespace
+
+extern "C" {
+
+int spexis_version(void) { return SPEXIS_VERSION; }
+
+const char* spexis_last_error(void) { return g_last_error.c_str(); }
+
+int spexis_append_kv(void* k_cache, void* v_cache, int32_t num_blocks, int32_t num_kv_heads,
+                     int32_t block_size, int32_t head_dim, int32_t num_seqs,
+                     const int32_t* query_start_loc, const int32_t* seq_lens,
+                     const int32_t* block_tables, int32_t max_blocks_per_seq,
+                     int32_t total_tokens, int32_t max_query_len, const void* new_k,
+                     const void* new_v, void* stream) {
+  if (!k_cache || !v_cache || !query_start_loc || !seq_lens || !block_tables || !new_k || !new_v)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_append_kv: null pointer");
+  if (num_blocks <= 0 || num_kv_heads <= 0 || num_seqs < 0 || max_blocks_per_seq <= 0 || total_tokens < 0 ||
+      max_query_len <= 0)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_append_kv: non-positive size");
+  if (bad_cache_shape(block_size, head_dim))
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_append_kv: block_size %d / head_dim %d not in {16,32} x {64,128}",
+                block_size, head_dim);
+  if (num_seqs == 0 || total_tokens == 0) return ok();
+  spexis::AppendParams p{k_cache, v_cache, query_start_loc, seq_lens, block_tables, new_k, new_v,
+                         num_blocks, num_kv_heads, block_size, head_dim, num_seqs, max_blocks_per_seq,
+                         total_tokens};
+  return hip_result(spexis::launch_append(p, (hipStream_t)stream), "spexis_append_kv");
+}
+
+size_t spexis_verify_attention_workspace_size(int32_t num_seqs, int32_t num_q_heads, int32_t num_kv_heads,
+                                              int32_t head_dim, int32_t max_query_len, int32_t max_seq_len,
+                                              int32_t kv_chunk_tokens) {
+  if (num_seqs <= 0 || num_kv_heads <= 0 || num_q_heads <= 0 || max_query_len <= 0 || max_seq_len <= 0)
+    return 0;
+  int chunk, nch;
+  attn_chunking(max_seq_len, kv_chunk_tokens, &chunk, &nch);
+  if (nch <= 1) return 0;
+  const int rmax = (num_q_heads / num_kv_heads) * max_query_len;
+  return (size_t)num_seqs * num_kv_heads * nch * spexis::attn_slot_floats(rmax, head_dim) * sizeof(float);
+}
+
+int spexis_verify_attention(const void* k_cache, const void* v_cache, int32_t num_blocks,
+                            int32_t num_kv_heads, int32_t block_size, int32_t head_dim,
+                            int32_t num_seqs, const int32_t* query_start_loc,
+                            const int32_t* seq_lens, const int32_t* block_tables,
+                            int32_t max_blocks_per_seq, int32_t total_tokens,
+                            int32_t max_query_len, int32_t max_seq_len, const void* q,
+                            int32_t num_q_heads, float scale, void* out,
+                            int32_t kv_chunk_tokens, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  if (!k_cache || !v_cache || !query_start_loc || !seq_lens || !block_tables || !q || !out)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: null pointer");
+  if (num_blocks <= 0 || num_kv_heads <= 0 || num_q_heads <= 0 || num_seqs < 0 || max_blocks_per_seq <= 0 ||
+      total_tokens < 0 || max_query_len <= 0 || max_seq_len <= 0 || kv_chunk_tokens < 0)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: non-positive size");
+  if (num_q_heads % num_kv_heads != 0)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: %d query heads not a multiple of %d KV heads",
+                num_q_heads, num_kv_heads);
+  if (!std::isfinite(scale)) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: scale not finite");
+  if (q == out) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: out aliases q");
+  if (bad_cache_shape(block_size, head_dim))
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_verify_attention: block_size %d / head_dim %d not in {16,32} x {64,128}",
+                block_size, head_dim);
+  const int group = num_q_heads / num_kv_heads;
+  if ((int64_t)group * max_query_len > kMaxRows)
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_verify_attention: (Hq/Hkv)*max_query_len = %d > %d",
+                group * max_query_len, kMaxRows);
+  if ((int64_t)max_blocks_per_seq * block_size < max_query_len)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: block tables hold fewer slots than a query");
+  if (num_seqs == 0 || total_tokens == 0) return ok();
+  int chunk, nch;
+  attn_chunking(max_seq_len, kv_chunk_tokens, &chunk, &nch);
+  const size_t need = spexis_verify_attention_workspace_size(num_seqs, num_q_heads, num_kv_heads, head_dim,
+                                                             max_query_len, max_seq_len, kv_chunk_tokens);
+  if (need > 0 && (!workspace || workspace_bytes < need))
+    return fail(SPEXIS_ERR_WORKSPACE_TOO_SMALL, "spexis_verify_attention: workspace %zu bytes < %zu needed",
+                workspace_bytes, need);
+  if ((int64_t)nch * num_seqs * num_kv_heads >= (1ll << 31))
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_verify_attention: grid too large");
+  spexis::AttnParams p{};
+  p.k_cache = k_cache;
+  p.v_cache = v_cache;
+  p.qsl = query_start_loc;
+  p.seq_lens = seq_lens;
+  p.block_tables = block_tables;
+  p.q = q;
+  p.out = out;
+  p.ws = static_cast<float*>(workspace);
+  p.num_blocks = num_blocks;
+  p.hkv = num_kv_heads;
+  p.block_size = block_size;
+  p.head_dim = head_dim;
+  p.num_seqs = num_seqs;
+  p.max_blocks = max_blocks_per_seq;
+  p.total_tokens = total_tokens;
+  p.hq = num_q_heads;
+  p.group = group;
+  p.rmax = group * max_query_len;
+  p.chunk = chunk;
+  p.nch_max = nch;
+  p.scale_log2e = (float)((double)scale * 1.4426950408889634);
+  return hip_result(spexis::launch_attention(p, (hipStream_t)stream), "spexis_verify_attention");
+}
+
+int spexis_softmax_rows(const float* logits, float* probs, int64_t rows, int32_t vocab, float temperature,
+                        void* stream) {
+  if (!logits || !probs) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_softmax_rows: null pointer");
+  if (rows < 0 || vocab <= 0) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_softmax_rows: bad size");
+  if (!(temperature > 0.f) || !std::isfinite(temperature))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_softmax_rows: temperature must be finite and > 0");
+  if (rows >= (1ll << 31)) return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_softmax_rows: too many rows");
+  const float c = (float)(1.4426950408889634 / (double)temperature);
+  return hip_result(spexis::launch_softmax(logits, probs, rows, vocab, c, (hipStream_t)stream),
+                    "spexis_softmax_rows");
+}
+
+size_t spexis_accept_workspace_size(int32_t num_seqs, int32_t vocab, int32_t max_k) {
+  if (num_seqs <= 0 || vocab <= 0 || max_k < 0) return 0;
+  return accept_layout(num_seqs, vocab, max_k).total;
+}
+
+int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, float temperature,
+                  int32_t total_tokens, const int32_t* query_start_loc, const float* target, const float* draft,
+                  const int32_t* draft_ids, const float* u_accept, const float* u_sample, int32_t* accepted_len,
+                  int32_t* out_tokens, int32_t* row_status, int32_t* seq_lens_inout, void* workspace,
+                  size_t workspace_bytes, void* stream) {
+  if (kind != SPEXIS_INPUT_PROBS && kind != SPEXIS_INPUT_LOGITS)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept: kind %d is neither PROBS nor LOGITS", kind);
+  if (num_seqs < 0 || vocab <= 0 || max_k < 0 || total_tokens < num_seqs)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept: bad size");
+  const bool has_drafts = total_tokens > num_seqs;
+  if (!query_start_loc || !target || !u_sample || !accepted_len || !out_tokens || !row_status ||
+      (has_drafts && (!draft || !draft_ids || !u_accept)))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept: null pointer");
+  if (kind == SPEXIS_INPUT_LOGITS && (!(temperature > 0.f) || !std::isfinite(temperature)))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept: temperature must be finite and > 0 for logits");
+  if (max_k > kMaxK) return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_accept: max_k %d > %d", max_k, kMaxK);
+  if (vocab > kMaxVocab) return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_accept: vocab %d > %d", vocab, kMaxVocab);
+  if (num_seqs == 0) return ok();
+  const AcceptLayout lay = accept_layout(num_seqs, vocab, max_k);
+  if (!workspace || workspace_bytes < lay.total)
+    return fail(SPEXIS_ERR_WORKSPACE_TOO_SMALL, "spexis_accept: workspace %zu bytes < %zu needed", workspace_bytes,
+                lay.total);
+  const int64_t nsub = accept_nsub(vocab);
+  const int64_t ipr = (nsub + spexis::kSubPerItem - 1) / spexis::kSubPerItem;
+  if ((int64_t)num_seqs * ipr * 2 >= (1ll << 31))
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_accept: grid too large");
+  char* ws = static_cast<char*>(workspace);
+  spexis::AcceptParams p{};
+  p.kind = kind;
+  p.B = num_seqs;
+  p.V = vocab;
+  p.max_k = max_k;
+  p.T = total_tokens;
+  p.nsub = (int)nsub;
+  p.ipr = (int)ipr;
+  p.c = kind == SPEXIS_INPUT_LOGITS ? (float)(1.4426950408889634 / (double)temperature) : 1.f;
+  p.qsl = query_start_loc;
+  p.target = target;
+  p.draft = draft;
+  p.ids = draft_ids;
+  p.u_accept = u_accept;
+  p.u_sample = u_sample;
+  p.accepted_len = accepted_len;
+  p.out_tokens = out_tokens;
+  p.row_status = row_status;
+  p.seq_lens_inout = seq_lens_inout;
+  p.st_a = reinterpret_cast<int32_t*>(ws + lay.st_a);
+  p.st_mode = reinterpret_cast<int32_t*>(ws + lay.st_mode);
+  p.ctr = reinterpret_cast<int32_t*>(ws + lay.ctr);
+  p.counts = reinterpret_cast<int32_t*>(ws + lay.counts);
+  p.lists = reinterpret_cast<int32_t*>(ws + lay.lists);
+  p.lse_part = reinterpret_cast<float*>(ws + lay.lse);
+  p.row_stats = reinterpret_cast<float*>(ws + lay.row_stats);
+  p.max_part = reinterpret_cast<float*>(ws + lay.max_part);
+  p.bad_part = reinterpret_cast<int32_t*>(ws + lay.bad_part);
+  p.sum_part = reinterpret_cast<uint64_t*>(ws + lay.sum_part);
+  return hip_result(spexis::launch_accept(p, (hipStream_t)stream), "spexis_accept");
+}
+
+}  // extern "C"

@@ -1,0 +1,78 @@
+// Launch parameters and host-side launchers of the libspexis kernels (internal).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace spexis {
+
+struct AppendParams {
+  void* k_cache;
+  void* v_cache;
+  const int32_t* qsl;
+  const int32_t* seq_lens;
+  const int32_t* block_tables;
+  const void* new_k;
+  const void* new_v;
+  int num_blocks, hkv, block_size, head_dim, num_seqs, max_blocks, total_tokens;
+};
+
+struct AttnParams {
+  const void* k_cache;
+  const void* v_cache;
+  const int32_t* qsl;
+  const int32_t* seq_lens;
+  const int32_t* block_tables;
+  const void* q;
+  void* out;
+  float* ws;             // split-KV partials: [B*Hkv*nch_max][rmax][D] acc, then m and l
+  int num_blocks, hkv, block_size, head_dim, num_seqs, max_blocks, total_tokens;
+  int hq, group;         // Hq, G = Hq / Hkv
+  int rmax;              // G * max_query_len (rows per (sequence, KV head)), <= 64
+  int chunk;             // KV tokens per work item (multiple of 32)
+  int nch_max;           // chunks per sequence covered by the grid / workspace
+  float scale_log2e;     // scale * log2(e): scores live in the base-2 domain
+};
+
+// Workspace layout of the split-KV partials for one (sequence, KV head, chunk) slot.
+// Rounded up to 16 floats so that every slot starts 64-byte aligned.
+__host__ __device__ inline int64_t attn_slot_floats(int rmax, int D) { return ((int64_t)rmax * (D + 2) + 15) / 16 * 16; }
+
+struct AcceptParams {
+  int kind;              // 0 probs, 1 logits
+  int B, V, max_k, T;
+  int nsub;              // ceil(V / kAcceptSub): partial results are kept per sub-chunk
+  int ipr;               // ceil(nsub / kSubPerItem): work items per vocabulary row
+  float c;               // log2(e) / temperature (logits mode)
+  const int32_t* qsl;
+  const float* target;
+  const float* draft;
+  const int32_t* ids;
+  const float* u_accept;
+  const float* u_sample;
+  int32_t* accepted_len;
+  int32_t* out_tokens;
+  int32_t* row_status;
+  int32_t* seq_lens_inout;
+  // workspace views
+  int32_t* st_a;         // [B] accepted count so far / final a_b
+  int32_t* st_mode;      // [B] 0 testing, 1 residual, 2 bonus, 3 done (outputs written)
+  int32_t* ctr;          // [B] arrival counters (zeroed by the init kernel, reset by the last arrival)
+  int32_t* counts;       // [max_k+2] sequences still testing when round i starts (logits mode)
+  int32_t* lists;        // [max_k+1][B] those sequences (round 0 uses 0..B-1)
+  float* lse_part;       // [2][B][nsub][2] sub-chunk (max, sum of 2^(y-max)) of the current round
+  float* row_stats;      // [B][max_k+1][4] (M, Z) of target row i, then of draft row i
+  float* max_part;       // [B][nsub][2] (max w, max p)
+  int32_t* bad_part;     // [B][nsub]
+  uint64_t* sum_part;    // [B][nsub]
+};
+
+constexpr int kAcceptSub = 4096;     // vocab entries per partial result (one wave's share)
+constexpr int kSubPerItem = 8;       // sub-chunks per work item (two per wave of a workgroup)
+
+hipError_t launch_append(const AppendParams& p, hipStream_t s);
+hipError_t launch_attention(const AttnParams& p, hipStream_t s);
+hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V, float c, hipStream_t s);
+hipError_t launch_accept(const AcceptParams& p, hipStream_t s);
+
+}  // namespace spexis

@@ -1,0 +1,150 @@
+"""Python binding of libspexis: the C entry points under the same names, taking torch tensors.
+
+Argument marshalling only -- every step runs in the HIP kernels of libspexis.so.  Tensors must
+live on the GPU (torch's ``cuda`` device on ROCm); the calls are asynchronous on the given
+stream (default: torch's current stream).  There is no CPU fallback: without the built
+library every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libspexis.so")
+HEADER = os.path.join(os.path.dirname(_PKG), "include", "spexis.h")
+
+SPEXIS_OK = 0
+SPEXIS_ERR_INVALID_ARGUMENT = -1
+SPEXIS_ERR_UNSUPPORTED = -2
+SPEXIS_ERR_WORKSPACE_TOO_SMALL = -3
+SPEXIS_ERR_HIP = -4
+SPEXIS_INPUT_PROBS = 0
+SPEXIS_INPUT_LOGITS = 1
+SPEXIS_ROW_OK, SPEXIS_ROW_EMPTY, SPEXIS_ROW_BAD_VALUE, SPEXIS_ROW_BAD_TOKEN = 0, 1, 2, 3
+
+
+class SpexisError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def header_functions() -> list:
+    """Names of the functions include/spexis.h declares."""
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(spexis_\w+)\s*\(", text, re.M)))
+
+
+def lib():
+    """The loaded libspexis.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                           "(the HIP path has no fallback)")
+    L = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+    L.spexis_version.argtypes, L.spexis_version.restype = [], ctypes.c_int
+    L.spexis_last_error.argtypes, L.spexis_last_error.restype = [], ctypes.c_char_p
+    L.spexis_append_kv.argtypes = [P, P, i32, i32, i32, i32, i32, P, P, P, i32, i32, i32, P, P, P]
+    L.spexis_append_kv.restype = ctypes.c_int
+    L.spexis_verify_attention_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32, i32]
+    L.spexis_verify_attention_workspace_size.restype = sz
+    L.spexis_verify_attention.argtypes = [P, P, i32, i32, i32, i32, i32, P, P, P, i32, i32, i32, i32, P, i32, f32,
+                                          P, i32, P, sz, P]
+    L.spexis_verify_attention.restype = ctypes.c_int
+    L.spexis_softmax_rows.argtypes = [P, P, i64, i32, f32, P]
+    L.spexis_softmax_rows.restype = ctypes.c_int
+    L.spexis_accept_workspace_size.argtypes = [i32, i32, i32]
+    L.spexis_accept_workspace_size.restype = sz
+    L.spexis_accept.argtypes = [i32, i32, i32, i32, f32, i32, P, P, P, P, P, P, P, P, P, P, P, sz, P]
+    L.spexis_accept.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(rc: int) -> None:
+    if rc != SPEXIS_OK:
+        raise SpexisError(rc, lib().spexis_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor], dtype=None):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensor must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"expected {dtype}, got {t.dtype}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def spexis_version() -> int:
+    return int(lib().spexis_version())
+
+
+def spexis_append_kv(k_cache, v_cache, num_blocks, num_kv_heads, block_size, head_dim, query_start_loc, seq_lens,
+                     block_tables, total_tokens, max_query_len, new_k, new_v, stream=None) -> None:
+    _check(lib().spexis_append_kv(
+        _ptr(k_cache, torch.bfloat16), _ptr(v_cache, torch.bfloat16), num_blocks, num_kv_heads, block_size,
+        head_dim, query_start_loc.shape[0] - 1, _ptr(query_start_loc, torch.int32), _ptr(seq_lens, torch.int32),
+        _ptr(block_tables, torch.int32), block_tables.shape[1], total_tokens, max_query_len,
+        _ptr(new_k, torch.bfloat16), _ptr(new_v, torch.bfloat16), _stream(stream)))
+
+
+def spexis_verify_attention_workspace_size(num_seqs, num_q_heads, num_kv_heads, head_dim, max_query_len, max_seq_len,
+                                           kv_chunk_tokens=0) -> int:
+    return int(lib().spexis_verify_attention_workspace_size(num_seqs, num_q_heads, num_kv_heads, head_dim,
+                                                            max_query_len, max_seq_len, kv_chunk_tokens))
+
+
+def spexis_verify_attention(k_cache, v_cache, num_blocks, num_kv_heads, block_size, head_dim, query_start_loc,
+                            seq_lens, block_tables, total_tokens, max_query_len, max_seq_len, q, num_q_heads, scale,
+                            out, workspace=None, kv_chunk_tokens=0, stream=None) -> None:
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().spexis_verify_attention(
+        _ptr(k_cache, torch.bfloat16), _ptr(v_cache, torch.bfloat16), num_blocks, num_kv_heads, block_size,
+        head_dim, query_start_loc.shape[0] - 1, _ptr(query_start_loc, torch.int32), _ptr(seq_lens, torch.int32),
+        _ptr(block_tables, torch.int32), block_tables.shape[1], total_tokens, max_query_len, max_seq_len,
+        _ptr(q, torch.bfloat16), num_q_heads, ctypes.c_float(scale), _ptr(out, torch.bfloat16), kv_chunk_tokens,
+        _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def spexis_softmax_rows(logits, probs, temperature=1.0, stream=None) -> None:
+    rows, vocab = logits.shape
+    _check(lib().spexis_softmax_rows(_ptr(logits, torch.float32), _ptr(probs, torch.float32), rows, vocab,
+                                     ctypes.c_float(temperature), _stream(stream)))
+
+
+def spexis_accept_workspace_size(num_seqs, vocab, max_k) -> int:
+    return int(lib().spexis_accept_workspace_size(num_seqs, vocab, max_k))
+
+
+def spexis_accept(kind, query_start_loc, target, draft, draft_ids, u_accept, u_sample, max_k, accepted_len,
+                  out_tokens, row_status, workspace, temperature=1.0, seq_lens_inout=None, stream=None) -> None:
+    num_seqs = query_start_loc.shape[0] - 1
+    total_tokens, vocab = target.shape
+    ws_bytes = workspace.numel() * workspace.element_size()
+    nd = total_tokens - num_seqs
+    _check(lib().spexis_accept(
+        kind, num_seqs, vocab, max_k, ctypes.c_float(temperature), total_tokens, _ptr(query_start_loc, torch.int32),
+        _ptr(target, torch.float32), _ptr(draft, torch.float32) if nd > 0 else None,
+        _ptr(draft_ids, torch.int32) if nd > 0 else None, _ptr(u_accept, torch.float32) if nd > 0 else None,
+        _ptr(u_sample, torch.float32), _ptr(accepted_len, torch.int32), _ptr(out_tokens, torch.int32),
+        _ptr(row_status, torch.int32), _ptr(seq_lens_inout, torch.int32), _ptr(workspace), ws_bytes,
+        _stream(stream)))

@@ -1,0 +1,109 @@
+"""The C-ABI library loads, exports every function include/spexis.h declares, and rejects
+bad scalar arguments on the host with the documented codes (no GPU needed: validation
+returns before any device call)."""
+import ctypes
+import os
+import subprocess
+
+import pytest
+import torch
+
+from paper_2609_34370_amd import spexis as sx
+
+pytestmark = pytest.mark.skipif(not os.path.exists(sx.LIB_PATH), reason="libspexis.so not built")
+
+# Never dereferenced: every call that passes FAKE fails host validation before any launch.
+# As a second guard these calls only run where no GPU is visible.
+FAKE = ctypes.c_void_p(256)
+no_gpu = pytest.mark.skipif(torch.cuda.is_available(), reason="fake-pointer validation runs only without a GPU")
+
+
+def test_every_header_function_is_exported():
+    declared = sx.header_functions()
+    assert {"spexis_append_kv", "spexis_verify_attention", "spexis_accept"} <= set(declared)
+    out = subprocess.run(["nm", "-D", "--defined-only", sx.LIB_PATH], capture_output=True, text=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    missing = [f for f in declared if f not in exported]
+    assert not missing, missing
+    L = sx.lib()
+    for f in declared:
+        assert hasattr(L, f)
+
+
+@no_gpu
+def test_version_and_last_error():
+    assert sx.spexis_version() == 100
+    L = sx.lib()
+    assert L.spexis_append_kv(None, None, 1, 1, 16, 64, 1, None, None, None, 1, 1, 1, None, None, None) == \
+        sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert b"null pointer" in L.spexis_last_error()
+
+
+def attn(**kw):
+    a = dict(k=FAKE, v=FAKE, nb=10, hkv=2, bs=16, d=64, B=2, qsl=FAKE, sl=FAKE, bt=FAKE, mb=4, T=4, mq=2, ms=40,
+             q=FAKE, hq=8, scale=0.125, out=ctypes.c_void_p(512), chunk=0, ws=None, wsb=0)
+    a.update(kw)
+    return sx.lib().spexis_verify_attention(a["k"], a["v"], a["nb"], a["hkv"], a["bs"], a["d"], a["B"], a["qsl"],
+                                            a["sl"], a["bt"], a["mb"], a["T"], a["mq"], a["ms"], a["q"], a["hq"],
+                                            ctypes.c_float(a["scale"]), a["out"], a["chunk"], a["ws"], a["wsb"],
+                                            None)
+
+
+@no_gpu
+def test_attention_validation():
+    assert attn(hq=7) == sx.SPEXIS_ERR_INVALID_ARGUMENT          # Hq not a multiple of Hkv
+    assert attn(d=96) == sx.SPEXIS_ERR_UNSUPPORTED
+    assert attn(bs=8) == sx.SPEXIS_ERR_UNSUPPORTED
+    assert attn(hq=66, hkv=2, mq=3) == sx.SPEXIS_ERR_UNSUPPORTED  # G = 33, 99 rows
+    assert attn(out=FAKE) == sx.SPEXIS_ERR_INVALID_ARGUMENT       # out aliases q
+    assert attn(scale=float("nan")) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert attn(ms=4000, chunk=32) == sx.SPEXIS_ERR_WORKSPACE_TOO_SMALL
+    assert b"workspace" in sx.lib().spexis_last_error()
+
+
+def test_workspace_queries():
+    # no split -> no workspace
+    assert sx.spexis_verify_attention_workspace_size(4, 8, 2, 64, 5, 256, 0) == 0
+    n = sx.spexis_verify_attention_workspace_size(64, 32, 8, 128, 5, 4100, 0)
+    assert n > 0 and n % 64 == 0
+    assert sx.spexis_accept_workspace_size(64, 128256, 4) > 64 * 32 * 8
+
+
+def acc(**kw):
+    a = dict(kind=1, B=2, V=100, mk=2, t=1.0, T=6, qsl=FAKE, tg=FAKE, dr=FAKE, ids=FAKE, ua=FAKE, us=FAKE,
+             al=FAKE, ot=FAKE, rs=FAKE, sl=None, ws=FAKE, wsb=1 << 20)
+    a.update(kw)
+    return sx.lib().spexis_accept(a["kind"], a["B"], a["V"], a["mk"], ctypes.c_float(a["t"]), a["T"], a["qsl"],
+                                  a["tg"], a["dr"], a["ids"], a["ua"], a["us"], a["al"], a["ot"], a["rs"], a["sl"],
+                                  a["ws"], a["wsb"], None)
+
+
+@no_gpu
+def test_accept_validation():
+    assert acc(kind=5) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert acc(t=0.0) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert acc(t=-1.0) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert acc(dr=None) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert acc(mk=33) == sx.SPEXIS_ERR_UNSUPPORTED
+    assert acc(V=(1 << 22) + 1) == sx.SPEXIS_ERR_UNSUPPORTED
+    assert acc(wsb=16) == sx.SPEXIS_ERR_WORKSPACE_TOO_SMALL
+    assert acc(T=1) == sx.SPEXIS_ERR_INVALID_ARGUMENT            # fewer rows than sequences
+
+
+@no_gpu
+def test_softmax_validation():
+    L = sx.lib()
+    assert L.spexis_softmax_rows(FAKE, FAKE, 4, 10, ctypes.c_float(0.0), None) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert L.spexis_softmax_rows(FAKE, FAKE, -1, 10, ctypes.c_float(1.0), None) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert L.spexis_softmax_rows(None, FAKE, 4, 10, ctypes.c_float(1.0), None) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+
+
+@no_gpu
+def test_append_validation():
+    L = sx.lib()
+    assert L.spexis_append_kv(FAKE, FAKE, 10, 2, 8, 64, 2, FAKE, FAKE, FAKE, 4, 4, 2, FAKE, FAKE, None) == \
+        sx.SPEXIS_ERR_UNSUPPORTED
+    assert L.spexis_append_kv(FAKE, FAKE, 0, 2, 16, 64, 2, FAKE, FAKE, FAKE, 4, 4, 2, FAKE, FAKE, None) == \
+        sx.SPEXIS_ERR_INVALID_ARGUMENT
+    # nothing to do: no launch, success
+    assert L.spexis_append_kv(FAKE, FAKE, 10, 2, 16, 64, 0, FAKE, FAKE, FAKE, 4, 0, 2, FAKE, FAKE, None) == sx.SPEXIS_OK

@@ -1,0 +1,328 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle on the same seeded inputs.
+
+Bars: append bit-exact; attention |gpu - oracle| <= 1e-2 + 1e-2 |oracle| per element (bf16
+inputs, fp32 accumulation, bf16 output); softmax within 1e-5 absolute; acceptance (accepted
+lengths, emitted tokens, row status) bit-exact when both sides get identical fp32
+probabilities and uniforms.  The oracle's inputs are the generator's host copies, never
+anything the GPU computed.  Full-size workloads are checked on sampled sequences, chosen to
+include the longest context and the shortest/ragged cases.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_34370_amd import spexis as sx
+from paper_2609_34370_amd import workloads as wl
+from paper_2609_34370_amd.step import VerifyStep, bf16_to_u16
+
+pytestmark = pytest.mark.gpu
+
+ATOL = RTOL = 1e-2
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def case(wid, seed=None, accept=True, **over):
+    spec = wl.spec_with(wid, **over) if over else wl.WORKLOADS[wid]
+    batch = wl.make_batch(spec, seed=seed)
+    attn = wl.make_attention_inputs(spec, batch, device="cuda", seed=seed)
+    acc = wl.make_accept_inputs(spec, batch, device="cuda", seed=seed) if accept else None
+    return spec, batch, attn, acc
+
+
+def pick_seqs(batch, n, rng):
+    if batch.B <= n:
+        return np.arange(batch.B)
+    must = {int(np.argmax(batch.seq_lens)), int(np.argmin(batch.seq_lens)), int(np.argmax(batch.k)),
+            int(np.argmin(batch.k))}
+    rest = rng.choice(batch.B, size=n, replace=False)
+    return np.array(sorted(must | set(int(x) for x in rest)))[: max(n, len(must))]
+
+
+def oracle_pools_after_append(spec, batch, k0, v0, attn):
+    kp, vp = k0.copy(), v0.copy()
+    oracle.append_kv(kp, vp, batch.num_blocks, spec.num_kv_heads, spec.block_size, spec.head_dim, batch.qsl,
+                     batch.seq_lens, batch.block_tables, bf16_to_u16(attn.new_k), bf16_to_u16(attn.new_v))
+    return kp, vp
+
+
+def bf16_out_to_f64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+# ---------------------------------------------------------------------------- append
+
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
+def test_append_bit_exact(wid):
+    say(f"[append] workload {wid}")
+    spec, batch, attn, _ = case(wid, accept=False)
+    k0, v0 = bf16_to_u16(attn.k_pool), bf16_to_u16(attn.v_pool)
+    step = VerifyStep(batch, attn, None)
+    step.append()
+    torch.cuda.synchronize()
+    kp, vp = oracle_pools_after_append(spec, batch, k0, v0, attn)
+    assert np.array_equal(bf16_to_u16(attn.k_pool), kp)
+    assert np.array_equal(bf16_to_u16(attn.v_pool), vp)
+
+
+# ------------------------------------------------------------------------- attention
+
+def check_attention(wid, nseq, seed=None, kv_chunk_tokens=0, **over):
+    spec, batch, attn, _ = case(wid, seed=seed, accept=False, **over)
+    say(f"[attention] workload {wid} B={batch.B} T={batch.T} max_S={batch.max_seq_len} chunk={kv_chunk_tokens}")
+    k0, v0 = bf16_to_u16(attn.k_pool), bf16_to_u16(attn.v_pool)
+    step = VerifyStep(batch, attn, None, kv_chunk_tokens=kv_chunk_tokens)
+    step.append()
+    step.attention()
+    torch.cuda.synchronize()
+    got = bf16_out_to_f64(step.out)
+    kp, vp = oracle_pools_after_append(spec, batch, k0, v0, attn)
+    seqs = pick_seqs(batch, nseq, np.random.default_rng(wid))
+    ref = oracle.attention(kp, vp, batch.num_blocks, spec.num_kv_heads, spec.block_size, spec.head_dim, batch.qsl,
+                           batch.seq_lens, batch.block_tables, bf16_to_u16(attn.q), spec.num_q_heads,
+                           float(np.float32(step.scale)), seqs=seqs)
+    rows = np.concatenate([np.arange(batch.qsl[b], batch.qsl[b + 1]) for b in seqs])
+    err = np.abs(got[rows] - ref[rows])
+    bound = ATOL + RTOL * np.abs(ref[rows])
+    worst = float((err / bound).max())
+    say(f"  seqs={len(seqs)} max|err|={err.max():.3e} worst err/bound={worst:.3f}")
+    assert np.isfinite(got[rows]).all()
+    assert (err <= bound).all(), worst
+    return step, got
+
+
+@pytest.mark.parametrize("wid,nseq", [(1, 4), (2, 12), (3, 6), (4, 12), (5, 16)])
+def test_attention_matches_oracle(wid, nseq):
+    check_attention(wid, nseq)
+
+
+@pytest.mark.parametrize("chunk", [32, 96, 4096])
+def test_attention_split_kv_settings(chunk):
+    # many small chunks, an odd multiple of 32, and no split at all
+    check_attention(1, 4, seed=77, kv_chunk_tokens=chunk, batch=6, ctx=("uniform", 1, 300))
+
+
+def test_attention_short_contexts_and_tails():
+    # empty caches, contexts shorter than one tile, block-size-32 pools, k = 0 rows
+    check_attention(1, 8, seed=5, batch=8, ctx=("uniform", 0, 40), k=("uniform", 0, 6))
+    check_attention(5, 8, seed=6, batch=8, ctx=("uniform", 0, 70), k=("uniform", 0, 8))
+
+
+def test_attention_head_dim_64_block_32_and_wide_groups():
+    check_attention(1, 6, seed=8, batch=6, block_size=32, num_q_heads=16, num_kv_heads=2, k=("fixed", 7))
+
+
+def test_attention_block_permutation_invariance():
+    spec, batch, attn, _ = case(1, seed=9, accept=False, batch=5, ctx=("uniform", 40, 200))
+    step = VerifyStep(batch, attn, None)
+    step.append()
+    step.attention()
+    base = step.out.clone()
+    # move every physical block to a new id (whole (block, head) chunks are contiguous)
+    nb = batch.num_blocks
+    perm = torch.as_tensor(np.random.default_rng(3).permutation(nb), device="cuda")
+    blk = spec.num_kv_heads * spec.block_size * spec.head_dim
+    kp = torch.empty_like(attn.k_pool)
+    vp = torch.empty_like(attn.v_pool)
+    kp.view(nb, blk)[perm] = attn.k_pool.view(nb, blk)
+    vp.view(nb, blk)[perm] = attn.v_pool.view(nb, blk)
+    attn2 = wl.AttentionInputs(kp, vp, attn.q, attn.new_k, attn.new_v)
+    tables = perm.cpu().numpy()[batch.block_tables].astype(np.int32)
+    batch2 = wl.Batch(spec, batch.ctx_lens, batch.k, batch.qsl, batch.seq_lens, tables, nb)
+    step2 = VerifyStep(batch2, attn2, None)
+    step2.attention()
+    torch.cuda.synchronize()
+    assert torch.equal(base.view(torch.int16), step2.out.view(torch.int16))
+
+
+def test_attention_ignores_garbage_past_sequence_end():
+    # slots past S_b in a sequence's last block hold NaN: they must not leak into the output
+    spec, batch, attn, _ = case(1, seed=10, accept=False, batch=4, ctx=("uniform", 20, 90))
+    step = VerifyStep(batch, attn, None)
+    step.append()
+    step.attention()
+    clean = step.out.clone()
+    kp = bf16_to_u16(attn.k_pool).copy()
+    vp = bf16_to_u16(attn.v_pool).copy()
+    hkv, bs, D = spec.num_kv_heads, spec.block_size, spec.head_dim
+    from tests import layout_ref as lr
+    for b in range(batch.B):
+        S = int(batch.seq_lens[b])
+        last_blk = batch.block_tables[b, (S - 1) // bs]
+        for slot in range(S % bs or bs, bs):
+            for h in range(hkv):
+                d = np.arange(D)
+                kp[lr.k_offsets(last_blk, h, slot, d, hkv, bs, D)] = 0x7FC0   # bf16 NaN
+                vp[lr.v_offsets(last_blk, h, slot, d, hkv, bs, D)] = 0x7FC0
+    attn.k_pool.copy_(torch.as_tensor(kp.view(np.int16)).view(torch.bfloat16).cuda())
+    attn.v_pool.copy_(torch.as_tensor(vp.view(np.int16)).view(torch.bfloat16).cuda())
+    step.attention()
+    torch.cuda.synchronize()
+    assert torch.equal(clean.view(torch.int16), step.out.view(torch.int16))
+
+
+# --------------------------------------------------------------------------- softmax
+
+@pytest.mark.parametrize("wid", [1, 2, 4, 5])
+def test_softmax_matches_oracle(wid):
+    spec, batch, _, acc = case(wid, seed=None, batch=min(16, wl.WORKLOADS[wid].batch))
+    say(f"[softmax] workload {wid} rows={acc.target_logits.shape[0]} V={spec.vocab} T={acc.temperature}")
+    probs = torch.empty_like(acc.target_logits)
+    sx.spexis_softmax_rows(acc.target_logits, probs, acc.temperature)
+    torch.cuda.synchronize()
+    ref = oracle.softmax(acc.target_logits.cpu().numpy(), acc.temperature)
+    err = np.abs(probs.cpu().numpy() - ref).max()
+    say(f"  max|err|={err:.3e}")
+    assert err <= 1e-5
+
+
+def test_softmax_odd_vocab_and_masked_logits():
+    x = torch.randn((7, 1003), device="cuda") * 5
+    x[:, 17] = -float("inf")
+    p = torch.empty_like(x)
+    sx.spexis_softmax_rows(x, p, 0.9)
+    torch.cuda.synchronize()
+    ref = oracle.softmax(x.cpu().numpy(), 0.9)
+    assert np.abs(p.cpu().numpy() - ref).max() <= 1e-5
+    assert (p[:, 17] == 0).all()
+
+
+# ------------------------------------------------------------------------ acceptance
+
+def oracle_probs(acc):
+    return (oracle.softmax(acc.target_logits.cpu().numpy(), acc.temperature),
+            oracle.softmax(acc.draft_logits.cpu().numpy(), acc.temperature))
+
+
+def run_accept_probs(step, p_host, q_host, seq_lens=None):
+    acc = step.acc
+    tp = torch.as_tensor(p_host, device="cuda")
+    dq = torch.as_tensor(q_host, device="cuda")
+    sl = torch.as_tensor(seq_lens, device="cuda") if seq_lens is not None else None
+    step.accept(target=tp, draft=dq, kind=sx.SPEXIS_INPUT_PROBS, seq_lens_inout=sl)
+    torch.cuda.synchronize()
+    a, t, s = step.accept_outputs()
+    return a, t, s, (sl.cpu().numpy() if sl is not None else None)
+
+
+@pytest.mark.parametrize("wid,B", [(1, None), (2, None), (3, 64), (4, None), (5, 96)])
+def test_accept_probs_bit_exact(wid, B):
+    over = {} if B is None else {"batch": B}
+    spec, batch, attn, acc = case(wid, **over)
+    say(f"[accept probs] workload {wid} B={batch.B} V={spec.vocab} max_k={batch.max_k}")
+    p, q = oracle_probs(acc)
+    step = VerifyStep(batch, attn, acc)
+    a, t, s, sl = run_accept_probs(step, p, q, seq_lens=batch.seq_lens)
+    ra, rt, rs, rsl = oracle.accept(batch.qsl, p, q, acc.draft_ids.cpu().numpy(), acc.u_accept.cpu().numpy(),
+                                    acc.u_sample.cpu().numpy(), max_k=batch.max_k, seq_lens=batch.seq_lens)
+    say(f"  mean accepted={a.mean():.3f} emitted={int((a + 1).sum())}")
+    np.testing.assert_array_equal(a, ra)
+    np.testing.assert_array_equal(t, rt)
+    np.testing.assert_array_equal(s, rs)
+    np.testing.assert_array_equal(sl, rsl)
+
+
+def test_accept_identical_draft_accepts_all():
+    spec, batch, attn, acc = case(2, batch=32)
+    p, _ = oracle_probs(acc)
+    q = p[wl.draft_row_index(batch)]
+    rng = np.random.default_rng(1)
+    ids = np.array([rng.choice(q.shape[1], p=r / r.sum(dtype=np.float64)) for r in q.astype(np.float64)], np.int32)
+    acc.draft_ids.copy_(torch.as_tensor(ids))
+    step = VerifyStep(batch, attn, acc)
+    a, t, s, _ = run_accept_probs(step, p, q)
+    np.testing.assert_array_equal(a, batch.k)
+    assert (s == 0).all()
+
+
+def test_accept_status_codes_and_edge_rows():
+    V = 5000
+    qsl = np.array([0, 3, 6, 9, 10, 13], np.int32)      # k = 2, 2, 2, 0, 2
+    B = 5
+    rng = np.random.default_rng(2)
+    p = rng.random((13, V)).astype(np.float32)
+    p /= p.sum(1, keepdims=True)
+    q = rng.random((8, V)).astype(np.float32)
+    q /= q.sum(1, keepdims=True)
+    ids = rng.integers(0, V, 8).astype(np.int32)
+    ids[3] = V + 7                                      # seq 1: bad token id
+    p[6, ids[4]] = 0.0                                  # seq 2: rejects position 0 ...
+    p[6, 100] = np.nan                                  # ... and its residual row holds a NaN
+    p[9] = 0.0                                          # seq 3 (k = 0): an all-zero bonus row
+    q[6, :] = 0.0                                       # seq 4: a one-hot draft row
+    q[6, ids[6]] = 1.0
+    ua = rng.random(8, dtype=np.float32)
+    us = rng.random(B, dtype=np.float32)
+    ra, rt, rs, _ = oracle.accept(qsl, p, q, ids, ua, us, max_k=2)
+    assert list(rs[:4]) == [0, 3, 2, 1]
+    dev = lambda x: torch.as_tensor(x, device="cuda")
+    accepted = torch.empty(B, dtype=torch.int32, device="cuda")
+    toks = torch.empty((B, 3), dtype=torch.int32, device="cuda")
+    stat = torch.empty(B, dtype=torch.int32, device="cuda")
+    for kind in (sx.SPEXIS_INPUT_PROBS,):
+        ws = torch.empty(sx.spexis_accept_workspace_size(B, V, 2), dtype=torch.uint8, device="cuda")
+        sx.spexis_accept(kind, dev(qsl), dev(p), dev(q), dev(ids), dev(ua), dev(us), 2, accepted, toks, stat, ws)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(accepted.cpu().numpy(), ra)
+        np.testing.assert_array_equal(toks.cpu().numpy(), rt)
+        np.testing.assert_array_equal(stat.cpu().numpy(), rs)
+
+
+def borderline(p, q, ids, ua, us, qsl, b, a_o, t_o, a_g, t_g, tol=1e-4):
+    """True if a logits-mode disagreement sits within fp32 rounding of a decision boundary."""
+    t0, d0 = qsl[b], qsl[b] - b
+    if a_o != a_g:
+        i = min(a_o, a_g)
+        x = ids[d0 + i]
+        return abs(float(ua[d0 + i]) * float(q[d0 + i, x]) - float(p[t0 + i, x])) <= tol
+    k = qsl[b + 1] - qsl[b] - 1
+    a = a_o
+    w = np.maximum(p[t0 + a].astype(np.float64) - q[d0 + a], 0) if a < k else p[t0 + a].astype(np.float64)
+    cdf = np.cumsum(w) / w.sum()
+    m = min(t_o[a], t_g[a])
+    return abs(cdf[m] - float(us[b])) <= tol
+
+
+@pytest.mark.parametrize("wid,B", [(1, None), (2, None), (3, 64), (4, None), (5, 128)])
+def test_accept_logits_agrees_with_oracle(wid, B):
+    over = {} if B is None else {"batch": B}
+    spec, batch, attn, acc = case(wid, **over)
+    say(f"[accept logits] workload {wid} B={batch.B} V={spec.vocab} T={acc.temperature}")
+    step = VerifyStep(batch, attn, acc)
+    step.accept()
+    torch.cuda.synchronize()
+    a, t, s = step.accept_outputs()
+    p, q = oracle_probs(acc)
+    ids, ua, us = acc.draft_ids.cpu().numpy(), acc.u_accept.cpu().numpy(), acc.u_sample.cpu().numpy()
+    ra, rt, rs, _ = oracle.accept(batch.qsl, p, q, ids, ua, us, max_k=batch.max_k)
+    assert (s == 0).all() and (rs == 0).all()
+    diff = [b for b in range(batch.B) if a[b] != ra[b] or not np.array_equal(t[b], rt[b])]
+    say(f"  mean accepted={a.mean():.3f} disagreements={len(diff)}")
+    assert len(diff) <= max(1, batch.B // 100)
+    for b in diff:
+        assert borderline(p, q, ids, ua, us, batch.qsl, b, ra[b], rt[b], a[b], t[b]), b
+
+
+# -------------------------------------------------------------------------- boundary
+
+def test_boundary_errors_on_gpu():
+    spec, batch, attn, acc = case(1)
+    step = VerifyStep(batch, attn, acc, kv_chunk_tokens=32)
+    small = torch.empty(16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(sx.SpexisError) as e:
+        sx.spexis_verify_attention(attn.k_pool, attn.v_pool, batch.num_blocks, spec.num_kv_heads, spec.block_size,
+                                   spec.head_dim, step.qsl, step.seq_lens, step.tables, batch.T, batch.max_query_len,
+                                   batch.max_seq_len, attn.q, spec.num_q_heads, 0.125, step.out, small,
+                                   kv_chunk_tokens=32)
+    assert e.value.code == sx.SPEXIS_ERR_WORKSPACE_TOO_SMALL
+    with pytest.raises(sx.SpexisError) as e:
+        sx.spexis_accept(sx.SPEXIS_INPUT_LOGITS, step.qsl, acc.target_logits, acc.draft_logits, acc.draft_ids,
+                         acc.u_accept, acc.u_sample, batch.max_k, step.accepted_len, step.out_tokens,
+                         step.row_status, step.acc_ws, temperature=0.0)
+    assert e.value.code == sx.SPEXIS_ERR_INVALID_ARGUMENT
