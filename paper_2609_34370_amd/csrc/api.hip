@@ -48,11 +48,16 @@ bool bad_cache_shape(int32_t bs, int32_t d) { return !((bs == 16 || bs == 32) &&
 
 // KV tokens per split-KV work item and the number of items per sequence.
 void attn_chunking(int32_t max_seq_len, int32_t req, int* chunk, int* nch) {
-  int64_t c = req > 0 ? round_up(req, 32) : std::max<int64_t>(512, round_up((max_seq_len + 15) / 16, 32));
+  int64_t c = req > 0 ? round_up(req, 32) : std::max<int64_t>(1024, round_up((max_seq_len + 15) / 16, 32));
   int64_t n = (max_seq_len + c - 1) / c;
   if (n > kMaxChunks) {
     c = round_up((max_seq_len + kMaxChunks - 1) / kMaxChunks, 32);
     n = (max_seq_len + c - 1) / c;
+  }
+  if (c > 8192) c = 8192;   // the attention kernel stages one chunk's block ids in LDS
+  n = (max_seq_len + c - 1) / c;
+  if (n > kMaxChunks) {      // only for max_seq_len > 64 * 8192: the last chunk takes the rest
+    n = kMaxChunks;
   }
   *chunk = (int)c;
   *nch = (int)std::max<int64_t>(n, 1);

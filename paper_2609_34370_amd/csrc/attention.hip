@@ -26,9 +26,12 @@
 namespace spexis {
 
 constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" of the running maxima
+constexpr float kLazy = 8.0f;         // base-2 headroom before the running maximum moves
+constexpr int kMaxChunkBlocks = 512;  // block ids of one chunk staged in LDS (chunk <= 8192 tokens)
 
 template <int D, int BS, int NT>
-__global__ __launch_bounds__(256) void verify_attn_kernel(AttnParams p) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NT == 1 ? 2 : 1)))
+void verify_attn_kernel(AttnParams p) {
   constexpr int KS = D / 16;   // k-steps of the score product
   constexpr int MT = D / 32;   // 32-wide head-dim tiles of the output
   const int item = blockIdx.x;
@@ -57,12 +60,25 @@ __global__ __launch_bounds__(256) void verify_attn_kernel(AttnParams p) {
   const int ntiles = (t_end - t_begin + 31) >> 5;
 
   const int32_t* bt = p.block_tables + (int64_t)b * p.max_blocks;
+  // Block ids of the chunk, staged in LDS: tile addresses then never wait on a global load
+  // (which, counted in order with the K/V loads, would drain the prefetch pipeline).
+  __shared__ int sm_blk[kMaxChunkBlocks];
+  const int blk0 = t_begin / BS;
+  const int nblk = (t_end - 1) / BS - blk0 + 1;
+  for (int x = threadIdx.x; x < nblk && x < kMaxChunkBlocks; x += blockDim.x)
+    sm_blk[x] = clampi(bt[blk0 + x], 0, p.num_blocks - 1);
+  auto block_of = [&](int token) {
+    const int x = token / BS - blk0;
+    return x < kMaxChunkBlocks ? sm_blk[x] : clampi(bt[token / BS], 0, p.num_blocks - 1);
+  };
   const uint16_t* kc = reinterpret_cast<const uint16_t*>(p.k_cache);
   const uint16_t* vc = reinterpret_cast<const uint16_t*>(p.v_cache);
   const int64_t head_stride = (int64_t)BS * D;   // elements of one (block, head) chunk
 
-  // ---- query rows of this lane: row r = nt*32 + col is (token j, head g) with r = j*G + g
-  bf16x8 qop[NT][KS];
+  // ---- query rows of this lane: row r = nt*32 + col is (token j, head g) with r = j*G + g.
+  // The score product's B operand (Q) is the same for the four waves: wave 0 stages it in LDS
+  // in operand order, every wave reads it back per tile.
+  __shared__ u32x4 sm_q[NT][KS][kWave];
   int lim[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
@@ -70,11 +86,15 @@ __global__ __launch_bounds__(256) void verify_attn_kernel(AttnParams p) {
     const int j = r < R ? r / p.group : n - 1;    // padding rows repeat a real row
     const int g = r < R ? r % p.group : 0;
     lim[nt] = L + j;                              // keys 0..L+j are visible
-    const uint16_t* qrow = reinterpret_cast<const uint16_t*>(p.q) +
-                           ((int64_t)(q0 + j) * p.hq + kvh * p.group + g) * D + 8 * half;
+    if (wave == 0) {
+      const uint16_t* qrow = reinterpret_cast<const uint16_t*>(p.q) +
+                             ((int64_t)(q0 + j) * p.hq + kvh * p.group + g) * D + 8 * half;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) qop[nt][s] = as_bf16x8(ld16(qrow + 16 * s));
+      for (int s = 0; s < KS; ++s) sm_q[nt][s][lane] = ld16(qrow + 16 * s);
+    }
   }
+
+  __syncthreads();   // block ids and Q staged
 
   float m[NT], l[NT];
   f32x16 acc[NT][MT];
@@ -88,38 +108,40 @@ __global__ __launch_bounds__(256) void verify_attn_kernel(AttnParams p) {
       for (int i = 0; i < 16; ++i) acc[nt][mt][i] = 0.f;
   }
 
-  u32x4 kn[KS], vn[MT][2];   // operands of the next tile (prefetched)
-  auto load_tile = [&](int tile) {
-    const int t0 = t_begin + tile * 32;
+  // Operand buffers.  Tile i of this wave is chunk tile wave + 4 i; DEPTH buffers rotate so
+  // that DEPTH-1 tiles are in flight while one is computed.  Loads are issued unconditionally:
+  // an index past the wave's last tile re-reads that tile (an L2 hit), which keeps the number of
+  // outstanding loads the same on every path and lets the waits stay partial.
+  constexpr int DEPTH = 2;
+  struct Buf {
+    u32x4 k[KS];
+    u32x4 v[MT][2];
+  };
+  Buf buf[DEPTH];
+  const int cnt = ntiles > wave ? (ntiles - wave + 3) / 4 : 0;   // tiles of this wave
+
+  auto load_tile = [&](Buf& B, int i) {
+    const int t0 = t_begin + (wave + 4 * (i < cnt ? i : cnt - 1)) * 32;
     int tk = t0 + col;
     if (tk > S - 1) tk = S - 1;                   // past the end: any valid slot, masked later
-    const int kb = clampi(bt[tk / BS], 0, p.num_blocks - 1);
+    const int kb = block_of(tk);
     const uint16_t* kp = kc + ((int64_t)kb * p.hkv + kvh) * head_stride + (tk % BS) * 8 + half * BS * 8;
 #pragma unroll
-    for (int s = 0; s < KS; ++s) kn[s] = ld16(kp + s * (2 * BS * 8));
+    for (int s = 0; s < KS; ++s) B.k[s] = ld16(kp + s * (2 * BS * 8));
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
       int tv = t0 + 16 * s2;
       if (tv > S - 1) tv = S - 1;
-      const int vb = clampi(bt[tv / BS], 0, p.num_blocks - 1);
+      const int vb = block_of(tv);
       const uint16_t* vp = vc + ((int64_t)vb * p.hkv + kvh) * head_stride + (BS == 32 ? 16 * s2 : 0) +
                            8 * half + (int64_t)col * BS;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) vn[mt][s2] = ld16(vp + (int64_t)(32 * mt) * BS);
+      for (int mt = 0; mt < MT; ++mt) B.v[mt][s2] = ld16(vp + (int64_t)(32 * mt) * BS);
     }
   };
 
-  int tile = wave;
-  if (tile < ntiles) load_tile(tile);
-  for (; tile < ntiles; tile += 4) {
-    u32x4 kop[KS], vop[MT][2];
-#pragma unroll
-    for (int s = 0; s < KS; ++s) kop[s] = kn[s];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) { vop[mt][0] = vn[mt][0]; vop[mt][1] = vn[mt][1]; }
-    if (tile + 4 < ntiles) load_tile(tile + 4);
-
-    const int t0 = t_begin + tile * 32;
+  auto process = [&](Buf& B, int i) {
+    const int t0 = t_begin + (wave + 4 * i) * 32;
     if (t0 + 32 > S) {
       // the tile runs past the sequence: zero V rows of keys >= S (they may hold anything)
 #pragma unroll
@@ -130,7 +152,7 @@ __global__ __launch_bounds__(256) void verify_attn_kernel(AttnParams p) {
           const int kbase = t0 + 16 * s2 + 8 * ((2 * w) >> 2) + 4 * half + ((2 * w) & 3);
           const uint32_t keep = (kbase < S ? 0x0000FFFFu : 0u) | (kbase + 1 < S ? 0xFFFF0000u : 0u);
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt) vop[mt][s2][w] &= keep;
+          for (int mt = 0; mt < MT; ++mt) B.v[mt][s2][w] &= keep;
         }
       }
     }
@@ -140,38 +162,43 @@ __global__ __launch_bounds__(256) void verify_attn_kernel(AttnParams p) {
     for (int nt = 0; nt < NT; ++nt) {
       f32x16 sc;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) sc[i] = 0.f;
+      for (int e = 0; e < 16; ++e) sc[e] = 0.f;
 #pragma unroll
       for (int s = 0; s < KS; ++s)
-        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kop[s]), qop[nt][s], sc, 0, 0, 0);
+        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(B.k[s]), as_bf16x8(sm_q[nt][s][lane]), sc, 0, 0, 0);
       float x[16];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) x[i] = sc[i] * p.scale_log2e;
+      for (int e = 0; e < 16; ++e) x[e] = sc[e] * p.scale_log2e;
       if (need_mask) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = t0 + (i >> 2) * 8 + 4 * half + (i & 3);
-          if (key > lim[nt]) x[i] = -INFINITY;
+        for (int e = 0; e < 16; ++e) {
+          const int key = t0 + (e >> 2) * 8 + 4 * half + (e & 3);
+          if (key > lim[nt]) x[e] = -INFINITY;
         }
       }
       float mx = x[0];
 #pragma unroll
-      for (int i = 1; i < 16; ++i) mx = fmaxf(mx, x[i]);
+      for (int e = 1; e < 16; ++e) mx = fmaxf(mx, x[e]);
       mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-      const float mnew = fmaxf(m[nt], mx);
-      const float alpha = fast_exp2(m[nt] - mnew);
-      m[nt] = mnew;
+      // Lazy rescaling: the reference maximum moves only when a score exceeds it by more than
+      // 2^kLazy, so 2^(x - m) stays <= 2^kLazy and the accumulators are rescaled rarely.
+      if (__builtin_amdgcn_ballot_w64(mx > m[nt] + kLazy) != 0) {
+        const float mnew = fmaxf(m[nt], mx);
+        const float alpha = fast_exp2(m[nt] - mnew);
+        m[nt] = mnew;
+        l[nt] *= alpha;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[nt][mt][e] *= alpha;
+      }
       float ps = 0.f;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        x[i] = fast_exp2(x[i] - mnew);
-        ps += x[i];
+      for (int e = 0; e < 16; ++e) {
+        x[e] = fast_exp2(x[e] - m[nt]);
+        ps += x[e];
       }
-      l[nt] = l[nt] * alpha + ps;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) acc[nt][mt][i] *= alpha;
+      l[nt] += ps;
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
         u32x4 pw;
@@ -180,7 +207,20 @@ __global__ __launch_bounds__(256) void verify_attn_kernel(AttnParams p) {
         const bf16x8 pb = as_bf16x8(pw);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
-          acc[nt][mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vop[mt][s2]), pb, acc[nt][mt], 0, 0, 0);
+          acc[nt][mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(B.v[mt][s2]), pb, acc[nt][mt], 0, 0, 0);
+      }
+    }
+  };
+
+  if (cnt > 0) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) load_tile(buf[d], d);
+    for (int i = 0; i < cnt; i += DEPTH) {
+#pragma unroll
+      for (int d = 0; d < DEPTH; ++d) {
+        if (i + d >= cnt) break;
+        process(buf[d], i + d);
+        load_tile(buf[d], i + d + DEPTH);
       }
     }
   }
