@@ -64,7 +64,7 @@ void attn_chunking(int32_t max_seq_len, int32_t req, int* chunk, int* nch) {
 }
 
 struct AcceptLayout {
-  size_t st_a, st_mode, ctr, counts, lists, lse, row_stats, max_part, bad_part, sum_part, total;
+  size_t geo, st_a, st_mode, counts, lists, tin, lse, max_part, bad_part, sum_part, total;
 };
 
 int64_t accept_nsub(int64_t V) { return (V + spexis::kAcceptSub - 1) / spexis::kAcceptSub; }
@@ -78,13 +78,13 @@ AcceptLayout accept_layout(int64_t B, int64_t V, int64_t max_k) {
     off += (size_t)round_up((int64_t)bytes, 256);
     return at;
   };
+  l.geo = take(B * 16);
   l.st_a = take(B * 4);
   l.st_mode = take(B * 4);
-  l.ctr = take(B * 4);
   l.counts = take((max_k + 2) * 4);
-  l.lists = take((max_k + 1) * B * 4);
-  l.lse = take(2 * B * ns * 2 * 4);
-  l.row_stats = take(B * (max_k + 1) * 4 * 4);
+  l.lists = take((max_k + 1) * B * 4 * 4);
+  l.tin = take(B * (max_k > 0 ? max_k : 1) * 4 * 4);
+  l.lse = take(2 * 2 * B * ns * 2 * 4);
   l.max_part = take(B * ns * 2 * 4);
   l.bad_part = take(B * ns * 4);
   l.sum_part = take(B * ns * 8);
@@ -237,7 +237,7 @@ int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, 
                 lay.total);
   const int64_t nsub = accept_nsub(vocab);
   const int64_t ipr = (nsub + spexis::kSubPerItem - 1) / spexis::kSubPerItem;
-  if ((int64_t)num_seqs * ipr * 2 >= (1ll << 31))
+  if ((int64_t)num_seqs * ipr >= (1ll << 31))
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_accept: grid too large");
   char* ws = static_cast<char*>(workspace);
   spexis::AcceptParams p{};
@@ -259,13 +259,13 @@ int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, 
   p.out_tokens = out_tokens;
   p.row_status = row_status;
   p.seq_lens_inout = seq_lens_inout;
+  p.geo = reinterpret_cast<int32_t*>(ws + lay.geo);
   p.st_a = reinterpret_cast<int32_t*>(ws + lay.st_a);
   p.st_mode = reinterpret_cast<int32_t*>(ws + lay.st_mode);
-  p.ctr = reinterpret_cast<int32_t*>(ws + lay.ctr);
   p.counts = reinterpret_cast<int32_t*>(ws + lay.counts);
   p.lists = reinterpret_cast<int32_t*>(ws + lay.lists);
+  p.tin = reinterpret_cast<float*>(ws + lay.tin);
   p.lse_part = reinterpret_cast<float*>(ws + lay.lse);
-  p.row_stats = reinterpret_cast<float*>(ws + lay.row_stats);
   p.max_part = reinterpret_cast<float*>(ws + lay.max_part);
   p.bad_part = reinterpret_cast<int32_t*>(ws + lay.bad_part);
   p.sum_part = reinterpret_cast<uint64_t*>(ws + lay.sum_part);

@@ -42,6 +42,17 @@ void verify_attn_kernel(AttnParams p) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 31, half = lane >> 5;
 
+  // Block ids this chunk may use, loaded together with the sequence geometry (the chunk start
+  // does not depend on the sequence length).
+  const int32_t* bt = p.block_tables + (int64_t)b * p.max_blocks;
+  const int blk0 = (c * p.chunk) / BS;
+  int bt_pre[kMaxChunkBlocks / 256];
+#pragma unroll
+  for (int u = 0; u < kMaxChunkBlocks / 256; ++u) {
+    const int x = blk0 + threadIdx.x + 256 * u;
+    bt_pre[u] = bt[x < p.max_blocks ? x : p.max_blocks - 1];
+  }
+
   // ---- sequence geometry (clamped so that every address stays inside its buffer)
   const int cap = p.max_blocks * BS;
   const int q0 = clampi(p.qsl[b], 0, p.total_tokens);
@@ -59,14 +70,12 @@ void verify_attn_kernel(AttnParams p) {
   const int t_end = (c == nch - 1) ? S : t_begin + p.chunk;   // the last chunk takes the rest
   const int ntiles = (t_end - t_begin + 31) >> 5;
 
-  const int32_t* bt = p.block_tables + (int64_t)b * p.max_blocks;
   // Block ids of the chunk, staged in LDS: tile addresses then never wait on a global load
   // (which, counted in order with the K/V loads, would drain the prefetch pipeline).
   __shared__ int sm_blk[kMaxChunkBlocks];
-  const int blk0 = t_begin / BS;
-  const int nblk = (t_end - 1) / BS - blk0 + 1;
-  for (int x = threadIdx.x; x < nblk && x < kMaxChunkBlocks; x += blockDim.x)
-    sm_blk[x] = clampi(bt[blk0 + x], 0, p.num_blocks - 1);
+#pragma unroll
+  for (int u = 0; u < kMaxChunkBlocks / 256; ++u)
+    sm_blk[threadIdx.x + 256 * u] = clampi(bt_pre[u], 0, p.num_blocks - 1);
   auto block_of = [&](int token) {
     const int x = token / BS - blk0;
     return x < kMaxChunkBlocks ? sm_blk[x] : clampi(bt[token / BS], 0, p.num_blocks - 1);

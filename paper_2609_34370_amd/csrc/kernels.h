@@ -42,7 +42,7 @@ struct AcceptParams {
   int kind;              // 0 probs, 1 logits
   int B, V, max_k, T;
   int nsub;              // ceil(V / kAcceptSub): partial results are kept per sub-chunk
-  int ipr;               // ceil(nsub / kSubPerItem): work items per vocabulary row
+  int ipr;               // ceil(nsub / kSubPerItem): work items per sequence
   float c;               // log2(e) / temperature (logits mode)
   const int32_t* qsl;
   const float* target;
@@ -55,20 +55,21 @@ struct AcceptParams {
   int32_t* row_status;
   int32_t* seq_lens_inout;
   // workspace views
-  int32_t* st_a;         // [B] accepted count so far / final a_b
+  int32_t* geo;          // [B][4] first target row, first draft row, k, valid
+  int32_t* st_a;         // [B] final a_b
   int32_t* st_mode;      // [B] 0 testing, 1 residual, 2 bonus, 3 done (outputs written)
-  int32_t* ctr;          // [B] arrival counters (zeroed by the init kernel, reset by the last arrival)
   int32_t* counts;       // [max_k+2] sequences still testing when round i starts (logits mode)
-  int32_t* lists;        // [max_k+1][B] those sequences (round 0 uses 0..B-1)
-  float* lse_part;       // [2][B][nsub][2] sub-chunk (max, sum of 2^(y-max)) of the current round
-  float* row_stats;      // [B][max_k+1][4] (M, Z) of target row i, then of draft row i
-  float* max_part;       // [B][nsub][2] (max w, max p)
+  int32_t* lists;        // [max_k+1][B][4] those sequences: b, first target row, first draft row, k
+  float* tin;            // [B][max_k][4] test inputs of position i: target logit and draft logit
+                         // of x_i, u_i (logits mode; gathered by the init kernel)
+  float* lse_part;       // [2 round parity][2 row kind][B][nsub][2] (max, sum of 2^(y-max))
+  float* max_part;       // [B][nsub][2] (max w, max p) of the sampled row(s)
   int32_t* bad_part;     // [B][nsub]
   uint64_t* sum_part;    // [B][nsub]
 };
 
 constexpr int kAcceptSub = 4096;     // vocab entries per partial result (one wave's share)
-constexpr int kSubPerItem = 8;       // sub-chunks per work item (two per wave of a workgroup)
+constexpr int kSubPerItem = 4;       // sub-chunks per work item (one per wave of a workgroup)
 
 hipError_t launch_append(const AppendParams& p, hipStream_t s);
 hipError_t launch_attention(const AttnParams& p, hipStream_t s);
