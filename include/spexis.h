@@ -107,8 +107,10 @@ int spexis_append_kv(void* k_cache, void* v_cache, int32_t num_blocks, int32_t n
                      const void* new_v, void* stream);
 
 /*
- * Bytes of workspace spexis_verify_attention needs for these host-side bounds (0 when no
- * sequence is split across KV chunks).  kv_chunk_tokens as in spexis_verify_attention.
+ * Bytes of workspace spexis_verify_attention needs for these host-side bounds (> 0 whenever
+ * the sizes are valid; 0 for invalid sizes).  kv_chunk_tokens as in spexis_verify_attention.
+ * With kv_chunk_tokens = 0 it is at most 1024 * (2 * (Hq/Hkv) * max_query_len * (head_dim + 2)
+ * + 40) * 4 bytes (about 68 MB at 64 rows, head_dim 128), whatever the sequence lengths.
  */
 size_t spexis_verify_attention_workspace_size(int32_t num_seqs, int32_t num_q_heads,
                                               int32_t num_kv_heads, int32_t head_dim,
@@ -130,10 +132,14 @@ size_t spexis_verify_attention_workspace_size(int32_t num_seqs, int32_t num_q_he
  *           must not alias q)
  *   scale   softmax scale, usually 1/sqrt(head_dim)
  *   max_seq_len      host: >= max_b S_b, and S_b <= max_blocks_per_seq * block_size
- *   kv_chunk_tokens  host: KV tokens per work item when a sequence is split across
- *                    workgroups (0 = automatic; otherwise rounded up to a multiple of 32)
- *   workspace        fp32 partials, >= spexis_verify_attention_workspace_size(...) bytes
- * Supported: head_dim in {64, 128}, block_size in {16, 32}, (Hq/Hkv) * max_query_len <= 64.
+ *   kv_chunk_tokens  host: the keys of all (sequence, KV head) pairs are cut into 32-key
+ *                    tiles and split into equal shares, one per wave; 0 = an even split
+ *                    over at most 1024 waves, otherwise shares of ceil(kv_chunk_tokens/32)
+ *                    tiles (widened if the sequences hold more than max_seq_len allows)
+ *   workspace        fp32 partials of pairs cut between shares, plus one header per share;
+ *                    >= spexis_verify_attention_workspace_size(...) bytes, device memory
+ * Supported: head_dim in {64, 128}, block_size in {16, 32}, (Hq/Hkv) * max_query_len <= 64,
+ * num_seqs * Hkv * ceil(max_blocks_per_seq * block_size / 32) < 2^31.
  * Errors: INVALID_ARGUMENT, UNSUPPORTED, WORKSPACE_TOO_SMALL, HIP.
  */
 int spexis_verify_attention(const void* k_cache, const void* v_cache, int32_t num_blocks,

@@ -39,28 +39,29 @@ int hip_result(hipError_t e, const char* what) {
 
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
-constexpr int kMaxChunks = 64;     // split-KV chunks per sequence (merge kernel's LDS table)
 constexpr int kMaxRows = 64;       // query rows per (sequence, KV head)
 constexpr int kMaxK = 32;
 constexpr int kMaxVocab = 1 << 22; // keeps sum W_v < 2^63 (W_v < 2^41)
 
 bool bad_cache_shape(int32_t bs, int32_t d) { return !((bs == 16 || bs == 32) && (d == 64 || d == 128)); }
 
-// KV tokens per split-KV work item and the number of items per sequence.
-void attn_chunking(int32_t max_seq_len, int32_t req, int* chunk, int* nch) {
-  int64_t c = req > 0 ? round_up(req, 32) : std::max<int64_t>(1024, round_up((max_seq_len + 15) / 16, 32));
-  int64_t n = (max_seq_len + c - 1) / c;
-  if (n > kMaxChunks) {
-    c = round_up((max_seq_len + kMaxChunks - 1) / kMaxChunks, 32);
-    n = (max_seq_len + c - 1) / c;
-  }
-  if (c > 8192) c = 8192;   // the attention kernel stages one chunk's block ids in LDS
-  n = (max_seq_len + c - 1) / c;
-  if (n > kMaxChunks) {      // only for max_seq_len > 64 * 8192: the last chunk takes the rest
-    n = kMaxChunks;
-  }
-  *chunk = (int)c;
-  *nch = (int)std::max<int64_t>(n, 1);
+// Shares per KV head, grid waves and the 32-key tiles of a share.  kv_chunk_tokens = 0: about
+// kAttnMaxWaves waves split each head's tiles evenly (at least kAttnMinTilesPerWave each);
+// otherwise every share takes ceil(kv_chunk_tokens / 32) tiles and there are enough shares for
+// the most tiles that max_seq_len allows.  (The kernel widens the shares if the sequences hold
+// more.)
+bool attn_waves(int32_t num_seqs, int32_t num_kv_heads, int32_t max_seq_len, int32_t req, int* tpw,
+                int* nshares, int* nwaves) {
+  const int64_t max_tiles = (int64_t)num_seqs * ((max_seq_len + 31) / 32);   // per KV head
+  const int64_t per = req > 0 ? ((int64_t)req + 31) / 32 : spexis::kAttnMinTilesPerWave;
+  int64_t sh = (max_tiles + per - 1) / per;
+  if (req == 0) sh = std::min<int64_t>(sh, std::max(1, spexis::kAttnMaxWaves / num_kv_heads));
+  sh = std::max<int64_t>(sh, 1);
+  const int64_t w = round_up(sh * num_kv_heads, 4);
+  *tpw = req > 0 ? (int)per : 0;
+  *nshares = (int)std::min<int64_t>(sh, 1 << 30);
+  *nwaves = (int)std::min<int64_t>(w, 1 << 30);
+  return w <= (1 << 24);
 }
 
 struct AcceptLayout {
@@ -126,11 +127,10 @@ size_t spexis_verify_attention_workspace_size(int32_t num_seqs, int32_t num_q_he
                                               int32_t kv_chunk_tokens) {
   if (num_seqs <= 0 || num_kv_heads <= 0 || num_q_heads <= 0 || max_query_len <= 0 || max_seq_len <= 0)
     return 0;
-  int chunk, nch;
-  attn_chunking(max_seq_len, kv_chunk_tokens, &chunk, &nch);
-  if (nch <= 1) return 0;
+  int tpw, nshares, nwaves;
+  if (!attn_waves(num_seqs, num_kv_heads, max_seq_len, kv_chunk_tokens, &tpw, &nshares, &nwaves)) return 0;
   const int rmax = (num_q_heads / num_kv_heads) * max_query_len;
-  return (size_t)num_seqs * num_kv_heads * nch * spexis::attn_slot_floats(rmax, head_dim) * sizeof(float);
+  return (size_t)spexis::attn_ws_bytes(nwaves, rmax, head_dim);
 }
 
 int spexis_verify_attention(const void* k_cache, const void* v_cache, int32_t num_blocks,
@@ -161,16 +161,19 @@ int spexis_verify_attention(const void* k_cache, const void* v_cache, int32_t nu
                 group * max_query_len, kMaxRows);
   if ((int64_t)max_blocks_per_seq * block_size < max_query_len)
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: block tables hold fewer slots than a query");
+  // every tile index of the stream fits in 32 bits
+  if ((int64_t)num_seqs * (((int64_t)max_blocks_per_seq * block_size + 31) / 32) >= (1ll << 31))
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_verify_attention: more than 2^31 key tiles");
   if (num_seqs == 0 || total_tokens == 0) return ok();
-  int chunk, nch;
-  attn_chunking(max_seq_len, kv_chunk_tokens, &chunk, &nch);
+  int tpw, nshares, nwaves;
+  if (!attn_waves(num_seqs, num_kv_heads, max_seq_len, kv_chunk_tokens, &tpw, &nshares, &nwaves))
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_verify_attention: kv_chunk_tokens %d asks for too many waves",
+                kv_chunk_tokens);
   const size_t need = spexis_verify_attention_workspace_size(num_seqs, num_q_heads, num_kv_heads, head_dim,
                                                              max_query_len, max_seq_len, kv_chunk_tokens);
-  if (need > 0 && (!workspace || workspace_bytes < need))
+  if (!workspace || workspace_bytes < need)
     return fail(SPEXIS_ERR_WORKSPACE_TOO_SMALL, "spexis_verify_attention: workspace %zu bytes < %zu needed",
                 workspace_bytes, need);
-  if ((int64_t)nch * num_seqs * num_kv_heads >= (1ll << 31))
-    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_verify_attention: grid too large");
   spexis::AttnParams p{};
   p.k_cache = k_cache;
   p.v_cache = v_cache;
@@ -190,8 +193,9 @@ int spexis_verify_attention(const void* k_cache, const void* v_cache, int32_t nu
   p.hq = num_q_heads;
   p.group = group;
   p.rmax = group * max_query_len;
-  p.chunk = chunk;
-  p.nch_max = nch;
+  p.tiles_per_wave = tpw;
+  p.nshares = nshares;
+  p.nwaves = nwaves;
   p.scale_log2e = (float)((double)scale * 1.4426950408889634);
   return hip_result(spexis::launch_attention(p, (hipStream_t)stream), "spexis_verify_attention");
 }

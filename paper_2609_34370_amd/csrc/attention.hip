@@ -2,18 +2,25 @@
 // the k drafts, Sec. 4) attend causally over that sequence's paged KV cache, all query heads
 // of one KV head (GQA group) together.
 //
-// Work decomposition: one workgroup per (KV chunk, sequence, KV head).  The G*(k+1) query rows
-// of a (sequence, KV head) pair -- at most 64 -- form one or two 32-row tiles.  Each of the
-// four waves streams its own 32-key tiles of the chunk (tiles w, w+4, ...) from HBM straight
-// into matrix-core operand registers, keeps its own online-softmax state, and the waves merge
-// through LDS at the end.  Chunks of one sequence merge in a second kernel (split-KV).
+// Work decomposition.  An item is one (sequence, KV head) pair: its G*(k+1) query rows -- at
+// most 64, one or two 32-row tiles -- against the sequence's keys.  For each KV head the keys
+// of all sequences form one stream of 32-key tiles (sequence, then position), cut into equal
+// contiguous shares; wave (share s, head h) is wave s*Hkv + h, so the waves of a workgroup
+// walk the same tiles of neighbouring heads at about the same time and read neighbouring
+// memory (the cache stores a block's heads together).  A wave walks its share alone: no
+// barrier, no merge, a prefetch pipeline of DEPTH tiles that runs on across sequence
+// boundaries, and block ids fetched one tile ahead with scalar loads (their wait counter is
+// not the one the tile loads use).  An item a wave covers whole is normalised and written as
+// bf16; an item cut between shares leaves fp32 partials (reference maximum, sum,
+// unnormalised output) that a second kernel combines.  Balance is exact to one tile, whatever
+// the mix of sequence lengths.
 //
 // Per 32-key tile and 32-row tile, with v_mfma_f32_32x32x16_bf16 (operand A: lane l holds row
 // l%32, k-slice 8*(l/32)..+7; B: column l%32, same k-slice; C: lane l, value i holds row
 // 8*(i/4) + 4*(l/32) + i%4, column l%32):
 //   S^T[key][row] = K[key][:] . Q[row][:]   A = K tile (one 16-byte load per lane per k-step:
 //                                           the K layout keeps 8 head-dim values of a slot
-//                                           together), B = Q (registers, loaded once)
+//                                           together), B = Q (registers, loaded per item)
 //   lane l then owns query row l%32 and keys (i/4)*8 + 4*(l/32) + i%4: the row maximum is a
 //   max over 16 values plus one exchange with lane l^32.
 //   O^T[d][row] += V^T[d][key] . P^T[key][row]   A = V^T tile: the V layout stores slots with
@@ -27,130 +34,267 @@ namespace spexis {
 
 constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" of the running maxima
 constexpr float kLazy = 8.0f;         // base-2 headroom before the running maximum moves
-constexpr int kMaxChunkBlocks = 512;  // block ids of one chunk staged in LDS (chunk <= 8192 tokens)
+constexpr int kWaitVmcnt0 = 0x0F70;   // s_waitcnt operand: vmcnt(0), expcnt and lgkmcnt not waited
+
+// Read-only view of an int32 array: loads through it at wave-uniform addresses become scalar
+// loads, counted apart from the vector loads of the tiles.
+typedef const __attribute__((address_space(4))) int32_t sint32;
+
+struct SeqGeo {
+  int q0, n, S, nt;   // first query token, query tokens, keys, 32-key tiles (0: no query)
+};
+
+// Geometry of sequence b, clamped so that every address derived from it stays in its buffer.
+template <typename Ptr>
+__device__ __forceinline__ SeqGeo seq_geo(const AttnParams& p, Ptr qsl, Ptr seq_lens, int b) {
+  SeqGeo g;
+  g.q0 = clampi(qsl[b], 0, p.total_tokens);
+  const int q1 = clampi(qsl[b + 1], g.q0, p.total_tokens);
+  g.n = min(q1 - g.q0, p.rmax / p.group);
+  g.S = clampi(seq_lens[b], max(g.n, 1), p.max_blocks * p.block_size);
+  g.nt = g.n >= 1 ? (g.S + 31) >> 5 : 0;
+  return g;
+}
+
+// Position in a head's tile stream: sequence, tile of the sequence, and the sequence's size.
+struct Cursor {
+  int b, t, nt, S;
+};
+
+__device__ __forceinline__ void advance(const AttnParams& p, Cursor& c) {
+  if (++c.t < c.nt) return;
+  c.t = 0;
+  SeqGeo g;
+  do {
+    if (c.b + 1 >= p.num_seqs) return;   // never past the stream's end; stay on a valid item
+    ++c.b;
+    g = seq_geo(p, (sint32*)p.qsl, (sint32*)p.seq_lens, c.b);
+  } while (g.nt == 0);
+  c.nt = g.nt;
+  c.S = g.S;
+}
 
 template <int D, int BS, int NT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NT == 1 ? 2 : 1)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1)))
 void verify_attn_kernel(AttnParams p) {
   constexpr int KS = D / 16;   // k-steps of the score product
   constexpr int MT = D / 32;   // 32-wide head-dim tiles of the output
-  const int item = blockIdx.x;
-  const int kvh = item % p.hkv;
-  const int rest = item / p.hkv;
-  const int b = rest % p.num_seqs;
-  const int c = rest / p.num_seqs;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int col = lane & 31, half = lane >> 5;
+  // Tiles in flight: the register file of one wave per SIMD holds DEPTH operand buffers.
+  constexpr int DEPTH = NT == 1 ? 3 : 2;
+  const int lane = threadIdx.x & 63, col = lane & 31, half = lane >> 5;
+  const int wid = __builtin_amdgcn_readfirstlane((int)blockIdx.x * 4 + (int)(threadIdx.x >> 6));
+  const int64_t slot_f = attn_slot_floats(p.rmax, D);
+  float* slots = p.ws + (int64_t)wid * 2 * slot_f;
+  int32_t* hdr = reinterpret_cast<int32_t*>(p.ws + (int64_t)p.nwaves * 2 * slot_f) + (int64_t)wid * kAttnHdrInts;
 
-  // Block ids this chunk may use, loaded together with the sequence geometry (the chunk start
-  // does not depend on the sequence length).
-  const int32_t* bt = p.block_tables + (int64_t)b * p.max_blocks;
-  const int blk0 = (c * p.chunk) / BS;
-  int bt_pre[kMaxChunkBlocks / 256];
-#pragma unroll
-  for (int u = 0; u < kMaxChunkBlocks / 256; ++u) {
-    const int x = blk0 + threadIdx.x + 256 * u;
-    bt_pre[u] = bt[x < p.max_blocks ? x : p.max_blocks - 1];
+  auto no_share = [&]() {
+    if (lane == 0) *reinterpret_cast<u32x4*>(hdr) = u32x4{0u, 0u, 0u, 0u};
+  };
+  const int h = wid % p.hkv, share = wid / p.hkv;
+  if (share >= p.nshares) return no_share();
+
+  // ---- this wave's share [g0, g0 + cnt) of head h's tile stream
+  int per_lane = 0;
+  for (int base = 0; base < p.num_seqs; base += kWave)
+    if (base + lane < p.num_seqs) per_lane += seq_geo(p, p.qsl, p.seq_lens, base + lane).nt;
+  const int total = __builtin_amdgcn_readfirstlane(wave_sum_i32(per_lane));   // < 2^31 (host)
+  const int even = (total + p.nshares - 1) / p.nshares;
+  const int P = max(p.tiles_per_wave > 0 ? p.tiles_per_wave : kAttnMinTilesPerWave, even);
+  if ((int64_t)share * P >= total) return no_share();
+  const int g0 = share * P;
+  const int cnt = min(P, total - g0);
+  // the sequence holding tile g0, and the stream index of its first tile
+  int before = 0, b0 = 0, f0 = 0;
+  for (int base = 0; base < p.num_seqs; base += kWave) {
+    const int b = base + lane;
+    const int v = b < p.num_seqs ? seq_geo(p, p.qsl, p.seq_lens, b).nt : 0;
+    const int incl = wave_incl_scan_i32(v, lane);
+    const uint64_t hit = __builtin_amdgcn_ballot_w64(before + incl > g0);
+    if (hit != 0) {
+      const int l0 = __builtin_ctzll(hit);
+      b0 = base + l0;
+      f0 = before + __shfl(incl - v, l0, kWave);
+      break;
+    }
+    before += __shfl(incl, kWave - 1, kWave);
+  }
+  b0 = __builtin_amdgcn_readfirstlane(b0);
+  f0 = __builtin_amdgcn_readfirstlane(f0);
+  Cursor start;
+  {
+    const SeqGeo g = seq_geo(p, (sint32*)p.qsl, (sint32*)p.seq_lens, b0);
+    if (g.nt == 0 || g0 < f0 || g0 - f0 >= g.nt) return no_share();   // inputs changed under us
+    start.b = b0;
+    start.nt = g.nt;
+    start.S = g.S;
+    start.t = g0 - f0;
   }
 
-  // ---- sequence geometry (clamped so that every address stays inside its buffer)
-  const int cap = p.max_blocks * BS;
-  const int q0 = clampi(p.qsl[b], 0, p.total_tokens);
-  const int q1 = clampi(p.qsl[b + 1], q0, p.total_tokens);
-  int n = q1 - q0;
-  if (n > p.rmax / p.group) n = p.rmax / p.group;
-  if (n < 1) return;
-  const int S = clampi(p.seq_lens[b], n, cap);
-  const int L = S - n;
-  const int R = p.group * n;
-  int nch = (S + p.chunk - 1) / p.chunk;
-  if (nch > p.nch_max) nch = p.nch_max;
-  if (c >= nch) return;
-  const int t_begin = c * p.chunk;
-  const int t_end = (c == nch - 1) ? S : t_begin + p.chunk;   // the last chunk takes the rest
-  const int ntiles = (t_end - t_begin + 31) >> 5;
-
-  // Block ids of the chunk, staged in LDS: tile addresses then never wait on a global load
-  // (which, counted in order with the K/V loads, would drain the prefetch pipeline).
-  __shared__ int sm_blk[kMaxChunkBlocks];
-#pragma unroll
-  for (int u = 0; u < kMaxChunkBlocks / 256; ++u)
-    sm_blk[threadIdx.x + 256 * u] = clampi(bt_pre[u], 0, p.num_blocks - 1);
-  auto block_of = [&](int token) {
-    const int x = token / BS - blk0;
-    return x < kMaxChunkBlocks ? sm_blk[x] : clampi(bt[token / BS], 0, p.num_blocks - 1);
-  };
   const uint16_t* kc = reinterpret_cast<const uint16_t*>(p.k_cache);
   const uint16_t* vc = reinterpret_cast<const uint16_t*>(p.v_cache);
   const int64_t head_stride = (int64_t)BS * D;   // elements of one (block, head) chunk
-
-  // ---- query rows of this lane: row r = nt*32 + col is (token j, head g) with r = j*G + g.
-  // The score product's B operand (Q) is the same for the four waves: wave 0 stages it in LDS
-  // in operand order, every wave reads it back per tile.
-  __shared__ u32x4 sm_q[NT][KS][kWave];
-  int lim[NT];
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const int r = nt * 32 + col;
-    const int j = r < R ? r / p.group : n - 1;    // padding rows repeat a real row
-    const int g = r < R ? r % p.group : 0;
-    lim[nt] = L + j;                              // keys 0..L+j are visible
-    if (wave == 0) {
-      const uint16_t* qrow = reinterpret_cast<const uint16_t*>(p.q) +
-                             ((int64_t)(q0 + j) * p.hq + kvh * p.group + g) * D + 8 * half;
-#pragma unroll
-      for (int s = 0; s < KS; ++s) sm_q[nt][s][lane] = ld16(qrow + 16 * s);
+  // Physical blocks of a tile: keys 0..15 and 16..31 (one block when BS = 32).  The second id
+  // repeats the first past the sequence end; those keys are masked.
+  auto tile_blocks = [&](const Cursor& c, int& ka, int& kb) {
+    sint32* row = (sint32*)p.block_tables + (int64_t)c.b * p.max_blocks;
+    if (BS == 16) {
+      ka = clampi(row[2 * c.t], 0, p.num_blocks - 1);
+      kb = clampi(row[min(2 * c.t + 1, (c.S - 1) >> 4)], 0, p.num_blocks - 1);
+    } else {
+      ka = kb = clampi(row[c.t], 0, p.num_blocks - 1);
     }
+  };
+
+  // load side: the tile being issued (lc, its block ids) and the next one (nc), one step ahead
+  Cursor lc = start, nc = start;
+  int lidx = 0, la, lb, na = 0, nb = 0;
+  tile_blocks(lc, la, lb);
+  if (cnt > 1) {
+    advance(p, nc);
+    tile_blocks(nc, na, nb);
   }
 
-  __syncthreads();   // block ids and Q staged
-
-  float m[NT], l[NT];
-  f32x16 acc[NT][MT];
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    m[nt] = kNegBig;
-    l[nt] = 0.f;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc[nt][mt][i] = 0.f;
-  }
-
-  // Operand buffers.  Tile i of this wave is chunk tile wave + 4 i; DEPTH buffers rotate so
-  // that DEPTH-1 tiles are in flight while one is computed.  Loads are issued unconditionally:
-  // an index past the wave's last tile re-reads that tile (an L2 hit), which keeps the number of
-  // outstanding loads the same on every path and lets the waits stay partial.
-  constexpr int DEPTH = 2;
+  // Operand buffers; DEPTH rotate so that DEPTH-1 tiles are in flight while one is computed.
+  // Loads are issued unconditionally -- past the share's end they re-read its last tile (an L2
+  // hit) -- so the count of outstanding loads is the same on every path and waits stay partial.
   struct Buf {
     u32x4 k[KS];
     u32x4 v[MT][2];
   };
   Buf buf[DEPTH];
-  const int cnt = ntiles > wave ? (ntiles - wave + 3) / 4 : 0;   // tiles of this wave
 
   auto load_tile = [&](Buf& B, int i) {
-    const int t0 = t_begin + (wave + 4 * (i < cnt ? i : cnt - 1)) * 32;
-    int tk = t0 + col;
-    if (tk > S - 1) tk = S - 1;                   // past the end: any valid slot, masked later
-    const int kb = block_of(tk);
-    const uint16_t* kp = kc + ((int64_t)kb * p.hkv + kvh) * head_stride + (tk % BS) * 8 + half * BS * 8;
+    if (i < cnt && i > lidx) {
+      lc = nc;
+      la = na;
+      lb = nb;
+      lidx = i;
+      if (i + 1 < cnt) {
+        advance(p, nc);
+        tile_blocks(nc, na, nb);
+      }
+    }
+    const int t0 = lc.t * 32;
+    const int tk = min(t0 + col, lc.S - 1);   // past the end: any valid slot, masked later
+    const int kblk = (BS == 16 && (tk >> 4) != 2 * lc.t) ? lb : la;
+    const uint16_t* kp = kc + ((int64_t)kblk * p.hkv + h) * head_stride + (tk % BS) * 8 + half * BS * 8;
 #pragma unroll
     for (int s = 0; s < KS; ++s) B.k[s] = ld16(kp + s * (2 * BS * 8));
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
-      int tv = t0 + 16 * s2;
-      if (tv > S - 1) tv = S - 1;
-      const int vb = block_of(tv);
-      const uint16_t* vp = vc + ((int64_t)vb * p.hkv + kvh) * head_stride + (BS == 32 ? 16 * s2 : 0) +
+      const int vblk = (BS == 16 && s2 == 1) ? lb : la;
+      const uint16_t* vp = vc + ((int64_t)vblk * p.hkv + h) * head_stride + (BS == 32 ? 16 * s2 : 0) +
                            8 * half + (int64_t)col * BS;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) B.v[mt][s2] = ld16(vp + (int64_t)(32 * mt) * BS);
     }
   };
 
+  // process side: the item being computed and its online-softmax state
+  Cursor pc = start;
+  int q0 = 0, n = 1, L = 0, R = 0;
+  bool starts_before = false;
+  int head_b = 0, head_f = 0, head_nt = 0, head_q0 = 0, head_n = 0, head_flag = 0;
+  int lim[NT];
+  // Q, the score product's B operand, in operand order.  Two row tiles keep it in this wave's
+  // part of LDS (registers would not hold it next to two tiles' accumulators); one in registers.
+  constexpr bool kQinLds = NT == 2;
+  u32x4 qr[kQinLds ? 1 : NT][KS];
+  __shared__ u32x4 sm_q[kQinLds ? 4 : 1][NT][KS][kWave];
+  const int wave = threadIdx.x >> 6;
+  float m[NT], l[NT];
+  f32x16 acc[NT][MT];
+
+  auto begin_item = [&](int i) {
+    const SeqGeo g = seq_geo(p, (sint32*)p.qsl, (sint32*)p.seq_lens, pc.b);
+    q0 = g.q0;
+    n = g.n;
+    L = pc.S - n;
+    R = p.group * n;
+    starts_before = i == 0 && pc.t != 0;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      // row r = nt*32 + col is (token j, head g) with r = j*G + g; padding rows repeat a real row
+      const int r = nt * 32 + col;
+      const int j = r < R ? r / p.group : n - 1;
+      const int gq = r < R ? r % p.group : 0;
+      lim[nt] = L + j;   // keys 0..L+j are visible
+      const uint16_t* qrow = reinterpret_cast<const uint16_t*>(p.q) +
+                             ((int64_t)(q0 + j) * p.hq + h * p.group + gq) * D + 8 * half;
+      if (kQinLds) {
+        u32x4 t[KS];
+#pragma unroll
+        for (int s = 0; s < KS; ++s) t[s] = ld16(qrow + 16 * s);
+#pragma unroll
+        for (int s = 0; s < KS; ++s) sm_q[kQinLds ? wave : 0][nt][s][lane] = t[s];
+      } else {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) qr[kQinLds ? 0 : nt][s] = ld16(qrow + 16 * s);
+      }
+      m[nt] = kNegBig;
+      l[nt] = 0.f;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[nt][mt][e] = 0.f;
+    }
+    // Wait for Q here, explicitly (this drains the tiles in flight, once per item): the wait
+    // counter then knows Q complete on every path, and the tile loop's waits stay partial.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+  };
+
+  auto end_item = [&](int i) {
+    const bool ends_after = pc.t < pc.nt - 1;
+    const bool whole = !starts_before && !ends_after;
+    float* slot = slots + (starts_before ? 0 : slot_f);
+    if (!whole && !starts_before) {   // this wave holds the item's first tiles
+      head_flag = 1;
+      head_b = pc.b;
+      head_f = g0 + i - pc.t;
+      head_nt = pc.nt;
+      head_q0 = q0;
+      head_n = n;
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const float lt = l[nt] + __shfl_xor(l[nt], 32, kWave);
+      const int r = nt * 32 + col;
+      if (r >= R) continue;
+      if (whole) {
+        const int j = r / p.group, gq = r % p.group;
+        const float inv = 1.0f / lt;
+        uint16_t* orow = reinterpret_cast<uint16_t*>(p.out) + ((int64_t)(q0 + j) * p.hq + h * p.group + gq) * D;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int a = 0; a < 4; ++a) {
+            u32x2 w;
+            w[0] = pack_bf16x2(acc[nt][mt][4 * a] * inv, acc[nt][mt][4 * a + 1] * inv);
+            w[1] = pack_bf16x2(acc[nt][mt][4 * a + 2] * inv, acc[nt][mt][4 * a + 3] * inv);
+            *reinterpret_cast<u32x2*>(orow + 32 * mt + 8 * a + 4 * half) = w;
+          }
+      } else {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int a = 0; a < 4; ++a) {
+            const f32x4 v = {acc[nt][mt][4 * a], acc[nt][mt][4 * a + 1], acc[nt][mt][4 * a + 2],
+                             acc[nt][mt][4 * a + 3]};
+            *reinterpret_cast<f32x4*>(slot + (int64_t)r * D + 32 * mt + 8 * a + 4 * half) = v;
+          }
+        if (half == 0) {
+          slot[(int64_t)p.rmax * D + r] = m[nt];
+          slot[(int64_t)p.rmax * D + p.rmax + r] = lt;
+        }
+      }
+    }
+  };
+
   auto process = [&](Buf& B, int i) {
-    const int t0 = t_begin + (wave + 4 * i) * 32;
+    if (i >= cnt) return;   // padding past the share's end
+    if (i == 0 || pc.t == 0) begin_item(i);
+    const int t0 = pc.t * 32;
+    const int S = pc.S;
     if (t0 + 32 > S) {
       // the tile runs past the sequence: zero V rows of keys >= S (they may hold anything)
 #pragma unroll
@@ -165,7 +309,7 @@ void verify_attn_kernel(AttnParams p) {
         }
       }
     }
-    const bool need_mask = t0 + 31 > L;
+    const bool need_mask = t0 + 31 > L;   // causal edge (keys >= S are past every row's limit)
 
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -174,7 +318,9 @@ void verify_attn_kernel(AttnParams p) {
       for (int e = 0; e < 16; ++e) sc[e] = 0.f;
 #pragma unroll
       for (int s = 0; s < KS; ++s)
-        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(B.k[s]), as_bf16x8(sm_q[nt][s][lane]), sc, 0, 0, 0);
+        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            as_bf16x8(B.k[s]), as_bf16x8(kQinLds ? sm_q[kQinLds ? wave : 0][nt][s][lane] : qr[kQinLds ? 0 : nt][s]),
+            sc, 0, 0, 0);
       float x[16];
 #pragma unroll
       for (int e = 0; e < 16; ++e) x[e] = sc[e] * p.scale_log2e;
@@ -219,166 +365,99 @@ void verify_attn_kernel(AttnParams p) {
           acc[nt][mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(B.v[mt][s2]), pb, acc[nt][mt], 0, 0, 0);
       }
     }
+    if (pc.t == pc.nt - 1 || i == cnt - 1) end_item(i);
+    if (i + 1 < cnt) advance(p, pc);
   };
 
-  if (cnt > 0) {
+  // Wait counts retire in issue order, so the loop is shaped for them: every pass runs a whole
+  // group of DEPTH tiles with no exit inside it (an exit edge back to the loop head would make
+  // one buffer look younger than the next, and each wait for it would drain the prefetched
+  // tiles); the share is padded to a multiple of DEPTH with tiles that are loaded but skipped.
 #pragma unroll
-    for (int d = 0; d < DEPTH; ++d) load_tile(buf[d], d);
-    for (int i = 0; i < cnt; i += DEPTH) {
+  for (int d = 0; d < DEPTH; ++d) load_tile(buf[d], d);
+  for (int i = 0; i < cnt; i += DEPTH) {
 #pragma unroll
-      for (int d = 0; d < DEPTH; ++d) {
-        if (i + d >= cnt) break;
-        process(buf[d], i + d);
-        load_tile(buf[d], i + d + DEPTH);
-      }
+    for (int d = 0; d < DEPTH; ++d) {
+      process(buf[d], i + d);
+      load_tile(buf[d], i + d + DEPTH);
     }
   }
 
-  // ---- merge the four waves: common maximum per row, then a two-level sum through LDS
-  __shared__ float sm_m[4][NT * 32];
-  __shared__ float sm_l[4][NT * 32];
-  __shared__ float sm_acc[2][NT * MT * 16 * 64];
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    l[nt] += __shfl_xor(l[nt], 32, kWave);
-    if (half == 0) sm_m[wave][nt * 32 + col] = m[nt];
-  }
-  __syncthreads();
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const int r = nt * 32 + col;
-    const float M = fmaxf(fmaxf(sm_m[0][r], sm_m[1][r]), fmaxf(sm_m[2][r], sm_m[3][r]));
-    const float f = fast_exp2(m[nt] - M);
-    m[nt] = M;
-    l[nt] *= f;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc[nt][mt][i] *= f;
-    if (half == 0) sm_l[wave][r] = l[nt];
-  }
-  if (wave >= 2) {
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) sm_acc[wave - 2][((nt * MT + mt) * 16 + i) * 64 + lane] = acc[nt][mt][i];
-  }
-  __syncthreads();
-  if (wave < 2) {
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) acc[nt][mt][i] += sm_acc[wave][((nt * MT + mt) * 16 + i) * 64 + lane];
-  }
-  __syncthreads();
-  if (wave == 1) {
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) sm_acc[0][((nt * MT + mt) * 16 + i) * 64 + lane] = acc[nt][mt][i];
-  }
-  __syncthreads();
-  if (wave != 0) return;
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const int r = nt * 32 + col;
-    const float lt = sm_l[0][r] + sm_l[1][r] + sm_l[2][r] + sm_l[3][r];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc[nt][mt][i] += sm_acc[0][((nt * MT + mt) * 16 + i) * 64 + lane];
-    if (r >= R) continue;
-    const int j = r / p.group, g = r % p.group;
-    if (nch == 1) {
-      const float inv = 1.0f / lt;
-      uint16_t* orow = reinterpret_cast<uint16_t*>(p.out) + ((int64_t)(q0 + j) * p.hq + kvh * p.group + g) * D;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          u32x2 w;
-          w[0] = pack_bf16x2(acc[nt][mt][4 * a] * inv, acc[nt][mt][4 * a + 1] * inv);
-          w[1] = pack_bf16x2(acc[nt][mt][4 * a + 2] * inv, acc[nt][mt][4 * a + 3] * inv);
-          *reinterpret_cast<u32x2*>(orow + 32 * mt + 8 * a + 4 * half) = w;
-        }
-    } else {
-      float* slot = p.ws + ((int64_t)(b * p.hkv + kvh) * p.nch_max + c) * attn_slot_floats(p.rmax, D);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int a = 0; a < 4; ++a) {
-          f32x4 v = {acc[nt][mt][4 * a], acc[nt][mt][4 * a + 1], acc[nt][mt][4 * a + 2], acc[nt][mt][4 * a + 3]};
-          *reinterpret_cast<f32x4*>(slot + (int64_t)r * D + 32 * mt + 8 * a + 4 * half) = v;
-        }
-      if (half == 0) {
-        slot[(int64_t)p.rmax * D + r] = m[nt];
-        slot[(int64_t)p.rmax * D + p.rmax + r] = lt;
-      }
-    }
+  // header of the slot-1 partial: the item this wave starts and a later share finishes
+  if (lane == 0) {
+    *reinterpret_cast<u32x4*>(hdr) = u32x4{(uint32_t)head_flag, (uint32_t)head_b, (uint32_t)head_f, (uint32_t)head_nt};
+    *reinterpret_cast<u32x4*>(hdr + 4) = u32x4{(uint32_t)P, (uint32_t)head_q0, (uint32_t)head_n, 0u};
   }
 }
 
-// Split-KV merge: o = sum_c acc_c * 2^(m_c - M) / sum_c l_c * 2^(m_c - M), M = max_c m_c.
+// Combines the partials of every item cut between shares: workgroup w handles the item whose
+// first tiles wave w (share s, head h) holds, in its slot 1; shares s+1 .. s_last of head h
+// hold the rest, in their slot 0, where s_last holds the item's last tile.
+//   o = sum_c acc_c 2^(m_c - M) / sum_c l_c 2^(m_c - M),   M = max_c m_c
+// Contributors are read four at a time, every load of a group issued together.
 template <int D>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
-  const int kvh = blockIdx.x % p.hkv;
-  const int b = blockIdx.x / p.hkv;
-  const int cap = p.max_blocks * p.block_size;
-  const int q0 = clampi(p.qsl[b], 0, p.total_tokens);
-  const int q1 = clampi(p.qsl[b + 1], q0, p.total_tokens);
-  int n = q1 - q0;
-  if (n > p.rmax / p.group) n = p.rmax / p.group;
-  if (n < 1) return;
-  const int S = clampi(p.seq_lens[b], n, cap);
-  int nch = (S + p.chunk - 1) / p.chunk;
-  if (nch > p.nch_max) nch = p.nch_max;
-  if (nch <= 1) return;
-  const int R = p.group * n;
+  const int w = blockIdx.x;
   const int64_t slot_f = attn_slot_floats(p.rmax, D);
-  const float* base = p.ws + (int64_t)(b * p.hkv + kvh) * p.nch_max * slot_f;
-  __shared__ float w[64][64];   // [chunk][row] normalised weights (nch_max <= 64, rmax <= 64)
-  for (int r = threadIdx.x; r < R; r += blockDim.x) {
-    float M = kNegBig;
-    for (int c = 0; c < nch; ++c) M = fmaxf(M, base[c * slot_f + (int64_t)p.rmax * D + r]);
-    float den = 0.f;
-    for (int c = 0; c < nch; ++c) {
-      const float e = fast_exp2(base[c * slot_f + (int64_t)p.rmax * D + r] - M);
-      w[c][r] = e;
-      den += e * base[c * slot_f + (int64_t)p.rmax * D + p.rmax + r];
-    }
-    const float inv = 1.0f / den;
-    for (int c = 0; c < nch; ++c) w[c][r] *= inv;
-  }
-  __syncthreads();
+  const int32_t* hdr = reinterpret_cast<const int32_t*>(p.ws + (int64_t)p.nwaves * 2 * slot_f) +
+                       (int64_t)w * kAttnHdrInts;
+  const u32x4 h0 = *reinterpret_cast<const u32x4*>(hdr);
+  if (h0[0] != 1u) return;
+  const u32x4 h1 = *reinterpret_cast<const u32x4*>(hdr + 4);
+  const int f = (int)h0[2], nt = (int)h0[3], P = (int)h1[0], q0 = (int)h1[1], n = (int)h1[2];
+  const int h = w % p.hkv, s0 = w / p.hkv;
+  const int C = min((f + nt - 1) / P, p.nshares - 1) - s0 + 1;   // contributing shares
+  const int R = p.group * n;
+  const int64_t mo = (int64_t)p.rmax * D, lo = mo + p.rmax;
+  auto slot = [&](int c) -> const float* {
+    return p.ws + ((int64_t)((s0 + c) * p.hkv + h) * 2 + (c == 0 ? 1 : 0)) * slot_f;
+  };
   for (int idx = threadIdx.x; idx < R * (D / 4); idx += blockDim.x) {
     const int r = idx / (D / 4), d = (idx % (D / 4)) * 4;
+    float M = kNegBig, den = 0.f;
     f32x4 o = {0.f, 0.f, 0.f, 0.f};
-    for (int c = 0; c < nch; ++c) {
-      const f32x4 a = *reinterpret_cast<const f32x4*>(base + c * slot_f + (int64_t)r * D + d);
-      o += a * w[c][r];
+    for (int c0 = 0; c0 < C; c0 += 4) {
+      float mv[4], lv[4];
+      f32x4 av[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float* sp = slot(min(c0 + k, C - 1));
+        mv[k] = sp[mo + r];
+        lv[k] = sp[lo + r];
+        av[k] = *reinterpret_cast<const f32x4*>(sp + (int64_t)r * D + d);
+      }
+      float mc = M;
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (c0 + k < C) mc = fmaxf(mc, mv[k]);
+      const float a = fast_exp2(M - mc);
+      den *= a;
+      o *= a;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (c0 + k >= C) continue;
+        const float e = fast_exp2(mv[k] - mc);
+        den += e * lv[k];
+        o += av[k] * e;
+      }
+      M = mc;
     }
-    const int j = r / p.group, g = r % p.group;
-    uint16_t* orow = reinterpret_cast<uint16_t*>(p.out) + ((int64_t)(q0 + j) * p.hq + kvh * p.group + g) * D;
-    u32x2 v;
-    v[0] = pack_bf16x2(o[0], o[1]);
-    v[1] = pack_bf16x2(o[2], o[3]);
-    *reinterpret_cast<u32x2*>(orow + d) = v;
+    const float inv = 1.0f / den;
+    const int j = r / p.group, gq = r % p.group;
+    uint16_t* orow = reinterpret_cast<uint16_t*>(p.out) + ((int64_t)(q0 + j) * p.hq + h * p.group + gq) * D;
+    u32x2 v2;
+    v2[0] = pack_bf16x2(o[0] * inv, o[1] * inv);
+    v2[1] = pack_bf16x2(o[2] * inv, o[3] * inv);
+    *reinterpret_cast<u32x2*>(orow + d) = v2;
   }
 }
 
 template <int D, int BS, int NT>
 static hipError_t launch_attn_t(const AttnParams& p, hipStream_t s) {
-  const int64_t grid = (int64_t)p.nch_max * p.num_seqs * p.hkv;
-  hipLaunchKernelGGL((verify_attn_kernel<D, BS, NT>), dim3((unsigned)grid), dim3(256), 0, s, p);
+  hipLaunchKernelGGL((verify_attn_kernel<D, BS, NT>), dim3((unsigned)(p.nwaves / 4)), dim3(256), 0, s, p);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || p.nch_max <= 1) return e;
-  hipLaunchKernelGGL((attn_merge_kernel<D>), dim3(p.num_seqs * p.hkv), dim3(256), 0, s, p);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((attn_merge_kernel<D>), dim3((unsigned)p.nwaves), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

@@ -25,18 +25,26 @@ struct AttnParams {
   const int32_t* block_tables;
   const void* q;
   void* out;
-  float* ws;             // split-KV partials: [B*Hkv*nch_max][rmax][D] acc, then m and l
+  float* ws;             // per-wave partial slots [nwaves][2][slot], then headers [nwaves][kAttnHdrInts]
   int num_blocks, hkv, block_size, head_dim, num_seqs, max_blocks, total_tokens;
   int hq, group;         // Hq, G = Hq / Hkv
   int rmax;              // G * max_query_len (rows per (sequence, KV head)), <= 64
-  int chunk;             // KV tokens per work item (multiple of 32)
-  int nch_max;           // chunks per sequence covered by the grid / workspace
+  int tiles_per_wave;    // 32-key tiles per share; 0: the even split of each head's tiles
+  int nshares;           // shares per KV head; wave s*hkv + h takes share s of head h
+  int nwaves;            // waves of the attention grid (4 per workgroup, >= nshares * hkv)
   float scale_log2e;     // scale * log2(e): scores live in the base-2 domain
 };
 
-// Workspace layout of the split-KV partials for one (sequence, KV head, chunk) slot.
+constexpr int kAttnHdrInts = 8;           // per-wave header of the partial an item's first wave leaves
+constexpr int kAttnMinTilesPerWave = 2;   // floor of the even split (short batches)
+constexpr int kAttnMaxWaves = 1024;       // waves of the even split: one per SIMD of 256 CUs
+
+// One partial slot: [rmax][D] unnormalised output, then rmax reference maxima and rmax sums.
 // Rounded up to 16 floats so that every slot starts 64-byte aligned.
 __host__ __device__ inline int64_t attn_slot_floats(int rmax, int D) { return ((int64_t)rmax * (D + 2) + 15) / 16 * 16; }
+__host__ __device__ inline int64_t attn_ws_bytes(int nwaves, int rmax, int D) {
+  return (int64_t)nwaves * (2 * attn_slot_floats(rmax, D) * 4 + kAttnHdrInts * 4);
+}
 
 struct AcceptParams {
   int kind;              // 0 probs, 1 logits

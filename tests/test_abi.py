@@ -62,10 +62,25 @@ def test_attention_validation():
 
 
 def test_workspace_queries():
-    # no split -> no workspace
-    assert sx.spexis_verify_attention_workspace_size(4, 8, 2, 64, 5, 256, 0) == 0
-    n = sx.spexis_verify_attention_workspace_size(64, 32, 8, 128, 5, 4100, 0)
-    assert n > 0 and n % 64 == 0
+    # attention: one header and two partial slots per wave; each KV head's tiles are cut into
+    # shares (the even split: about 1024 waves in all, at least 2 tiles a share; a fixed share
+    # size: enough shares for the largest possible stream), one wave per (share, head)
+    def expect(B, hq, hkv, D, mq, max_s, chunk):
+        rows = (hq // hkv) * mq
+        slot = -(-rows * (D + 2) // 16) * 16
+        tiles = B * -(-max_s // 32)
+        per = -(-chunk // 32) if chunk else 2
+        shares = -(-tiles // per)
+        if not chunk:
+            shares = min(shares, max(1, 1024 // hkv))
+        waves = -(-(shares * hkv) // 4) * 4
+        return waves * (2 * slot * 4 + 8 * 4)
+    for args in [(4, 8, 2, 64, 5, 256, 0), (64, 32, 8, 128, 5, 4100, 0), (64, 32, 8, 128, 5, 4100, 100),
+                 (1, 8, 8, 128, 1, 1, 0), (3, 64, 8, 128, 8, 16384, 4096)]:
+        n = sx.spexis_verify_attention_workspace_size(*args)
+        assert n == expect(*args) and n % 64 == 0, args
+    assert sx.spexis_verify_attention_workspace_size(64, 32, 8, 128, 5, 1 << 20, 0) <= 1024 * (2 * 2608 * 4 + 32)
+    assert sx.spexis_verify_attention_workspace_size(0, 32, 8, 128, 5, 4100, 0) == 0
     assert sx.spexis_accept_workspace_size(64, 128256, 4) > 64 * 32 * 8
 
 
