@@ -8,23 +8,23 @@
 //   threshold t = floor(u * sum W) from a 128-bit product
 //   token     the smallest m whose inclusive prefix of W exceeds t
 //
-// Kernels, in order on the caller's stream (kernel boundaries are the only synchronisation;
-// the one atomic appends a sequence to the next round's list):
-//   init      one thread per sequence: geometry, draft-id check; with probability inputs
-//             also the ratio tests.
-//   round i   (logit inputs, i = 0..max_k) one work item per (sequence still testing, 8
-//             sub-chunks of 4096 entries), one wave per sub-chunk.  An item first re-derives
-//             test i-1 from the row statistics round i-1 left (every item of a sequence
-//             reaches the same decision).  Accepted: it computes the statistics
-//             (max, sum of 2^(y - max)) of target row i and draft row i over its entries, and
-//             the sequence moves to round i+1 (or, at i = k, is done with the bonus row k).
-//             Rejected: it computes the residual maxima of row i-1 over its entries instead.
-//             Only rows a sequence reaches are read.  Statistics alternate between two
-//             buffers by round parity, so a round never overwrites what it reads.
+// Partial results are kept per sub-chunk of 4096 vocab entries, one workgroup per sub-chunk:
+// its four waves take 1024 entries each and combine in LDS in a fixed order, so every consumer
+// reads the same partials.  Kernels, in order on the caller's stream (kernel boundaries are
+// the only synchronisation):
+//   stats     (logit inputs) the statistics (max, sum of 2^(y - max)) of every row a test or
+//             the sample can use -- target rows 0..k and draft rows 0..k-1 of each sequence --
+//             all at once, per (row, sub-chunk).  The tests are independent of each other, so
+//             nothing here waits for a decision; the inputs of the tests are gathered here too.
+//   decide    (logit inputs) one workgroup per (sequence, sub-chunk): every workgroup of a
+//             sequence runs the ratio tests from those statistics (its waves split the
+//             positions) and reaches the same first rejection a; for a residual it then
+//             computes the residual maxima of row a over its sub-chunk.
+//   init      (probability inputs) one thread per sequence: geometry, draft-id check, tests.
 //   max pass  (probability inputs) per sub-chunk: max of the weights, max of p, bad flag.
 //   sum pass  per sub-chunk: sum of W_v.
-//   search    one wave per sequence: total, exact threshold, the sub-chunk holding it, the
-//             token inside that sub-chunk, outputs.
+//   search    one workgroup per sequence: total, exact threshold, the sub-chunk holding it,
+//             the token inside that sub-chunk (its four waves split the entries), outputs.
 #include <math.h>
 
 #include "common.h"
@@ -35,10 +35,11 @@ namespace spexis {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
-constexpr int kF4 = kAcceptSub / (kWave * 4);   // float4 loads per lane per sub-chunk (16)
-constexpr int kPerLane = 4 * kF4;                // vocab entries per lane per sub-chunk (64)
+constexpr int kWaveSub = kAcceptSub / kWaves;   // entries of a sub-chunk one wave takes (1024)
+constexpr int kF4 = kWaveSub / (kWave * 4);      // float4 loads per lane (4)
+constexpr int kPerLane = 4 * kF4;                // vocab entries per lane (16)
 
-enum Mode { kTesting = 0, kResidual = 1, kBonus = 2, kDone = 3 };
+enum Mode { kResidual = 1, kBonus = 2, kDone = 3 };
 
 struct Geom {
   int t0, d0, k, valid;
@@ -47,6 +48,20 @@ struct Geom {
 __device__ __forceinline__ Geom load_geom(const AcceptParams& p, int b) {
   const u32x4 v = *reinterpret_cast<const u32x4*>(p.geo + 4 * (int64_t)b);
   return Geom{(int)v[0], (int)v[1], (int)v[2], (int)v[3]};
+}
+
+// Rows of sequence b: first target row t0, first draft row d0, draft count k (clamped so that
+// every row index stays inside its buffer); n = its query tokens (the sequence is valid iff n >= 1).
+__device__ __forceinline__ Geom seq_geom(const AcceptParams& p, int b, int& n) {
+  const int a0 = clampi(p.qsl[b], 0, p.T);
+  const int a1 = clampi(p.qsl[b + 1], a0, p.T);
+  n = a1 - a0;
+  const int nd = p.T - p.B > 0 ? p.T - p.B : 0;
+  int k = n - 1;
+  if (k < 0) k = 0;
+  if (k > p.max_k) k = p.max_k;
+  if (k > nd) k = nd;   // only reachable with an inconsistent qsl: stay inside the draft rows
+  return Geom{a0, clampi(a0 - b, 0, nd - k), k, n >= 1 ? 1 : 0};
 }
 
 // p = 2^(x*c - M) * (1/Z): the probability of a logit, the same expression in every pass
@@ -101,13 +116,14 @@ __device__ __forceinline__ f32x4 load4(const float* row, int e, int V, bool vec,
   return r;
 }
 
-// One wave's coalesced view of sub-chunk `sub`: lane l holds entries sub*4096 + 256 j + 4 l + i.
-// A sub-chunk inside the row (all but the last of a row whose length is a multiple of 4) takes
-// the straight-line path, so all 16 loads are in flight together.
-__device__ __forceinline__ void load_sub(const float* row, int sub, int V, bool vec, float fill, int lane,
+// Wave `wave`'s coalesced part of sub-chunk `sub`: lane l holds entries
+// sub*4096 + 1024 wave + 256 j + 4 l + i.  A part inside the row takes the straight-line path,
+// so all its loads are in flight together.
+__device__ __forceinline__ void load_sub(const float* row, int sub, int wave, int V, bool vec, float fill, int lane,
                                          float (&v)[kPerLane]) {
-  if (vec && (sub + 1) * kAcceptSub <= V) {
-    const f32x4* src = reinterpret_cast<const f32x4*>(row + sub * kAcceptSub) + lane;
+  const int base = sub * kAcceptSub + wave * kWaveSub;
+  if (vec && base + kWaveSub <= V) {
+    const f32x4* src = reinterpret_cast<const f32x4*>(row + base) + lane;
 #pragma unroll
     for (int j = 0; j < kF4; ++j) {
       const f32x4 x = src[j * kWave];
@@ -118,43 +134,38 @@ __device__ __forceinline__ void load_sub(const float* row, int sub, int V, bool 
   }
 #pragma unroll
   for (int j = 0; j < kF4; ++j) {
-    const f32x4 x = load4(row, sub * kAcceptSub + j * 4 * kWave + 4 * lane, V, vec, fill);
+    const f32x4 x = load4(row, base + j * 4 * kWave + 4 * lane, V, vec, fill);
 #pragma unroll
     for (int i = 0; i < 4; ++i) v[4 * j + i] = x[i];
   }
 }
 
-// The 64 consecutive entries base .. base+63 of one lane (base % 4 == 0), same fast path.
-__device__ __forceinline__ void load_run(const float* row, int base, int V, bool vec, float fill,
-                                         float (&v)[kPerLane]) {
-  if (vec && base + kPerLane <= V) {
-    const f32x4* src = reinterpret_cast<const f32x4*>(row + base);
-#pragma unroll
-    for (int j = 0; j < kF4; ++j) {
-      const f32x4 x = src[j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) v[4 * j + i] = x[i];
-    }
-    return;
-  }
-#pragma unroll
-  for (int j = 0; j < kF4; ++j) {
-    const f32x4 x = load4(row, base + 4 * j, V, vec, fill);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[4 * j + i] = x[i];
-  }
+// The (max, sum) partial of lane l's first sub-chunk (x = l), loaded ahead of its reduction so
+// that a consumer can have all of its partial loads in flight at once.
+struct Part2 {
+  float a, b;
+};
+__device__ __forceinline__ Part2 part_first(const float* part, int nsub, int lane, float fa, float fb) {
+  if (lane >= nsub) return Part2{fa, fb};
+  const f32x2 v = *reinterpret_cast<const f32x2*>(part + 2 * lane);
+  return Part2{v[0], v[1]};
 }
 
 // Statistics of one logit row from its sub-chunk partials, combined in a fixed order by one
 // full wave (every consumer calls exactly this, so all of them get identical M and 1/Z, the
 // latter returned in Z).  A row without a finite maximum or with a bad sum gives Z = NaN.
-__device__ __forceinline__ void row_stats(const float* part, int nsub, int lane, float& M, float& Z) {
-  float mm = -INFINITY;
-  for (int x = lane; x < nsub; x += kWave) mm = fmaxf(mm, part[2 * x]);
+// `f` is part_first(part, ...) with fill (-inf, 0).
+__device__ __forceinline__ void row_stats(const float* part, int nsub, int lane, Part2 f, float& M, float& Z) {
+  float mm = f.a;
+  for (int x = lane + kWave; x < nsub; x += kWave) mm = fmaxf(mm, part[2 * x]);
   mm = wave_max(mm);
   float zz = 0.f;
   int nan = 0;
-  for (int x = lane; x < nsub; x += kWave) {
+  if (lane < nsub) {
+    nan |= f.b != f.b;
+    if (f.a != -INFINITY) zz += f.b * fast_exp2(f.a - mm);
+  }
+  for (int x = lane + kWave; x < nsub; x += kWave) {
     const float z = part[2 * x + 1];
     nan |= z != z;
     if (part[2 * x] != -INFINITY) zz += z * fast_exp2(part[2 * x] - mm);
@@ -165,8 +176,9 @@ __device__ __forceinline__ void row_stats(const float* part, int nsub, int lane,
   Z = (nan || !(mm > -INFINITY) || !(mm < INFINITY)) ? NAN : 1.0f / zz;   // reciprocal of the sum
 }
 
-__device__ __forceinline__ float* lse_slot(const AcceptParams& p, int parity, int which, int b) {
-  return p.lse_part + ((((int64_t)parity * 2 + which) * p.B + b) * p.nsub) * 2;
+// Sub-chunk statistics of row i of sequence b (which = 0 target, 1 draft).
+__device__ __forceinline__ float* lse_slot(const AcceptParams& p, int b, int i, int which) {
+  return p.lse_part + ((((int64_t)b * (p.max_k + 1) + i) * 2 + which) * p.nsub) * 2;
 }
 
 // Final outputs of sequence b (called by exactly one thread).
@@ -178,10 +190,21 @@ __device__ void write_outputs(const AcceptParams& p, int b, const Geom& g, int a
   if (p.seq_lens_inout) p.seq_lens_inout[b] -= g.k - a;
 }
 
-// Row context of the sampled row(s): target row a (P) and, for a residual, draft row a (Q).
+// Outputs of a sequence that samples nothing (called by exactly one thread).
+__device__ void write_invalid(const AcceptParams& p, int b, int n) {
+  int32_t* row = p.out_tokens + (int64_t)b * (p.max_k + 1);
+  for (int i = 0; i <= p.max_k; ++i) row[i] = -1;
+  p.accepted_len[b] = 0;
+  p.row_status[b] = n >= 1 ? SPEXIS_ROW_BAD_TOKEN : SPEXIS_ROW_BAD_VALUE;
+  p.st_mode[b] = kDone;
+  p.st_a[b] = 0;
+}
+
+// Row context of a tested or sampled position a: target row a (P) and, for a residual, draft
+// row a (Q), with their statistics in logits mode.
 struct RowCtx {
   const float* P;
-  const float* Q;     // nullptr for the bonus row
+  const float* Q;        // nullptr for the bonus row
   float Mp, Rp, Mq, Rq;  // row maxima (scaled) and reciprocal sums (logits mode)
   bool logits;
 };
@@ -191,13 +214,46 @@ __device__ __forceinline__ float prob_of(const RowCtx& r, float raw, float c, bo
   return draft ? logit_prob(raw, c, r.Mq, r.Rq) : logit_prob(raw, c, r.Mp, r.Rp);
 }
 
-// Residual / bonus maxima of one sub-chunk by one wave, written to max_part / bad_part.
-__device__ void sub_maxima(const AcceptParams& p, const RowCtx& r, bool residual, int b, int sub, int lane) {
+// Context of position a of sequence b (computed identically everywhere); `with_q` also takes
+// draft row a.  In logits mode both rows' partials are loaded before either is reduced.
+__device__ __forceinline__ RowCtx row_ctx(const AcceptParams& p, int b, const Geom& g, int a, bool with_q, int lane) {
+  RowCtx r;
+  r.P = p.target + (int64_t)(g.t0 + a) * p.V;
+  r.Q = with_q ? p.draft + (int64_t)(g.d0 + a) * p.V : nullptr;
+  r.logits = p.kind == 1;
+  r.Mp = r.Rp = r.Mq = r.Rq = 1.f;
+  if (r.logits) {
+    const float* lp = lse_slot(p, b, a, 0);
+    const float* lq = lse_slot(p, b, a, 1);
+    const Part2 fp = part_first(lp, p.nsub, lane, -INFINITY, 0.f);
+    const Part2 fq = with_q ? part_first(lq, p.nsub, lane, -INFINITY, 0.f) : Part2{-INFINITY, 0.f};
+    row_stats(lp, p.nsub, lane, fp, r.Mp, r.Rp);
+    if (with_q) row_stats(lq, p.nsub, lane, fq, r.Mq, r.Rq);
+  }
+  return r;
+}
+
+// Combines a value of each of the four waves in wave order through LDS; every thread gets the
+// result.  (All four waves must call it.)
+template <typename T, typename F>
+__device__ __forceinline__ T wg_combine(T v, int wave, int lane, F op) {
+  __shared__ T sm[kWaves];
+  if (lane == 0) sm[wave] = v;
+  __syncthreads();
+  T r = sm[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) r = op(r, sm[w]);
+  __syncthreads();   // sm may be reused by the next call
+  return r;
+}
+
+// Residual / bonus maxima of sub-chunk `sub` by one workgroup, written to max_part / bad_part.
+__device__ void sub_maxima(const AcceptParams& p, const RowCtx& r, bool residual, int b, int sub, int wave, int lane) {
   const bool vec = (p.V & 3) == 0;
   const float fill = r.logits ? -INFINITY : 0.f;
   float pv[kPerLane], qv[kPerLane];
-  load_sub(r.P, sub, p.V, vec, fill, lane, pv);
-  if (residual) load_sub(r.Q, sub, p.V, vec, fill, lane, qv);
+  load_sub(r.P, sub, wave, p.V, vec, fill, lane, pv);
+  if (residual) load_sub(r.Q, sub, wave, p.V, vec, fill, lane, qv);
   float mw = 0.f, mp = 0.f;
   int bad = 0;
 #pragma unroll
@@ -210,78 +266,68 @@ __device__ void sub_maxima(const AcceptParams& p, const RowCtx& r, bool residual
     mw = w > mw ? w : mw;
     mp = P > mp ? P : mp;
   }
-  mw = wave_max(mw);
-  mp = wave_max(mp);
-  bad = wave_or(bad);
-  if (lane == 0) {
-    p.max_part[((int64_t)b * p.nsub + sub) * 2] = mw;
-    p.max_part[((int64_t)b * p.nsub + sub) * 2 + 1] = mp;
+  mw = wg_combine(wave_max(mw), wave, lane, [](float x, float y) { return fmaxf(x, y); });
+  mp = wg_combine(wave_max(mp), wave, lane, [](float x, float y) { return fmaxf(x, y); });
+  bad = wg_combine(wave_or(bad), wave, lane, [](int x, int y) { return x | y; });
+  if (threadIdx.x == 0) {
+    *reinterpret_cast<f32x2*>(p.max_part + ((int64_t)b * p.nsub + sub) * 2) = f32x2{mw, mp};
     p.bad_part[(int64_t)b * p.nsub + sub] = bad;
   }
+}
+
+// Row maxima and bad flag of the sampled row (one wave; any reduction order gives the same).
+// Logit bonus rows have no max pass: their largest probability is 2^0 * (1/Z).
+__device__ __forceinline__ void sampled_maxima(const AcceptParams& p, const RowCtx& r, int b, bool residual, int lane,
+                                               float& MW, float& MP, int& bad) {
+  if (r.logits && !residual) {
+    MP = MW = r.Rp;   // 2^0 * (1/Z)
+    bad = !(MP > 0.f) || isinf(MP);
+    return;
+  }
+  MW = 0.f;
+  MP = 0.f;
+  bad = 0;
+  for (int x = lane; x < p.nsub; x += kWave) {
+    const f32x2 v = *reinterpret_cast<const f32x2*>(p.max_part + ((int64_t)b * p.nsub + x) * 2);
+    MW = fmaxf(MW, v[0]);
+    MP = fmaxf(MP, v[1]);
+    bad |= p.bad_part[(int64_t)b * p.nsub + x];
+  }
+  MW = wave_max(MW);
+  MP = wave_max(MP);
+  bad = wave_or(bad);
 }
 
 // ---------------------------------------------------------------------------------- init
 
 __global__ __launch_bounds__(kThreads) void accept_init_kernel(AcceptParams p) {
-  if (blockIdx.x == 0 && threadIdx.x < p.max_k + 2) p.counts[threadIdx.x] = 0;
   const int b = blockIdx.x * kThreads + threadIdx.x;
   if (b >= p.B) return;
-  const int a0 = clampi(p.qsl[b], 0, p.T);
-  const int a1 = clampi(p.qsl[b + 1], a0, p.T);
-  const int n = a1 - a0;
-  int nd = p.T - p.B;
-  if (nd < 0) nd = 0;
-  int k = n - 1;
-  if (k < 0) k = 0;
-  if (k > p.max_k) k = p.max_k;
-  if (k > nd) k = nd;   // only reachable with an inconsistent qsl: stay inside the draft rows
-  const Geom g{a0, clampi(a0 - b, 0, nd - k), k, 0};
+  int n;
+  const Geom g = seq_geom(p, b, n);
   bool ok = n >= 1;
   for (int i = 0; ok && i < g.k; ++i) {
     const int x = p.ids[g.d0 + i];
     ok = x >= 0 && x < p.V;
   }
   *reinterpret_cast<u32x4*>(p.geo + 4 * (int64_t)b) = u32x4{(uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k, ok ? 1u : 0u};
-  if (!ok) {
-    int32_t* row = p.out_tokens + (int64_t)b * (p.max_k + 1);
-    for (int i = 0; i <= p.max_k; ++i) row[i] = -1;
-    p.accepted_len[b] = 0;
-    p.row_status[b] = n >= 1 ? SPEXIS_ROW_BAD_TOKEN : SPEXIS_ROW_BAD_VALUE;
-    p.st_mode[b] = kDone;
-    p.st_a[b] = 0;
-    return;
+  if (!ok) return write_invalid(p, b, n);
+  int a = 0;
+  while (a < g.k) {
+    const int x = p.ids[g.d0 + a];
+    const double pp = (double)p.target[(int64_t)(g.t0 + a) * p.V + x];
+    const double qq = (double)p.draft[(int64_t)(g.d0 + a) * p.V + x];
+    const double u = (double)p.u_accept[g.d0 + a];
+    if (u * qq < pp) ++a; else break;
   }
-  if (p.kind == 0) {
-    int a = 0;
-    while (a < g.k) {
-      const int x = p.ids[g.d0 + a];
-      const double pp = (double)p.target[(int64_t)(g.t0 + a) * p.V + x];
-      const double qq = (double)p.draft[(int64_t)(g.d0 + a) * p.V + x];
-      const double u = (double)p.u_accept[g.d0 + a];
-      if (u * qq < pp) ++a; else break;
-    }
-    p.st_a[b] = a;
-    p.st_mode[b] = a < g.k ? kResidual : kBonus;
-  } else {
-    // the inputs of every test, gathered now so that a round needs no dependent gather
-    for (int i = 0; i < g.k; ++i) {
-      const int x = p.ids[g.d0 + i];
-      f32x4 t;
-      t[0] = p.target[(int64_t)(g.t0 + i) * p.V + x];
-      t[1] = p.draft[(int64_t)(g.d0 + i) * p.V + x];
-      t[2] = p.u_accept[g.d0 + i];
-      t[3] = 0.f;
-      *reinterpret_cast<f32x4*>(p.tin + ((int64_t)b * p.max_k + i) * 4) = t;
-    }
-    p.st_a[b] = 0;
-    p.st_mode[b] = kTesting;
-  }
+  p.st_a[b] = a;
+  p.st_mode[b] = a < g.k ? kResidual : kBonus;
 }
 
-// ---------------------------------------------------------------- logits: one test round
+// ------------------------------------------------------------------- logits: statistics
 
-// (max, sum of 2^(y - max)) of one wave's 64 entries per lane; NaN sum if a logit is NaN/+inf.
-__device__ __forceinline__ void sub_stats(float (&v)[kPerLane], float c, float& m, float& z) {
+// (max, sum of 2^(y - max)) of one wave's entries; NaN sum if a logit is NaN/+inf.
+__device__ __forceinline__ void wave_stats(float (&v)[kPerLane], float c, float& m, float& z) {
   m = -INFINITY;
   int bad = 0;
 #pragma unroll
@@ -301,135 +347,105 @@ __device__ __forceinline__ void sub_stats(float (&v)[kPerLane], float c, float& 
   if (bad) z = NAN;
 }
 
-__global__ __launch_bounds__(kThreads) void accept_round_kernel(AcceptParams p, int i) {
+__global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int nseq = i == 0 ? p.B : p.counts[i];
-  const int64_t total = (int64_t)nseq * p.ipr;
-  const bool vec = (p.V & 3) == 0;
-  for (int64_t item = blockIdx.x; item < total; item += gridDim.x) {
-    const int sidx = (int)(item / p.ipr);
-    const int part = (int)(item % p.ipr);
-    const int sub = part * kSubPerItem + wave;   // this wave's sub-chunk
-    const bool has = sub < p.nsub;
-    int b;
-    Geom g;
-    if (i == 0) {
-      b = sidx;
-      g = load_geom(p, b);
-      if (!g.valid) continue;
-    } else {
-      const u32x4 e = *reinterpret_cast<const u32x4*>(p.lists + ((int64_t)i * p.B + sidx) * 4);
-      b = (int)e[0];
-      g = Geom{(int)e[1], (int)e[2], (int)e[3], 1};
+  const int sub = blockIdx.x % p.nsub;
+  int r = blockIdx.x / p.nsub;
+  const int which = r & 1;
+  r >>= 1;
+  const int i = r % (p.max_k + 1), b = r / (p.max_k + 1);
+  int n;
+  const Geom g = seq_geom(p, b, n);
+  if (!g.valid || i > g.k || (which == 1 && i == g.k)) return;
+  if (which == 0 && i < g.k && sub == 0 && threadIdx.x == 0) {
+    // the inputs of test i, gathered here so that the decision needs no dependent gather
+    const int x = p.ids[g.d0 + i];
+    const bool ok = x >= 0 && x < p.V;
+    f32x4 t;
+    t[0] = ok ? p.target[(int64_t)(g.t0 + i) * p.V + x] : 0.f;
+    t[1] = ok ? p.draft[(int64_t)(g.d0 + i) * p.V + x] : 0.f;
+    t[2] = p.u_accept[g.d0 + i];
+    t[3] = ok ? 1.f : 0.f;
+    *reinterpret_cast<f32x4*>(p.tin + ((int64_t)b * p.max_k + i) * 4) = t;
+  }
+  const float* row = which ? p.draft + (int64_t)(g.d0 + i) * p.V : p.target + (int64_t)(g.t0 + i) * p.V;
+  float v[kPerLane];
+  load_sub(row, sub, wave, p.V, (p.V & 3) == 0, -INFINITY, lane, v);
+  float m, z;
+  wave_stats(v, p.c, m, z);
+  // the four waves in order: common maximum, rescaled sums; NaN stays NaN
+  __shared__ float sm_m[kWaves], sm_z[kWaves];
+  if (lane == 0) {
+    sm_m[wave] = m;
+    sm_z[wave] = z;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float M = sm_m[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) M = fmaxf(M, sm_m[w]);
+    float Z = 0.f;
+    bool nan = false;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      nan |= sm_z[w] != sm_z[w];
+      if (sm_m[w] != -INFINITY) Z += sm_z[w] * fast_exp2(sm_m[w] - M);
     }
-    bool reject = false;
-    RowCtx r;
-    if (i >= 1) {
-      // test i-1 from the statistics round i-1 left (same decision in every wave of every item)
-      const f32x4 t = *reinterpret_cast<const f32x4*>(p.tin + ((int64_t)b * p.max_k + i - 1) * 4);
-      r.P = p.target + (int64_t)(g.t0 + i - 1) * p.V;
-      r.Q = p.draft + (int64_t)(g.d0 + i - 1) * p.V;
-      r.logits = true;
-      row_stats(lse_slot(p, (i - 1) & 1, 0, b), p.nsub, lane, r.Mp, r.Rp);
-      row_stats(lse_slot(p, (i - 1) & 1, 1, b), p.nsub, lane, r.Mq, r.Rq);
-      const float pp = logit_prob(t[0], p.c, r.Mp, r.Rp);
-      const float qq = logit_prob(t[1], p.c, r.Mq, r.Rq);
-      reject = !((double)t[2] * (double)qq < (double)pp);
-    }
-    if (reject) {
-      // the sequence stops at a = i-1: residual maxima of row i-1 over this item's entries
-      if (has) sub_maxima(p, r, true, b, sub, lane);
-      if (part == 0 && threadIdx.x == 0) {
-        p.st_a[b] = i - 1;
-        p.st_mode[b] = kResidual;
-      }
-      continue;
-    }
-    // accepted (or i = 0): statistics of target row i, and of draft row i while i < k
-    const bool two = i < g.k;
-    if (has) {
-      float vt[kPerLane], vd[kPerLane];
-      load_sub(p.target + (int64_t)(g.t0 + i) * p.V, sub, p.V, vec, -INFINITY, lane, vt);
-      if (two) load_sub(p.draft + (int64_t)(g.d0 + i) * p.V, sub, p.V, vec, -INFINITY, lane, vd);
-      float m, z;
-      sub_stats(vt, p.c, m, z);
-      if (lane == 0) {
-        float* dst = lse_slot(p, i & 1, 0, b) + 2 * sub;
-        dst[0] = m;
-        dst[1] = z;
-      }
-      if (two) {
-        sub_stats(vd, p.c, m, z);
-        if (lane == 0) {
-          float* dst = lse_slot(p, i & 1, 1, b) + 2 * sub;
-          dst[0] = m;
-          dst[1] = z;
-        }
-      }
-    }
-    if (part == 0 && threadIdx.x == 0) {
-      if (two) {
-        const int pos = __hip_atomic_fetch_add(p.counts + i + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        *reinterpret_cast<u32x4*>(p.lists + ((int64_t)(i + 1) * p.B + pos) * 4) =
-            u32x4{(uint32_t)b, (uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k};
-      } else {
-        p.st_a[b] = g.k;
-        p.st_mode[b] = kBonus;
-      }
-    }
+    *reinterpret_cast<f32x2*>(lse_slot(p, b, i, which) + 2 * sub) = f32x2{M, nan ? NAN : Z};
   }
 }
 
-// Context of the sampled row of sequence b after the tests (computed identically everywhere).
-__device__ __forceinline__ RowCtx sampled_row(const AcceptParams& p, int b, const Geom& g, int a, bool residual,
-                                              int lane) {
-  RowCtx r;
-  r.P = p.target + (int64_t)(g.t0 + a) * p.V;
-  r.Q = residual ? p.draft + (int64_t)(g.d0 + a) * p.V : nullptr;
-  r.logits = p.kind == 1;
-  r.Mp = r.Rp = r.Mq = r.Rq = 1.f;
-  if (r.logits) {
-    row_stats(lse_slot(p, a & 1, 0, b), p.nsub, lane, r.Mp, r.Rp);
-    if (residual) row_stats(lse_slot(p, a & 1, 1, b), p.nsub, lane, r.Mq, r.Rq);
-  }
-  return r;
-}
+// ---------------------------------------------------------------------- logits: decide
 
-// Row maxima and bad flag of the sampled row (one wave; any reduction order gives the same).
-// Logit bonus rows have no max pass: their largest probability is 2^0 * (1/Z).
-__device__ __forceinline__ void sampled_maxima(const AcceptParams& p, const RowCtx& r, int b, bool residual, int lane,
-                                               float& MW, float& MP, int& bad) {
-  if (r.logits && !residual) {
-    MP = MW = r.Rp;   // 2^0 * (1/Z)
-    bad = !(MP > 0.f) || isinf(MP);
+__global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p) {
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int b = blockIdx.x / p.nsub, sub = blockIdx.x % p.nsub;
+  const bool lead = sub == 0 && threadIdx.x == 0;
+  int n;
+  const Geom g = seq_geom(p, b, n);
+  const f32x4* tin = reinterpret_cast<const f32x4*>(p.tin) + (int64_t)b * p.max_k;
+  int bad = !g.valid;
+  for (int i = lane; i < g.k; i += kWave) bad |= tin[i][3] != 1.f;
+  if (wave_or(bad)) {
+    if (lead) write_invalid(p, b, n);
     return;
   }
-  MW = 0.f;
-  MP = 0.f;
-  bad = 0;
-  for (int x = lane; x < p.nsub; x += kWave) {
-    MW = fmaxf(MW, p.max_part[((int64_t)b * p.nsub + x) * 2]);
-    MP = fmaxf(MP, p.max_part[((int64_t)b * p.nsub + x) * 2 + 1]);
-    bad |= p.bad_part[(int64_t)b * p.nsub + x];
+  // position i fails when !(u_i q_i(x_i) < p_i(x_i)) (NaN statistics fail); a = the first failure
+  __shared__ int sm_fail[kWaves];
+  int fail = g.k;
+  for (int i = wave; i < g.k; i += kWaves) {
+    const f32x4 t = tin[i];
+    const RowCtx r = row_ctx(p, b, g, i, true, lane);
+    const float pp = logit_prob(t[0], p.c, r.Mp, r.Rp);
+    const float qq = logit_prob(t[1], p.c, r.Mq, r.Rq);
+    if (!((double)t[2] * (double)qq < (double)pp)) {
+      fail = i;
+      break;
+    }
   }
-  MW = wave_max(MW);
-  MP = wave_max(MP);
-  bad = wave_or(bad);
+  if (lane == 0) sm_fail[wave] = fail;
+  __syncthreads();
+  const int a = min(min(sm_fail[0], sm_fail[1]), min(sm_fail[2], sm_fail[3]));
+  if (lead) {
+    *reinterpret_cast<u32x4*>(p.geo + 4 * (int64_t)b) = u32x4{(uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k, 1u};
+    p.st_a[b] = a;
+    p.st_mode[b] = a < g.k ? kResidual : kBonus;
+  }
+  // a residual needs the maxima of w = max(0, p_a - q_a); a logit bonus row needs no max pass
+  if (a < g.k) sub_maxima(p, row_ctx(p, b, g, a, true, lane), true, b, sub, wave, lane);
 }
 
 // ------------------------------------------------------------------- probability max pass
 
 __global__ __launch_bounds__(kThreads) void accept_max_kernel(AcceptParams p) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int b = blockIdx.x / p.ipr;
-  const int sub = (blockIdx.x % p.ipr) * kSubPerItem + wave;
+  const int b = blockIdx.x / p.nsub, sub = blockIdx.x % p.nsub;
   const int mode = p.st_mode[b];
   const int a = p.st_a[b];
   const Geom g = load_geom(p, b);
-  if ((mode != kResidual && mode != kBonus) || sub >= p.nsub) return;
+  if (mode != kResidual && mode != kBonus) return;
   const bool residual = mode == kResidual;
-  const RowCtx r = sampled_row(p, b, g, a, residual, lane);
-  sub_maxima(p, r, residual, b, sub, lane);
+  sub_maxima(p, row_ctx(p, b, g, a, residual, lane), residual, b, sub, wave, lane);
 }
 
 // ------------------------------------------------------------------------------ sum pass
@@ -449,14 +465,19 @@ __device__ __forceinline__ uint64_t entry_weight(const RowCtx& r, float c, float
 
 __global__ __launch_bounds__(kThreads) void accept_sum_kernel(AcceptParams p) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int b = blockIdx.x / p.ipr;
-  const int sub = (blockIdx.x % p.ipr) * kSubPerItem + wave;
+  const int b = blockIdx.x / p.nsub, sub = blockIdx.x % p.nsub;
   const int mode = p.st_mode[b];
   const int a = p.st_a[b];
   const Geom g = load_geom(p, b);
-  if ((mode != kResidual && mode != kBonus) || sub >= p.nsub) return;
+  if (mode != kResidual && mode != kBonus) return;
   const bool residual = mode == kResidual;
-  const RowCtx r = sampled_row(p, b, g, a, residual, lane);
+  const bool vec = (p.V & 3) == 0;
+  const float fill = p.kind == 1 ? -INFINITY : 0.f;
+  // the entries first: their loads overlap the reductions of the row statistics and maxima
+  float pv[kPerLane], qv[kPerLane];
+  load_sub(p.target + (int64_t)(g.t0 + a) * p.V, sub, wave, p.V, vec, fill, lane, pv);
+  if (residual) load_sub(p.draft + (int64_t)(g.d0 + a) * p.V, sub, wave, p.V, vec, fill, lane, qv);
+  const RowCtx r = row_ctx(p, b, g, a, residual, lane);
   float MW, MP;
   int bad;
   sampled_maxima(p, r, b, residual, lane, MW, MP, bad);
@@ -464,30 +485,25 @@ __global__ __launch_bounds__(kThreads) void accept_sum_kernel(AcceptParams p) {
   const float M = use_p ? MP : MW;
   if (bad || !(M > 0.f)) return;                // the search kernel writes these outputs
   const int s = 40 - floor_log2(M);
-  const bool vec = (p.V & 3) == 0;
-  const float fill = r.logits ? -INFINITY : 0.f;
-  float pv[kPerLane], qv[kPerLane];
-  load_sub(r.P, sub, p.V, vec, fill, lane, pv);
-  if (!use_p) load_sub(r.Q, sub, p.V, vec, fill, lane, qv);
   uint64_t sum = 0;
 #pragma unroll
   for (int e = 0; e < kPerLane; ++e) sum += entry_weight(r, p.c, pv[e], use_p ? 0.f : qv[e], use_p, s);
-  sum = wave_sum_u64(sum);
-  if (lane == 0) p.sum_part[(int64_t)b * p.nsub + sub] = sum;
+  sum = wg_combine(wave_sum_u64(sum), wave, lane, [](uint64_t x, uint64_t y) { return x + y; });
+  if (threadIdx.x == 0) p.sum_part[(int64_t)b * p.nsub + sub] = sum;
 }
 
 // -------------------------------------------------------------------------------- search
 
 __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int b = blockIdx.x * kWaves + wave;
-  if (b >= p.B) return;
+  const int b = blockIdx.x;
   const int mode = p.st_mode[b];
   const int a = p.st_a[b];
   const Geom g = load_geom(p, b);
   if (mode != kResidual && mode != kBonus) return;
   const bool residual = mode == kResidual;
-  const RowCtx r = sampled_row(p, b, g, a, residual, lane);
+  // every wave takes the same decisions from the same partials
+  const RowCtx r = row_ctx(p, b, g, a, residual, lane);
   float MW, MP;
   int bad;
   sampled_maxima(p, r, b, residual, lane, MW, MP, bad);
@@ -497,14 +513,15 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
   const int c_lo = min(p.nsub, lane * per), c_hi = min(p.nsub, c_lo + per);
   uint64_t own = 0;
   for (int x = c_lo; x < c_hi; ++x) own += sums[x];
+  const bool lead = threadIdx.x == 0;
   if (bad) {
-    if (lane == 0) write_outputs(p, b, g, a, -1, SPEXIS_ROW_BAD_VALUE);
+    if (lead) write_outputs(p, b, g, a, -1, SPEXIS_ROW_BAD_VALUE);
     return;
   }
   const bool use_p = !residual || MW == 0.f;
   const float M = use_p ? MP : MW;
   if (!(M > 0.f)) {
-    if (lane == 0) write_outputs(p, b, g, a, -1, SPEXIS_ROW_EMPTY);
+    if (lead) write_outputs(p, b, g, a, -1, SPEXIS_ROW_EMPTY);
     return;
   }
   const int s = 40 - floor_log2(M);
@@ -538,16 +555,25 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
   cstar = __shfl(cstar, src, kWave);
   tt = __shfl(tt, src, kWave);
   if (cstar < 0) return;   // unreachable: S > 0 because M > 0 gives a weight >= 2^40
-  // lane l owns entries cstar*4096 + 64 l .. + 63 of the sub-chunk, in order
-  const int base = cstar * kAcceptSub + kPerLane * lane;
-  float pv[kPerLane], qv[kPerLane];
-  load_run(r.P, base, p.V, vec, fill, pv);
-  if (!use_p) load_run(r.Q, base, p.V, vec, fill, qv);
-  uint64_t wv[kPerLane];
+  // wave w owns entries cstar*4096 + 1024 w .. + 1023 of the sub-chunk, lane l 16 of them, in order
+  constexpr int kRun = kAcceptSub / (kWaves * kWave);   // 16
+  const int base = cstar * kAcceptSub + kRun * (kWave * wave + lane);
+  float pv[kRun], qv[kRun];
+#pragma unroll
+  for (int j = 0; j < kRun / 4; ++j) {
+    const f32x4 x = load4(r.P, base + 4 * j, p.V, vec, fill);
+    const f32x4 y = use_p ? f32x4{0.f, 0.f, 0.f, 0.f} : load4(r.Q, base + 4 * j, p.V, vec, fill);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      pv[4 * j + i] = x[i];
+      qv[4 * j + i] = y[i];
+    }
+  }
+  uint64_t wv[kRun];
   uint64_t mine = 0;
 #pragma unroll
-  for (int e = 0; e < kPerLane; ++e) {
-    wv[e] = entry_weight(r, p.c, pv[e], use_p ? 0.f : qv[e], use_p, s);
+  for (int e = 0; e < kRun; ++e) {
+    wv[e] = entry_weight(r, p.c, pv[e], qv[e], use_p, s);
     mine += wv[e];
   }
   uint64_t inc2 = mine;
@@ -556,11 +582,16 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
     const uint64_t y = __shfl_up(inc2, o, kWave);
     if (lane >= o) inc2 += y;
   }
+  __shared__ uint64_t sm_tot[kWaves];
+  if (lane == kWave - 1) sm_tot[wave] = inc2;
+  __syncthreads();
   uint64_t pre = inc2 - mine;
-  if (pre <= tt && tt < inc2) {
+  for (int w = 0; w < wave; ++w) pre += sm_tot[w];
+  const uint64_t hi = pre + mine;
+  if (pre <= tt && tt < hi) {
     int token = base;
 #pragma unroll
-    for (int e = 0; e < kPerLane; ++e) {
+    for (int e = 0; e < kRun; ++e) {
       if (tt < pre + wv[e]) {
         token = base + e;
         break;
@@ -626,24 +657,23 @@ hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V
 }
 
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
-  hipLaunchKernelGGL(accept_init_kernel, dim3((p.B + kThreads - 1) / kThreads), dim3(kThreads), 0, s, p);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const unsigned items = (unsigned)((int64_t)p.B * p.ipr);
+  const unsigned items = (unsigned)((int64_t)p.B * p.nsub);
+  hipError_t e;
   if (p.kind == 1) {
-    // bounded grid: the work items of the sequences still testing are strided over it
-    const unsigned grid = items < 2048 ? items : 2048;
-    for (int i = 0; i <= p.max_k; ++i) {
-      hipLaunchKernelGGL(accept_round_kernel, dim3(grid), dim3(kThreads), 0, s, p, i);
-      if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
+    const unsigned rows = (unsigned)((int64_t)p.B * (p.max_k + 1) * 2 * p.nsub);
+    hipLaunchKernelGGL(accept_stats_kernel, dim3(rows), dim3(kThreads), 0, s, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(accept_decide_kernel, dim3(items), dim3(kThreads), 0, s, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
   } else {
+    hipLaunchKernelGGL(accept_init_kernel, dim3((p.B + kThreads - 1) / kThreads), dim3(kThreads), 0, s, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(accept_max_kernel, dim3(items), dim3(kThreads), 0, s, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   hipLaunchKernelGGL(accept_sum_kernel, dim3(items), dim3(kThreads), 0, s, p);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(accept_search_kernel, dim3((p.B + kWaves - 1) / kWaves), dim3(kThreads), 0, s, p);
+  hipLaunchKernelGGL(accept_search_kernel, dim3(p.B), dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }
 

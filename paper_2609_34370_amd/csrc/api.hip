@@ -65,7 +65,7 @@ bool attn_waves(int32_t num_seqs, int32_t num_kv_heads, int32_t max_seq_len, int
 }
 
 struct AcceptLayout {
-  size_t geo, st_a, st_mode, counts, lists, tin, lse, max_part, bad_part, sum_part, total;
+  size_t geo, st_a, st_mode, lse, tin, max_part, bad_part, sum_part, total;
 };
 
 int64_t accept_nsub(int64_t V) { return (V + spexis::kAcceptSub - 1) / spexis::kAcceptSub; }
@@ -82,10 +82,8 @@ AcceptLayout accept_layout(int64_t B, int64_t V, int64_t max_k) {
   l.geo = take(B * 16);
   l.st_a = take(B * 4);
   l.st_mode = take(B * 4);
-  l.counts = take((max_k + 2) * 4);
-  l.lists = take((max_k + 1) * B * 4 * 4);
+  l.lse = take(B * (max_k + 1) * 2 * ns * 2 * 4);
   l.tin = take(B * (max_k > 0 ? max_k : 1) * 4 * 4);
-  l.lse = take(2 * 2 * B * ns * 2 * 4);
   l.max_part = take(B * ns * 2 * 4);
   l.bad_part = take(B * ns * 4);
   l.sum_part = take(B * ns * 8);
@@ -240,8 +238,7 @@ int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, 
     return fail(SPEXIS_ERR_WORKSPACE_TOO_SMALL, "spexis_accept: workspace %zu bytes < %zu needed", workspace_bytes,
                 lay.total);
   const int64_t nsub = accept_nsub(vocab);
-  const int64_t ipr = (nsub + spexis::kSubPerItem - 1) / spexis::kSubPerItem;
-  if ((int64_t)num_seqs * ipr >= (1ll << 31))
+  if ((int64_t)num_seqs * (max_k + 1) * 2 * nsub >= (1ll << 31))
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_accept: grid too large");
   char* ws = static_cast<char*>(workspace);
   spexis::AcceptParams p{};
@@ -251,7 +248,6 @@ int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, 
   p.max_k = max_k;
   p.T = total_tokens;
   p.nsub = (int)nsub;
-  p.ipr = (int)ipr;
   p.c = kind == SPEXIS_INPUT_LOGITS ? (float)(1.4426950408889634 / (double)temperature) : 1.f;
   p.qsl = query_start_loc;
   p.target = target;
@@ -266,10 +262,8 @@ int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, 
   p.geo = reinterpret_cast<int32_t*>(ws + lay.geo);
   p.st_a = reinterpret_cast<int32_t*>(ws + lay.st_a);
   p.st_mode = reinterpret_cast<int32_t*>(ws + lay.st_mode);
-  p.counts = reinterpret_cast<int32_t*>(ws + lay.counts);
-  p.lists = reinterpret_cast<int32_t*>(ws + lay.lists);
-  p.tin = reinterpret_cast<float*>(ws + lay.tin);
   p.lse_part = reinterpret_cast<float*>(ws + lay.lse);
+  p.tin = reinterpret_cast<float*>(ws + lay.tin);
   p.max_part = reinterpret_cast<float*>(ws + lay.max_part);
   p.bad_part = reinterpret_cast<int32_t*>(ws + lay.bad_part);
   p.sum_part = reinterpret_cast<uint64_t*>(ws + lay.sum_part);

@@ -50,7 +50,6 @@ struct AcceptParams {
   int kind;              // 0 probs, 1 logits
   int B, V, max_k, T;
   int nsub;              // ceil(V / kAcceptSub): partial results are kept per sub-chunk
-  int ipr;               // ceil(nsub / kSubPerItem): work items per sequence
   float c;               // log2(e) / temperature (logits mode)
   const int32_t* qsl;
   const float* target;
@@ -65,19 +64,16 @@ struct AcceptParams {
   // workspace views
   int32_t* geo;          // [B][4] first target row, first draft row, k, valid
   int32_t* st_a;         // [B] final a_b
-  int32_t* st_mode;      // [B] 0 testing, 1 residual, 2 bonus, 3 done (outputs written)
-  int32_t* counts;       // [max_k+2] sequences still testing when round i starts (logits mode)
-  int32_t* lists;        // [max_k+1][B][4] those sequences: b, first target row, first draft row, k
-  float* tin;            // [B][max_k][4] test inputs of position i: target logit and draft logit
-                         // of x_i, u_i (logits mode; gathered by the init kernel)
-  float* lse_part;       // [2 round parity][2 row kind][B][nsub][2] (max, sum of 2^(y-max))
+  int32_t* st_mode;      // [B] 1 residual, 2 bonus, 3 done (outputs written)
+  float* lse_part;       // [B][max_k+1][2 target/draft][nsub][2] (max, sum of 2^(y-max)) (logits mode)
+  float* tin;            // [B][max_k][4] test inputs of position i: target and draft logit of x_i,
+                         // u_i, and 1 if x_i is a valid id (logits mode; gathered by the stats pass)
   float* max_part;       // [B][nsub][2] (max w, max p) of the sampled row(s)
   int32_t* bad_part;     // [B][nsub]
   uint64_t* sum_part;    // [B][nsub]
 };
 
-constexpr int kAcceptSub = 4096;     // vocab entries per partial result (one wave's share)
-constexpr int kSubPerItem = 4;       // sub-chunks per work item (one per wave of a workgroup)
+constexpr int kAcceptSub = 4096;     // vocab entries per partial result (one workgroup's share)
 
 hipError_t launch_append(const AppendParams& p, hipStream_t s);
 hipError_t launch_attention(const AttnParams& p, hipStream_t s);
