@@ -92,7 +92,17 @@ def main():
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--kv-chunk", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="first copy BYTES device-to-device 3 times (a known-size kernel for counter calibration)")
+    ap.add_argument("--ingest-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/traffic.json from two rocprofv3 --pmc counter_collection.csv files "
+                         "(FETCH_SIZE, WRITE_SIZE) of runs with --copy-probe N (pass the same N); needs no GPU")
     args = ap.parse_args()
+    if args.ingest_traffic:
+        if args.copy_probe <= 0:
+            raise SystemExit("--ingest-traffic needs --copy-probe N: the copy size the counter runs used")
+        ingest_traffic(*args.ingest_traffic, workload=args.workload, copy_bytes=args.copy_probe)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
@@ -118,6 +128,13 @@ def main():
                                              attn.new_v.cpu())
     step = VerifyStep(batch, attn, acc, kv_chunk_tokens=args.kv_chunk, kind=sx.SPEXIS_INPUT_LOGITS)
     stream = torch.cuda.current_stream()
+    if args.copy_probe > 0:
+        src = torch.empty(args.copy_probe, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     for _ in range(args.warmup):
         step.run()
@@ -196,11 +213,55 @@ def main():
     print(json.dumps(line), flush=True)
 
 
+ATTN_KERNELS = ("verify_attn_kernel", "attn_merge_kernel")   # the launches of spexis_verify_attention
+COPY_KERNEL = "copyBuffer"
+
+
+def ingest_traffic(fetch_csv: str, write_csv: str, workload: int, copy_bytes: int) -> None:
+    """HBM bytes per spexis_verify_attention call from two counter runs of
+    `bench.py --copy-probe N`: each counter's KiB per dispatch, summed over the call's kernels,
+    averaged over the dispatches, and scaled by N / (the counter's reading for one copy of N
+    bytes), so that a plain copy reads and writes exactly N bytes."""
+    import csv
+
+    def per_kernel(path, counter):
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        out = {}
+        for r in rows:
+            out.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]) * 1024.0)
+        return out
+
+    result = {}
+    for name, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        k = per_kernel(path, name)
+        copies = [v for n, vals in k.items() if COPY_KERNEL in n for v in vals]
+        if not copies:
+            raise SystemExit(f"{path}: no {COPY_KERNEL} dispatch; run the profile with --copy-probe N")
+        probe = max(copies)   # the 3 probe copies are the largest copies of the run
+        size = copy_bytes
+        factor = size / probe
+        attn = sum(float(np.mean(vals)) for n, vals in k.items() if any(a in n for a in ATTN_KERNELS))
+        result[name] = {"raw_bytes_per_call": attn, "copy_reading": probe, "copy_bytes": size,
+                        "factor": factor, "bytes_per_call": attn * factor}
+    total = result["FETCH_SIZE"]["bytes_per_call"] + result["WRITE_SIZE"]["bytes_per_call"]
+    prof = os.path.join(ROOT, "profiles", "traffic.json")
+    data = json.load(open(prof)) if os.path.exists(prof) else {}
+    data[f"workload{workload}"] = {"source_digest": _kernel_digest(), "bytes_per_launch": round(total),
+                                   "counters": result, "kernels": list(ATTN_KERNELS)}
+    with open(prof, "w") as f:
+        json.dump(data, f, indent=1)
+        f.write("\n")
+    print(json.dumps(data[f"workload{workload}"], indent=1))
+
+
 def _kernel_digest() -> str:
+    """Digest of the sources the attention kernels are built from: a stored traffic figure is
+    used only while they are unchanged."""
     import hashlib
     h = hashlib.sha256()
-    with open(os.path.join(ROOT, "paper_2609_34370_amd", "csrc", "attention.hip"), "rb") as f:
-        h.update(f.read())
+    for name in ("attention.hip", "common.h"):
+        with open(os.path.join(ROOT, "paper_2609_34370_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()[:16]
 
 
