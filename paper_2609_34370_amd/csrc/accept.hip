@@ -12,14 +12,17 @@
 // its four waves take 1024 entries each and combine in LDS in a fixed order, so every consumer
 // reads the same partials.  Kernels, in order on the caller's stream (kernel boundaries are
 // the only synchronisation):
-//   stats     (logit inputs) the statistics (max, sum of 2^(y - max)) of every row a test or
-//             the sample can use -- target rows 0..k and draft rows 0..k-1 of each sequence --
-//             all at once, per (row, sub-chunk).  The tests are independent of each other, so
-//             nothing here waits for a decision; the inputs of the tests are gathered here too.
-//   decide    (logit inputs) one workgroup per (sequence, sub-chunk): every workgroup of a
-//             sequence runs the ratio tests from those statistics (its waves split the
-//             positions) and reaches the same first rejection a; for a residual it then
-//             computes the residual maxima of row a over its sub-chunk.
+//   rounds    (logit inputs) the tests run in rounds of doubling width, positions {0,1},
+//             {2..5}, {6..13}, ... (one round for small batches); a round takes only the
+//             sequences that passed every test before it (a device-side list), so rows past a
+//             rejection are rarely read.
+//     stats   the statistics (max, sum of 2^(y - max)) of the round's target and draft rows,
+//             per (row, sub-chunk), and the inputs of its tests.  The tests of a round are
+//             independent of each other, so nothing here waits for a decision.
+//     decide  one work item per (sequence, sub-chunk): every item of a sequence runs the
+//             round's tests from those statistics (its waves split the positions) and reaches
+//             the same first failure a; then it computes the residual maxima of row a over
+//             its sub-chunk, or marks the bonus row, or puts the sequence on the next list.
 //   init      (probability inputs) one thread per sequence: geometry, draft-id check, tests.
 //   max pass  (probability inputs) per sub-chunk: max of the weights, max of p, bad flag.
 //   sum pass  per sub-chunk: sum of W_v.
@@ -38,6 +41,8 @@ constexpr int kWaves = kThreads / kWave;
 constexpr int kWaveSub = kAcceptSub / kWaves;   // entries of a sub-chunk one wave takes (1024)
 constexpr int kF4 = kWaveSub / (kWave * 4);      // float4 loads per lane (4)
 constexpr int kPerLane = 4 * kF4;                // vocab entries per lane (16)
+constexpr int kRoundGrid = 65536;                // workgroups of a later test round (256 per CU)
+constexpr int64_t kOneRoundBytes = 192ll << 20;  // target rows that one test round reads whole
 
 enum Mode { kResidual = 1, kBonus = 2, kDone = 3 };
 
@@ -347,92 +352,144 @@ __device__ __forceinline__ void wave_stats(float (&v)[kPerLane], float c, float&
   if (bad) z = NAN;
 }
 
-__global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p) {
+// Sequence li of round r's list: all sequences in round 0, the ones still accepting after.
+__device__ __forceinline__ void round_seq(const AcceptParams& p, int r, int li, int& b, Geom& g, int& n) {
+  if (r == 0) {
+    b = li;
+    g = seq_geom(p, b, n);
+    return;
+  }
+  const u32x4 e = *reinterpret_cast<const u32x4*>(p.lists + ((int64_t)(r - 1) * p.B + li) * 4);
+  b = (int)e[0];
+  g = Geom{(int)e[1], (int)e[2], (int)e[3], 1};
+  n = g.k + 1;
+}
+
+__device__ __forceinline__ int round_count(const AcceptParams& p, int r) { return r == 0 ? p.B : p.counts[r]; }
+
+// Round r, positions [lo, hi): statistics of target rows lo..min(hi-1, k) and draft rows
+// lo..min(hi, k)-1 of every sequence in the round's list, per (row, sub-chunk), and the inputs
+// of the tests at those positions.  Work items are strided over a bounded grid (the host does
+// not know how many sequences reach the round).
+__global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p, int r, int lo, int hi) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int sub = blockIdx.x % p.nsub;
-  int r = blockIdx.x / p.nsub;
-  const int which = r & 1;
-  r >>= 1;
-  const int i = r % (p.max_k + 1), b = r / (p.max_k + 1);
-  int n;
-  const Geom g = seq_geom(p, b, n);
-  if (!g.valid || i > g.k || (which == 1 && i == g.k)) return;
-  if (which == 0 && i < g.k && sub == 0 && threadIdx.x == 0) {
-    // the inputs of test i, gathered here so that the decision needs no dependent gather
-    const int x = p.ids[g.d0 + i];
-    const bool ok = x >= 0 && x < p.V;
-    f32x4 t;
-    t[0] = ok ? p.target[(int64_t)(g.t0 + i) * p.V + x] : 0.f;
-    t[1] = ok ? p.draft[(int64_t)(g.d0 + i) * p.V + x] : 0.f;
-    t[2] = p.u_accept[g.d0 + i];
-    t[3] = ok ? 1.f : 0.f;
-    *reinterpret_cast<f32x4*>(p.tin + ((int64_t)b * p.max_k + i) * 4) = t;
-  }
-  const float* row = which ? p.draft + (int64_t)(g.d0 + i) * p.V : p.target + (int64_t)(g.t0 + i) * p.V;
-  float v[kPerLane];
-  load_sub(row, sub, wave, p.V, (p.V & 3) == 0, -INFINITY, lane, v);
-  float m, z;
-  wave_stats(v, p.c, m, z);
-  // the four waves in order: common maximum, rescaled sums; NaN stays NaN
+  if (r == 0 && blockIdx.x == 0 && threadIdx.x <= kAcceptMaxRounds) p.counts[threadIdx.x] = 0;
+  const int rows = 2 * (hi - lo);
+  const int64_t total = (int64_t)round_count(p, r) * rows * p.nsub;
   __shared__ float sm_m[kWaves], sm_z[kWaves];
-  if (lane == 0) {
-    sm_m[wave] = m;
-    sm_z[wave] = z;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    float M = sm_m[0];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) M = fmaxf(M, sm_m[w]);
-    float Z = 0.f;
-    bool nan = false;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      nan |= sm_z[w] != sm_z[w];
-      if (sm_m[w] != -INFINITY) Z += sm_z[w] * fast_exp2(sm_m[w] - M);
+  for (int64_t item = blockIdx.x; item < total; item += gridDim.x) {
+    const int sub = (int)(item % p.nsub);
+    const int64_t rest = item / p.nsub;
+    const int rr = (int)(rest % rows), li = (int)(rest / rows);
+    const int pos = lo + (rr >> 1), which = rr & 1;
+    int b, n;
+    Geom g;
+    round_seq(p, r, li, b, g, n);
+    if (!g.valid || pos > g.k || (which == 1 && pos == g.k)) continue;
+    if (which == 0 && pos < g.k && sub == 0 && threadIdx.x == 0) {
+      // the inputs of test pos, gathered here so that the decision needs no dependent gather
+      const int x = p.ids[g.d0 + pos];
+      const bool ok = x >= 0 && x < p.V;
+      f32x4 t;
+      t[0] = ok ? p.target[(int64_t)(g.t0 + pos) * p.V + x] : 0.f;
+      t[1] = ok ? p.draft[(int64_t)(g.d0 + pos) * p.V + x] : 0.f;
+      t[2] = p.u_accept[g.d0 + pos];
+      t[3] = ok ? 1.f : 0.f;
+      *reinterpret_cast<f32x4*>(p.tin + ((int64_t)b * p.max_k + pos) * 4) = t;
     }
-    *reinterpret_cast<f32x2*>(lse_slot(p, b, i, which) + 2 * sub) = f32x2{M, nan ? NAN : Z};
+    const float* row = which ? p.draft + (int64_t)(g.d0 + pos) * p.V : p.target + (int64_t)(g.t0 + pos) * p.V;
+    float v[kPerLane];
+    load_sub(row, sub, wave, p.V, (p.V & 3) == 0, -INFINITY, lane, v);
+    float m, z;
+    wave_stats(v, p.c, m, z);
+    // the four waves in order: common maximum, rescaled sums; NaN stays NaN
+    if (lane == 0) {
+      sm_m[wave] = m;
+      sm_z[wave] = z;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float M = sm_m[0];
+#pragma unroll
+      for (int w = 1; w < kWaves; ++w) M = fmaxf(M, sm_m[w]);
+      float Z = 0.f;
+      bool nan = false;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        nan |= sm_z[w] != sm_z[w];
+        if (sm_m[w] != -INFINITY) Z += sm_z[w] * fast_exp2(sm_m[w] - M);
+      }
+      *reinterpret_cast<f32x2*>(lse_slot(p, b, pos, which) + 2 * sub) = f32x2{M, nan ? NAN : Z};
+    }
+    __syncthreads();
   }
 }
 
-// ---------------------------------------------------------------------- logits: decide
-
-__global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p) {
+// Round r, positions [lo, hi): one work item per (sequence of the list, sub-chunk).  Every item
+// of a sequence runs the tests at those positions (its waves split them) and reaches the same
+// first failure.  A failure at a: the sequence is done testing (residual at a), and the item
+// computes the residual maxima of row a over its sub-chunk.  No failure: the bonus row if the
+// round reached position k, else the sequence joins round r+1's list.
+__global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p, int r, int lo, int hi) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int b = blockIdx.x / p.nsub, sub = blockIdx.x % p.nsub;
-  const bool lead = sub == 0 && threadIdx.x == 0;
-  int n;
-  const Geom g = seq_geom(p, b, n);
-  const f32x4* tin = reinterpret_cast<const f32x4*>(p.tin) + (int64_t)b * p.max_k;
-  int bad = !g.valid;
-  for (int i = lane; i < g.k; i += kWave) bad |= tin[i][3] != 1.f;
-  if (wave_or(bad)) {
-    if (lead) write_invalid(p, b, n);
-    return;
-  }
-  // position i fails when !(u_i q_i(x_i) < p_i(x_i)) (NaN statistics fail); a = the first failure
+  const int64_t total = (int64_t)round_count(p, r) * p.nsub;
   __shared__ int sm_fail[kWaves];
-  int fail = g.k;
-  for (int i = wave; i < g.k; i += kWaves) {
-    const f32x4 t = tin[i];
-    const RowCtx r = row_ctx(p, b, g, i, true, lane);
-    const float pp = logit_prob(t[0], p.c, r.Mp, r.Rp);
-    const float qq = logit_prob(t[1], p.c, r.Mq, r.Rq);
-    if (!((double)t[2] * (double)qq < (double)pp)) {
-      fail = i;
-      break;
+  for (int64_t item = blockIdx.x; item < total; item += gridDim.x) {
+    const int sub = (int)(item % p.nsub), li = (int)(item / p.nsub);
+    const bool lead = sub == 0 && threadIdx.x == 0;
+    int b, n;
+    Geom g;
+    round_seq(p, r, li, b, g, n);
+    if (r == 0) {
+      int bad = !g.valid;
+      for (int i = lane; i < g.k; i += kWave) {
+        const int x = p.ids[g.d0 + i];
+        bad |= x < 0 || x >= p.V;
+      }
+      if (wave_or(bad)) {
+        if (lead) write_invalid(p, b, n);
+        continue;
+      }
+    }
+    // position i fails when !(u_i q_i(x_i) < p_i(x_i)) (NaN statistics fail)
+    const f32x4* tin = reinterpret_cast<const f32x4*>(p.tin) + (int64_t)b * p.max_k;
+    const int end = min(hi, g.k);
+    int fail = g.k + 1;   // none
+    for (int i = lo + wave; i < end; i += kWaves) {
+      const f32x4 t = tin[i];
+      const RowCtx rc = row_ctx(p, b, g, i, true, lane);
+      const float pp = logit_prob(t[0], p.c, rc.Mp, rc.Rp);
+      const float qq = logit_prob(t[1], p.c, rc.Mq, rc.Rq);
+      if (!((double)t[2] * (double)qq < (double)pp)) {
+        fail = i;
+        break;
+      }
+    }
+    if (lane == 0) sm_fail[wave] = fail;
+    __syncthreads();
+    const int a = min(min(sm_fail[0], sm_fail[1]), min(sm_fail[2], sm_fail[3]));
+    __syncthreads();
+    if (a < g.k) {
+      if (lead) {
+        *reinterpret_cast<u32x4*>(p.geo + 4 * (int64_t)b) = u32x4{(uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k, 1u};
+        p.st_a[b] = a;
+        p.st_mode[b] = kResidual;
+      }
+      // the residual needs the maxima of w = max(0, p_a - q_a)
+      sub_maxima(p, row_ctx(p, b, g, a, true, lane), true, b, sub, wave, lane);
+    } else if (hi > g.k) {
+      // every test passed: the bonus row k, whose largest probability is known from its statistics
+      if (lead) {
+        *reinterpret_cast<u32x4*>(p.geo + 4 * (int64_t)b) = u32x4{(uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k, 1u};
+        p.st_a[b] = g.k;
+        p.st_mode[b] = kBonus;
+      }
+    } else if (lead) {
+      const int at = __hip_atomic_fetch_add(p.counts + r + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      *reinterpret_cast<u32x4*>(p.lists + ((int64_t)r * p.B + at) * 4) =
+          u32x4{(uint32_t)b, (uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k};
     }
   }
-  if (lane == 0) sm_fail[wave] = fail;
-  __syncthreads();
-  const int a = min(min(sm_fail[0], sm_fail[1]), min(sm_fail[2], sm_fail[3]));
-  if (lead) {
-    *reinterpret_cast<u32x4*>(p.geo + 4 * (int64_t)b) = u32x4{(uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k, 1u};
-    p.st_a[b] = a;
-    p.st_mode[b] = a < g.k ? kResidual : kBonus;
-  }
-  // a residual needs the maxima of w = max(0, p_a - q_a); a logit bonus row needs no max pass
-  if (a < g.k) sub_maxima(p, row_ctx(p, b, g, a, true, lane), true, b, sub, wave, lane);
 }
 
 // ------------------------------------------------------------------- probability max pass
@@ -660,11 +717,25 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
   const unsigned items = (unsigned)((int64_t)p.B * p.nsub);
   hipError_t e;
   if (p.kind == 1) {
-    const unsigned rows = (unsigned)((int64_t)p.B * (p.max_k + 1) * 2 * p.nsub);
-    hipLaunchKernelGGL(accept_stats_kernel, dim3(rows), dim3(kThreads), 0, s, p);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(accept_decide_kernel, dim3(items), dim3(kThreads), 0, s, p);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // Rounds of doubling width until position max_k is covered.  A round costs a few
+    // microseconds of launch and latency, a row 4V bytes: when all the target rows together
+    // stream in well under that many rounds' worth of time, one round reads every row;
+    // otherwise the first round is two positions wide ({0,1}, {2..5}, {6..13}, ...), since
+    // most sequences pass the first test at usual acceptance rates.
+    const bool one_round = (int64_t)p.B * (p.max_k + 1) * p.V * 4 <= kOneRoundBytes;
+    int width = one_round ? p.max_k + 1 : 2;
+    for (int r = 0, lo = 0; lo <= p.max_k; ++r, lo += width, width *= 2) {
+      const int hi = lo + width;
+      // one workgroup per work item (a workgroup's items run one after another, their latency
+      // exposed); later rounds, whose size the host does not know, are capped
+      const int64_t rows = (int64_t)p.B * 2 * (hi - lo) * p.nsub;
+      const unsigned gs = (unsigned)(r == 0 || rows < kRoundGrid ? rows : kRoundGrid);
+      const unsigned gd = r == 0 || items < (unsigned)kRoundGrid ? items : (unsigned)kRoundGrid;
+      hipLaunchKernelGGL(accept_stats_kernel, dim3(gs), dim3(kThreads), 0, s, p, r, lo, hi);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      hipLaunchKernelGGL(accept_decide_kernel, dim3(gd), dim3(kThreads), 0, s, p, r, lo, hi);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
   } else {
     hipLaunchKernelGGL(accept_init_kernel, dim3((p.B + kThreads - 1) / kThreads), dim3(kThreads), 0, s, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -65,7 +65,7 @@ bool attn_waves(int32_t num_seqs, int32_t num_kv_heads, int32_t max_seq_len, int
 }
 
 struct AcceptLayout {
-  size_t geo, st_a, st_mode, lse, tin, max_part, bad_part, sum_part, total;
+  size_t geo, st_a, st_mode, counts, lists, lse, tin, max_part, bad_part, sum_part, total;
 };
 
 int64_t accept_nsub(int64_t V) { return (V + spexis::kAcceptSub - 1) / spexis::kAcceptSub; }
@@ -82,6 +82,8 @@ AcceptLayout accept_layout(int64_t B, int64_t V, int64_t max_k) {
   l.geo = take(B * 16);
   l.st_a = take(B * 4);
   l.st_mode = take(B * 4);
+  l.counts = take((spexis::kAcceptMaxRounds + 1) * 4);
+  l.lists = take(spexis::kAcceptMaxRounds * B * 4 * 4);
   l.lse = take(B * (max_k + 1) * 2 * ns * 2 * 4);
   l.tin = take(B * (max_k > 0 ? max_k : 1) * 4 * 4);
   l.max_part = take(B * ns * 2 * 4);
@@ -262,6 +264,8 @@ int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, 
   p.geo = reinterpret_cast<int32_t*>(ws + lay.geo);
   p.st_a = reinterpret_cast<int32_t*>(ws + lay.st_a);
   p.st_mode = reinterpret_cast<int32_t*>(ws + lay.st_mode);
+  p.counts = reinterpret_cast<int32_t*>(ws + lay.counts);
+  p.lists = reinterpret_cast<int32_t*>(ws + lay.lists);
   p.lse_part = reinterpret_cast<float*>(ws + lay.lse);
   p.tin = reinterpret_cast<float*>(ws + lay.tin);
   p.max_part = reinterpret_cast<float*>(ws + lay.max_part);

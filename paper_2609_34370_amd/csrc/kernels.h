@@ -66,6 +66,8 @@ struct AcceptParams {
   int32_t* st_a;         // [B] final a_b
   int32_t* st_mode;      // [B] 1 residual, 2 bonus, 3 done (outputs written)
   float* lse_part;       // [B][max_k+1][2 target/draft][nsub][2] (max, sum of 2^(y-max)) (logits mode)
+  int32_t* counts;       // [kAcceptMaxRounds+1] sequences entering round r (r >= 1; logits mode)
+  int32_t* lists;        // [kAcceptMaxRounds][B][4] those sequences: b, first target row, first draft row, k
   float* tin;            // [B][max_k][4] test inputs of position i: target and draft logit of x_i,
                          // u_i, and 1 if x_i is a valid id (logits mode; gathered by the stats pass)
   float* max_part;       // [B][nsub][2] (max w, max p) of the sampled row(s)
@@ -73,6 +75,7 @@ struct AcceptParams {
   uint64_t* sum_part;    // [B][nsub]
 };
 
+constexpr int kAcceptMaxRounds = 8;  // test rounds: widths 2, 4, 8, ... cover max_k <= 509
 constexpr int kAcceptSub = 4096;     // vocab entries per partial result (one workgroup's share)
 
 hipError_t launch_append(const AppendParams& p, hipStream_t s);
