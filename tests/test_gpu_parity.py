@@ -309,6 +309,86 @@ def test_accept_logits_agrees_with_oracle(wid, B):
         assert borderline(p, q, ids, ua, us, batch.qsl, b, ra[b], rt[b], a[b], t[b]), b
 
 
+def test_accept_logits_rounds_with_ragged_drafts():
+    # 128 sequences, k_b in 0..8, V = 128256: 590 MB of target rows, so the tests run in rounds
+    # {0,1}, {2..5}, {6..13}; draft noise spread U[0.1, 3] sends some sequences through all three
+    spec, batch, attn, acc = case(4, vocab=128256)
+    assert batch.B * (batch.max_k + 1) * spec.vocab * 4 > (192 << 20)
+    say(f"[accept logits rounds] B={batch.B} V={spec.vocab} k in [{batch.k.min()}, {batch.k.max()}]")
+    step = VerifyStep(batch, attn, acc)
+    step.accept()
+    torch.cuda.synchronize()
+    a, t, s = step.accept_outputs()
+    p, q = oracle_probs(acc)
+    ids, ua, us = acc.draft_ids.cpu().numpy(), acc.u_accept.cpu().numpy(), acc.u_sample.cpu().numpy()
+    ra, rt, rs, _ = oracle.accept(batch.qsl, p, q, ids, ua, us, max_k=batch.max_k)
+    assert (s == 0).all() and (rs == 0).all()
+    assert (a >= 2).sum() > 0 and (a >= 6).sum() > 0, "some sequences must reach the later rounds"
+    diff = [b for b in range(batch.B) if a[b] != ra[b] or not np.array_equal(t[b], rt[b])]
+    say(f"  accepted histogram={np.bincount(a, minlength=9).tolist()} disagreements={len(diff)}")
+    assert len(diff) <= max(1, batch.B // 100)
+    for b in diff:
+        assert borderline(p, q, ids, ua, us, batch.qsl, b, ra[b], rt[b], a[b], t[b]), b
+
+
+def test_accept_logits_edge_rows_across_rounds():
+    # 64 sequences, max_k = 8, V = 100000: several rounds.  Special sequences:
+    #   0: draft id out of range at position 5 (found before any test)   -> status 3
+    #   1: draft equal to target at 0..2, a NaN target logit at 3        -> a = 3, status 2
+    #   2: draft equal to target everywhere                              -> a = 8, bonus
+    #   3: k = 0                                                         -> bonus row 0
+    #   4: draft equal to target everywhere, bonus row all -inf          -> a = 8, status 2
+    V, B, K = 100000, 64, 8
+    rng = np.random.default_rng(11)
+    k = rng.integers(0, K + 1, B)
+    k[[0, 1, 2, 4]] = K
+    k[3] = 0
+    qsl = np.concatenate([[0], np.cumsum(k + 1)]).astype(np.int32)
+    T = int(qsl[-1])
+    tl = (rng.standard_normal((T, V)) * 3).astype(np.float32)
+    dl = np.empty((T - B, V), np.float32)
+    for b in range(B):
+        for i in range(k[b]):
+            dl[qsl[b] - b + i] = tl[qsl[b] + i] + rng.standard_normal(V).astype(np.float32)
+    for b, upto in ((1, 3), (2, K), (4, K)):
+        for i in range(upto):
+            dl[qsl[b] - b + i] = tl[qsl[b] + i]
+    tl[qsl[1] + 3, 777] = np.nan
+    tl[qsl[4] + K, :] = -np.inf
+    ids = np.empty(T - B, np.int32)
+    for b in range(B):                                  # drafts drawn from the draft rows
+        for i in range(k[b]):
+            row = dl[qsl[b] - b + i].astype(np.float64)
+            g = row - np.log(-np.log(rng.random(V)))
+            ids[qsl[b] - b + i] = int(np.argmax(g))
+    ids[qsl[0] - 0 + 5] = V + 3
+    ua = rng.random(T - B, dtype=np.float32)
+    us = rng.random(B, dtype=np.float32)
+    assert B * (K + 1) * V * 4 > (192 << 20)
+    dev = lambda x: torch.as_tensor(x, device="cuda")
+    accepted = torch.empty(B, dtype=torch.int32, device="cuda")
+    toks = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+    stat = torch.empty(B, dtype=torch.int32, device="cuda")
+    ws = torch.empty(sx.spexis_accept_workspace_size(B, V, K), dtype=torch.uint8, device="cuda")
+    sx.spexis_accept(sx.SPEXIS_INPUT_LOGITS, dev(qsl), dev(tl), dev(dl), dev(ids), dev(ua), dev(us), K, accepted,
+                     toks, stat, ws, temperature=1.0)
+    torch.cuda.synchronize()
+    a, t, s = accepted.cpu().numpy(), toks.cpu().numpy(), stat.cpu().numpy()
+    p, q = oracle.softmax(tl, 1.0), oracle.softmax(dl, 1.0)
+    ra, rt, rs, _ = oracle.accept(qsl, p, q, ids, ua, us, max_k=K)
+    say(f"[accept logits edges] status={s[:5].tolist()} a={a[:5].tolist()} oracle status={rs[:5].tolist()}")
+    assert list(rs[:5]) == [3, 2, 0, 0, 2] and list(ra[:5]) == [0, 3, 8, 0, 8]
+    np.testing.assert_array_equal(s, rs)
+    np.testing.assert_array_equal(a[:5], ra[:5])
+    np.testing.assert_array_equal(t[:2], rt[:2])
+    np.testing.assert_array_equal(t[4], rt[4])
+    np.testing.assert_array_equal(t[2, :K], rt[2, :K])
+    diff = [b for b in range(2, B) if b != 4 and (a[b] != ra[b] or not np.array_equal(t[b], rt[b]))]
+    assert len(diff) <= 1
+    for b in diff:
+        assert borderline(p, q, ids, ua, us, qsl, b, ra[b], rt[b], a[b], t[b]), b
+
+
 # -------------------------------------------------------------------------- boundary
 
 def test_boundary_errors_on_gpu():
