@@ -50,6 +50,7 @@ def lib():
         L.oracle_attention.argtypes = [P, P, i32, i32, i32, i32, i32, P, P, P, i32, P, i32, f32, P, i32, P]
         L.oracle_attention.restype = ctypes.c_int
         L.oracle_softmax.argtypes = [P, i64, i32, f32, P]
+        L.oracle_lm_head.argtypes = [P, P, i64, i32, i32, f32, P, P, P]
         L.oracle_softmax.restype = None
         L.oracle_accept.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, P, P]
         L.oracle_accept.restype = None
@@ -115,6 +116,23 @@ def softmax(logits: np.ndarray, temperature: float = 1.0) -> np.ndarray:
     out = np.empty_like(x)
     lib().oracle_softmax(_p(x), rows, V, ctypes.c_float(temperature), _p(out))
     return out
+
+
+def lm_head(h: np.ndarray, W: np.ndarray, temperature: float = 1.0, want_logits: bool = True):
+    """fp64 logits h W^T of bf16 bit arrays h [rows, d], W [V, d], and each row's softmax
+    statistics at `temperature`: (logits or None, mx [rows], z [rows]) with
+    mx = max(logits) / T and z = sum(exp(logits / T - mx))."""
+    hh = _c(h, np.uint16)
+    ww = _c(W, np.uint16)
+    rows, d = hh.shape
+    V, d2 = ww.shape
+    assert d == d2
+    logits = np.empty((rows, V), np.float64) if want_logits else None
+    mx = np.empty(rows, np.float64)
+    z = np.empty(rows, np.float64)
+    lib().oracle_lm_head(_p(hh), _p(ww), rows, V, d, ctypes.c_float(temperature),
+                         _p(logits) if want_logits else None, _p(mx), _p(z))
+    return logits, mx, z
 
 
 def accept(qsl, target: np.ndarray, draft: np.ndarray, draft_ids, u_accept, u_sample, max_k: int = None,

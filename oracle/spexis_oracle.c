@@ -15,6 +15,8 @@
  *   oracle_attention   -- causal, grouped-query attention of the k+1 query tokens of each
  *                         sequence over its paged KV, in fp64, straight from the definition.
  *   oracle_softmax     -- temperature softmax of fp32 logits, in fp64, rounded to fp32.
+ *   oracle_lm_head     -- the output projection in front of acceptance (logits = h W^T over
+ *                         bf16 inputs, in fp64) and each row's softmax statistics.
  *   oracle_accept      -- speculative-sampling acceptance (accept x_i with probability
  *                         min(1, p_i(x_i)/q_i(x_i)); on the first rejection sample from the
  *                         normalised residual max(0, p - q); otherwise sample the bonus token
@@ -175,6 +177,41 @@ void oracle_softmax(const float* logits, int64_t rows, int32_t V, float temperat
     for (int32_t v = 0; v < V; ++v) { e[v] = exp(((double)x[v] - m) / (double)temperature); z += e[v]; }
     for (int32_t v = 0; v < V; ++v) probs[r * V + v] = (float)(e[v] / z);
     free(e);
+  }
+}
+
+/* --------------------------------------------------------------- LM head */
+
+/*
+ * The output projection that produces the rows acceptance reads (the verifying stage owns an
+ * LM head, Implementation): for bf16 hidden states h [rows][d] and LM-head weights W [V][d],
+ *   logits[r][v] = sum_j h[r][j] * W[v][j]                       (fp64, exact products)
+ * and each row's softmax statistics at temperature T (the same convention as oracle_softmax):
+ *   mx[r] = max_v logits[r][v] / T,   z[r] = sum_v exp(logits[r][v] / T - mx[r]).
+ * `logits` (fp64 [rows][V]) may be NULL; mx and z are fp64 [rows].
+ */
+void oracle_lm_head(const uint16_t* h, const uint16_t* W, int64_t rows, int32_t V, int32_t d, float temperature,
+                    double* logits, double* mx, double* z) {
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t r = 0; r < rows; ++r) {
+    double* hr = (double*)malloc(sizeof(double) * (size_t)d);
+    double* lr = (double*)malloc(sizeof(double) * (size_t)V);
+    for (int32_t j = 0; j < d; ++j) hr[j] = bf16_to_double(h[r * d + j]);
+    for (int32_t v = 0; v < V; ++v) {
+      double acc = 0.0;
+      const uint16_t* wv = W + (int64_t)v * d;
+      for (int32_t j = 0; j < d; ++j) acc += hr[j] * bf16_to_double(wv[j]);
+      lr[v] = acc;
+    }
+    double m = -INFINITY;
+    for (int32_t v = 0; v < V; ++v) if (lr[v] / (double)temperature > m) m = lr[v] / (double)temperature;
+    double zz = 0.0;
+    for (int32_t v = 0; v < V; ++v) zz += exp(lr[v] / (double)temperature - m);
+    mx[r] = m;
+    z[r] = zz;
+    if (logits) memcpy(logits + r * V, lr, sizeof(double) * (size_t)V);
+    free(hr);
+    free(lr);
   }
 }
 

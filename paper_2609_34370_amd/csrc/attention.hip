@@ -396,14 +396,14 @@ void verify_attn_kernel(AttnParams p) {
 //   o = sum_c acc_c 2^(m_c - M) / sum_c l_c 2^(m_c - M),   M = max_c m_c
 // Contributors are read four at a time, every load of a group issued together.
 template <int D>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
+__global__ __launch_bounds__(512) void attn_merge_kernel(AttnParams p) {
   const int w = blockIdx.x;
   const int64_t slot_f = attn_slot_floats(p.rmax, D);
   const int32_t* hdr = reinterpret_cast<const int32_t*>(p.ws + (int64_t)p.nwaves * 2 * slot_f) +
                        (int64_t)w * kAttnHdrInts;
   const u32x4 h0 = *reinterpret_cast<const u32x4*>(hdr);
+  const u32x4 h1 = *reinterpret_cast<const u32x4*>(hdr + 4);   // loaded with h0: one round trip
   if (h0[0] != 1u) return;
-  const u32x4 h1 = *reinterpret_cast<const u32x4*>(hdr + 4);
   const int f = (int)h0[2], nt = (int)h0[3], P = (int)h1[0], q0 = (int)h1[1], n = (int)h1[2];
   const int h = w % p.hkv, s0 = w / p.hkv;
   const int C = min((f + nt - 1) / P, p.nshares - 1) - s0 + 1;   // contributing shares
@@ -457,7 +457,7 @@ static hipError_t launch_attn_t(const AttnParams& p, hipStream_t s) {
   hipLaunchKernelGGL((verify_attn_kernel<D, BS, NT>), dim3((unsigned)(p.nwaves / 4)), dim3(256), 0, s, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_merge_kernel<D>), dim3((unsigned)p.nwaves), dim3(256), 0, s, p);
+  hipLaunchKernelGGL((attn_merge_kernel<D>), dim3((unsigned)p.nwaves), dim3(512), 0, s, p);   // 512: fewer items per thread
   return hipGetLastError();
 }
 
