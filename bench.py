@@ -97,7 +97,12 @@ def main():
     ap.add_argument("--ingest-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic.json from two rocprofv3 --pmc counter_collection.csv files "
                          "(FETCH_SIZE, WRITE_SIZE) of runs with --copy-probe N (pass the same N); needs no GPU")
+    ap.add_argument("--component", choices=["step", "lm_head"], default="step",
+                    help="lm_head: time spexis_lm_head and acceptance from its fused statistics at the "
+                         "workload's shape instead of the verification step (prints its own JSON line)")
     args = ap.parse_args()
+    if args.component == "lm_head":
+        return bench_lm_head(args)
     if args.ingest_traffic:
         if args.copy_probe <= 0:
             raise SystemExit("--ingest-traffic needs --copy-probe N: the copy size the counter runs used")
@@ -210,6 +215,93 @@ def main():
                      "traffic": traffic, "algorithmic_bytes": abytes},
         "cpu_baseline": cpu,
     }
+    print(json.dumps(line), flush=True)
+
+
+HIDDEN = {1: 512, 2: 4096, 3: 4096, 4: 4096, 5: 3584}   # hidden size of the model behind each workload
+MFMA_BF16_TFLOPS = 2500.0
+
+
+def bench_lm_head(args):
+    """The LM head in front of acceptance (logits = h W^T with fused statistics) at the workload's
+    target rows, then acceptance from those statistics against acceptance that computes its own.
+    Synthetic bf16 weights; every input is resident in HBM before timing."""
+    import torch
+
+    from paper_2609_34370_amd import spexis as sx
+    from paper_2609_34370_amd import workloads as wl
+    from paper_2609_34370_amd.step import VerifyStep
+
+    spec = wl.WORKLOADS[args.workload]
+    batch = wl.make_batch(spec, seed=args.seed)
+    attn = wl.make_attention_inputs(spec, batch, device="cuda", seed=args.seed)
+    acc = wl.make_accept_inputs(spec, batch, device="cuda", seed=args.seed)
+    d, V, T = HIDDEN[spec.wid], spec.vocab, batch.T
+    g = torch.Generator(device="cuda").manual_seed(260934370)
+    h = torch.randn((T, d), generator=g, device="cuda").to(torch.bfloat16)
+    w = (torch.randn((V, d), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    tiles = sx.spexis_lm_head_tiles(V)
+    logits = torch.empty((T, V), dtype=torch.float32, device="cuda")
+    stats = torch.empty((T, tiles, 2), dtype=torch.float32, device="cuda")
+    dstats = torch.empty((batch.T - batch.B, tiles, 2), dtype=torch.float32, device="cuda")
+    temp = acc.temperature
+
+    def timed(fn, steps, warmup):
+        for _ in range(warmup):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / steps   # us
+
+    us_lm = timed(lambda: sx.spexis_lm_head(h, w, stats, logits=logits, temperature=temp), args.steps, args.warmup)
+    us_lm_stats = timed(lambda: sx.spexis_lm_head(h, w, stats, temperature=temp), args.steps, args.warmup)
+    # Acceptance on logits this LM head produced: target rows from h, draft rows from h plus
+    # noise (a draft model sharing the head), drafts drawn from the draft rows (input generation,
+    # untimed).  Timed: acceptance computing its own statistics, and from the fused ones.
+    step = VerifyStep(batch, attn, acc)
+    rows_d = torch.as_tensor(np.concatenate([np.arange(batch.qsl[b], batch.qsl[b] + batch.k[b])
+                                             for b in range(batch.B)]).astype(np.int64), device="cuda")
+    hd = (h.float()[rows_d] + 0.3 * torch.randn((len(rows_d), d), generator=g, device="cuda")).to(torch.bfloat16)
+    dlogits = torch.empty((len(rows_d), V), dtype=torch.float32, device="cuda")
+    sx.spexis_lm_head(h, w, stats, logits=logits, temperature=temp)
+    sx.spexis_lm_head(hd, w, dstats, logits=dlogits, temperature=temp)
+    ids = torch.multinomial(torch.softmax(dlogits / temp, dim=1), 1, generator=g).view(-1).to(torch.int32)
+    torch.cuda.synchronize()
+    run_own = lambda: sx.spexis_accept(sx.SPEXIS_INPUT_LOGITS, step.qsl, logits, dlogits, ids, acc.u_accept,
+                                       acc.u_sample, batch.max_k, step.accepted_len, step.out_tokens,
+                                       step.row_status, step.acc_ws, temperature=temp)
+    run_fused = lambda: sx.spexis_accept_with_stats(step.qsl, logits, dlogits, stats, dstats, ids, acc.u_accept,
+                                                    acc.u_sample, batch.max_k, step.accepted_len,
+                                                    step.out_tokens, step.row_status, step.acc_ws,
+                                                    temperature=temp)
+    us_acc = timed(run_own, args.steps, args.warmup)
+    a_own = step.accepted_len.cpu().numpy().copy()
+    us_acc_stats = timed(run_fused, args.steps, args.warmup)
+    a_fused = step.accepted_len.cpu().numpy()
+    log(f"[lm_head] accepted mean {a_own.mean():.3f} (own statistics) / {a_fused.mean():.3f} (fused); "
+        f"decisions differ on {int((a_own != a_fused).sum())} of {batch.B} sequences")
+    wbytes, hbytes, lbytes, sbytes = V * d * 2, T * d * 2, T * V * 4, T * tiles * 8
+    flops = 2.0 * T * V * d
+    gbs = (wbytes + hbytes + lbytes + sbytes) / (us_lm * 1e-6) / 1e9
+    tfl = flops / (us_lm * 1e-6) / 1e12
+    line = {
+        "component": "spexis_lm_head", "workload": spec.name, "rows": T, "hidden": d, "vocab": V,
+        "us": round(us_lm, 2), "us_stats_only": round(us_lm_stats, 2),
+        "hbm": {"achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                "bytes": wbytes + hbytes + lbytes + sbytes},
+        "mfma": {"achieved": round(tfl, 1), "peak": MFMA_BF16_TFLOPS, "unit": "TFLOP/s",
+                 "frac": round(tfl / MFMA_BF16_TFLOPS, 4), "flops": flops},
+        "accept_us": round(us_acc, 2), "accept_with_stats_us": round(us_acc_stats, 2),
+        "dtype": "bf16", "data": "synthetic",
+    }
+    log(f"[lm_head] {T}x{d} @ {V}x{d}: {us_lm:.1f} us ({us_lm_stats:.1f} us without logits) -> {gbs:.0f} GB/s "
+        f"({gbs / HBM_PEAK_GBS:.1%}), {tfl:.0f} TFLOP/s ({tfl / MFMA_BF16_TFLOPS:.1%}); accept {us_acc:.1f} us, "
+        f"with given statistics {us_acc_stats:.1f} us")
     print(json.dumps(line), flush=True)
 
 

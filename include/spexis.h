@@ -11,6 +11,8 @@
  *   spexis_append_kv         write the k+1 new K/V rows of every sequence into the cache
  *   spexis_verify_attention  causal grouped-query attention of those rows over the cache
  *   spexis_accept            ratio tests, residual / bonus sampling, outputs
+ *   spexis_lm_head           logits = h W^T with fused softmax statistics (next to accept)
+ *   spexis_accept_with_stats acceptance from logits whose statistics are known
  *   spexis_softmax_rows      temperature softmax of logit rows (probability inputs)
  *
  * Conventions shared by every entry point
@@ -205,6 +207,48 @@ int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k,
                   const float* u_accept, const float* u_sample, int32_t* accepted_len,
                   int32_t* out_tokens, int32_t* row_status, int32_t* seq_lens_inout,
                   void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * spexis_lm_head -- the output projection in front of acceptance (the verifying stage owns an
+ * LM head, Implementation), with the softmax statistics acceptance needs fused into it:
+ *   logits[m][v] = sum_j hidden[m][j] * weight[v][j]        (fp32 accumulation)
+ *   stats[m][t] = (max x*c, sum 2^(x*c - max)) over columns v of tile t = v / 128, v < vocab,
+ *                 x = logits[m][v], c = log2(e) / temperature
+ *
+ *   hidden   [rows][hidden_dim] bf16 (read);  weight [vocab][hidden_dim] bf16 (read)
+ *   logits   [rows][vocab] fp32 (written), or NULL to write only the statistics
+ *   stats    [rows][spexis_lm_head_tiles(vocab)][2] fp32 (written)
+ * Supported: hidden_dim a multiple of 256.  Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP.
+ */
+int spexis_lm_head(const void* hidden, const void* weight, int32_t rows, int32_t vocab,
+                   int32_t hidden_dim, float temperature, float* logits, float* stats,
+                   void* stream);
+
+/* Column tiles per row of spexis_lm_head's statistics: ceil(vocab / 128). */
+int32_t spexis_lm_head_tiles(int32_t vocab);
+
+/* Bytes of spexis_lm_head's statistics for `rows` rows. */
+size_t spexis_lm_head_stats_size(int32_t rows, int32_t vocab);
+
+/*
+ * spexis_accept_with_stats -- spexis_accept for logits whose softmax statistics are already
+ * known, e.g. from spexis_lm_head (same temperature): the acceptance then reads a logit row
+ * only where it samples, never to normalise it.  Arguments and outputs as spexis_accept with
+ * kind = SPEXIS_INPUT_LOGITS, plus
+ *   target_stats  [T][stats_tiles][2] fp32, draft_stats [T-B][stats_tiles][2] fp32: for
+ *                 every row, (max y*c, sum 2^(y*c - max)) over each of stats_tiles disjoint
+ *                 column ranges that together cover the row, c = log2(e) / temperature
+ * Errors: as spexis_accept.
+ */
+int spexis_accept_with_stats(int32_t num_seqs, int32_t vocab, int32_t max_k, float temperature,
+                             int32_t total_tokens, const int32_t* query_start_loc,
+                             const float* target_logits, const float* draft_logits,
+                             const float* target_stats, const float* draft_stats,
+                             int32_t stats_tiles, const int32_t* draft_ids,
+                             const float* u_accept, const float* u_sample,
+                             int32_t* accepted_len, int32_t* out_tokens, int32_t* row_status,
+                             int32_t* seq_lens_inout, void* workspace, size_t workspace_bytes,
+                             void* stream);
 
 #ifdef __cplusplus
 }

@@ -228,12 +228,15 @@ __device__ __forceinline__ RowCtx row_ctx(const AcceptParams& p, int b, const Ge
   r.logits = p.kind == 1;
   r.Mp = r.Rp = r.Mq = r.Rq = 1.f;
   if (r.logits) {
-    const float* lp = lse_slot(p, b, a, 0);
-    const float* lq = lse_slot(p, b, a, 1);
-    const Part2 fp = part_first(lp, p.nsub, lane, -INFINITY, 0.f);
-    const Part2 fq = with_q ? part_first(lq, p.nsub, lane, -INFINITY, 0.f) : Part2{-INFINITY, 0.f};
-    row_stats(lp, p.nsub, lane, fp, r.Mp, r.Rp);
-    if (with_q) row_stats(lq, p.nsub, lane, fq, r.Mq, r.Rq);
+    // partials computed here (per 4096-entry sub-chunk) or given by the caller (per column tile)
+    const bool ext = p.ext_tstats != nullptr;
+    const int np = ext ? p.ext_parts : p.nsub;
+    const float* lp = ext ? p.ext_tstats + (int64_t)(g.t0 + a) * np * 2 : lse_slot(p, b, a, 0);
+    const float* lq = ext ? p.ext_dstats + (int64_t)(g.d0 + a) * np * 2 : lse_slot(p, b, a, 1);
+    const Part2 fp = part_first(lp, np, lane, -INFINITY, 0.f);
+    const Part2 fq = with_q ? part_first(lq, np, lane, -INFINITY, 0.f) : Part2{-INFINITY, 0.f};
+    row_stats(lp, np, lane, fp, r.Mp, r.Rp);
+    if (with_q) row_stats(lq, np, lane, fq, r.Mq, r.Rq);
   }
   return r;
 }
@@ -423,6 +426,24 @@ __global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p, 
     }
     __syncthreads();
   }
+}
+
+// The inputs of every test, when the statistics are given and no stats pass gathers them.
+__global__ __launch_bounds__(kThreads) void accept_gather_kernel(AcceptParams p) {
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (idx >= (int64_t)p.B * p.max_k) return;
+  const int b = (int)(idx / p.max_k), i = (int)(idx % p.max_k);
+  int n;
+  const Geom g = seq_geom(p, b, n);
+  if (!g.valid || i >= g.k) return;
+  const int x = p.ids[g.d0 + i];
+  const bool ok = x >= 0 && x < p.V;
+  f32x4 t;
+  t[0] = ok ? p.target[(int64_t)(g.t0 + i) * p.V + x] : 0.f;
+  t[1] = ok ? p.draft[(int64_t)(g.d0 + i) * p.V + x] : 0.f;
+  t[2] = p.u_accept[g.d0 + i];
+  t[3] = ok ? 1.f : 0.f;
+  *reinterpret_cast<f32x4*>(p.tin + (idx) * 4) = t;
 }
 
 // Round r, positions [lo, hi): one work item per (sequence of the list, sub-chunk).  Every item
@@ -716,7 +737,17 @@ hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
   const unsigned items = (unsigned)((int64_t)p.B * p.nsub);
   hipError_t e;
-  if (p.kind == 1) {
+  if (p.kind == 1 && p.ext_tstats) {
+    // statistics given: gather the tests' inputs, then one round over every position
+    if (p.max_k > 0) {
+      const int64_t n = (int64_t)p.B * p.max_k;
+      hipLaunchKernelGGL(accept_gather_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                         s, p);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(accept_decide_kernel, dim3(items), dim3(kThreads), 0, s, p, 0, 0, p.max_k + 1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  } else if (p.kind == 1) {
     // Rounds of doubling width until position max_k is covered.  A round costs a few
     // microseconds of launch and latency, a row 4V bytes: when all the target rows together
     // stream in well under that many rounds' worth of time, one round reads every row;

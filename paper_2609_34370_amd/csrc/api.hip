@@ -217,31 +217,36 @@ size_t spexis_accept_workspace_size(int32_t num_seqs, int32_t vocab, int32_t max
   return accept_layout(num_seqs, vocab, max_k).total;
 }
 
-int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, float temperature,
-                  int32_t total_tokens, const int32_t* query_start_loc, const float* target, const float* draft,
-                  const int32_t* draft_ids, const float* u_accept, const float* u_sample, int32_t* accepted_len,
-                  int32_t* out_tokens, int32_t* row_status, int32_t* seq_lens_inout, void* workspace,
-                  size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+int accept_impl(const char* who, int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, float temperature,
+                int32_t total_tokens, const int32_t* query_start_loc, const float* target, const float* draft,
+                const float* target_stats, const float* draft_stats, int32_t stats_parts,
+                const int32_t* draft_ids, const float* u_accept, const float* u_sample, int32_t* accepted_len,
+                int32_t* out_tokens, int32_t* row_status, int32_t* seq_lens_inout, void* workspace,
+                size_t workspace_bytes, void* stream) {
   if (kind != SPEXIS_INPUT_PROBS && kind != SPEXIS_INPUT_LOGITS)
-    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept: kind %d is neither PROBS nor LOGITS", kind);
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: kind %d is neither PROBS nor LOGITS", who, kind);
   if (num_seqs < 0 || vocab <= 0 || max_k < 0 || total_tokens < num_seqs)
-    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept: bad size");
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: bad size", who);
   const bool has_drafts = total_tokens > num_seqs;
   if (!query_start_loc || !target || !u_sample || !accepted_len || !out_tokens || !row_status ||
       (has_drafts && (!draft || !draft_ids || !u_accept)))
-    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept: null pointer");
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: null pointer", who);
   if (kind == SPEXIS_INPUT_LOGITS && (!(temperature > 0.f) || !std::isfinite(temperature)))
-    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept: temperature must be finite and > 0 for logits");
-  if (max_k > kMaxK) return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_accept: max_k %d > %d", max_k, kMaxK);
-  if (vocab > kMaxVocab) return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_accept: vocab %d > %d", vocab, kMaxVocab);
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: temperature must be finite and > 0 for logits", who);
+  if (max_k > kMaxK) return fail(SPEXIS_ERR_UNSUPPORTED, "%s: max_k %d > %d", who, max_k, kMaxK);
+  if (vocab > kMaxVocab) return fail(SPEXIS_ERR_UNSUPPORTED, "%s: vocab %d > %d", who, vocab, kMaxVocab);
   if (num_seqs == 0) return ok();
   const AcceptLayout lay = accept_layout(num_seqs, vocab, max_k);
   if (!workspace || workspace_bytes < lay.total)
-    return fail(SPEXIS_ERR_WORKSPACE_TOO_SMALL, "spexis_accept: workspace %zu bytes < %zu needed", workspace_bytes,
+    return fail(SPEXIS_ERR_WORKSPACE_TOO_SMALL, "%s: workspace %zu bytes < %zu needed", who, workspace_bytes,
                 lay.total);
   const int64_t nsub = accept_nsub(vocab);
   if ((int64_t)num_seqs * (max_k + 1) * 2 * nsub >= (1ll << 31))
-    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_accept: grid too large");
+    return fail(SPEXIS_ERR_UNSUPPORTED, "%s: grid too large", who);
   char* ws = static_cast<char*>(workspace);
   spexis::AcceptParams p{};
   p.kind = kind;
@@ -271,7 +276,76 @@ int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, 
   p.max_part = reinterpret_cast<float*>(ws + lay.max_part);
   p.bad_part = reinterpret_cast<int32_t*>(ws + lay.bad_part);
   p.sum_part = reinterpret_cast<uint64_t*>(ws + lay.sum_part);
-  return hip_result(spexis::launch_accept(p, (hipStream_t)stream), "spexis_accept");
+  p.ext_tstats = target_stats;
+  p.ext_dstats = draft_stats;
+  p.ext_parts = stats_parts;
+  return hip_result(spexis::launch_accept(p, (hipStream_t)stream), who);
+}
+
+}  // namespace
+
+extern "C" {
+
+int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, float temperature,
+                  int32_t total_tokens, const int32_t* query_start_loc, const float* target, const float* draft,
+                  const int32_t* draft_ids, const float* u_accept, const float* u_sample, int32_t* accepted_len,
+                  int32_t* out_tokens, int32_t* row_status, int32_t* seq_lens_inout, void* workspace,
+                  size_t workspace_bytes, void* stream) {
+  return accept_impl("spexis_accept", kind, num_seqs, vocab, max_k, temperature, total_tokens, query_start_loc,
+                     target, draft, nullptr, nullptr, 0, draft_ids, u_accept, u_sample, accepted_len, out_tokens,
+                     row_status, seq_lens_inout, workspace, workspace_bytes, stream);
+}
+
+int32_t spexis_lm_head_tiles(int32_t vocab) { return vocab > 0 ? (vocab + spexis::kLmCols - 1) / spexis::kLmCols : 0; }
+
+int spexis_accept_with_stats(int32_t num_seqs, int32_t vocab, int32_t max_k, float temperature,
+                             int32_t total_tokens, const int32_t* query_start_loc, const float* target_logits,
+                             const float* draft_logits, const float* target_stats, const float* draft_stats,
+                             int32_t stats_tiles, const int32_t* draft_ids, const float* u_accept,
+                             const float* u_sample, int32_t* accepted_len, int32_t* out_tokens,
+                             int32_t* row_status, int32_t* seq_lens_inout, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  const bool has_drafts = total_tokens > num_seqs;
+  if (!target_stats || (has_drafts && !draft_stats))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept_with_stats: null statistics");
+  if (stats_tiles <= 0) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept_with_stats: stats_tiles <= 0");
+  return accept_impl("spexis_accept_with_stats", SPEXIS_INPUT_LOGITS, num_seqs, vocab, max_k, temperature,
+                     total_tokens, query_start_loc, target_logits, draft_logits, target_stats,
+                     has_drafts ? draft_stats : target_stats, stats_tiles, draft_ids, u_accept, u_sample,
+                     accepted_len, out_tokens, row_status, seq_lens_inout, workspace, workspace_bytes, stream);
+}
+
+size_t spexis_lm_head_stats_size(int32_t rows, int32_t vocab) {
+  if (rows <= 0 || vocab <= 0) return 0;
+  return (size_t)rows * spexis_lm_head_tiles(vocab) * 2 * sizeof(float);
+}
+
+int spexis_lm_head(const void* hidden, const void* weight, int32_t rows, int32_t vocab, int32_t hidden_dim,
+                   float temperature, float* logits, float* stats, void* stream) {
+  if (!hidden || !weight || !stats) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lm_head: null pointer");
+  if (rows < 0 || vocab <= 0 || hidden_dim <= 0)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lm_head: bad size");
+  if (!(temperature > 0.f) || !std::isfinite(temperature))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lm_head: temperature must be finite and > 0");
+  if (hidden_dim % 256 != 0)
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_lm_head: hidden_dim %d is not a multiple of 256", hidden_dim);
+  if (rows == 0) return ok();
+  const int64_t tiles = spexis_lm_head_tiles(vocab);
+  const int64_t groups = (rows + spexis::kLmRows - 1) / spexis::kLmRows;
+  if ((tiles + 7) / 8 * 8 * groups >= (1ll << 31) || (int64_t)rows * vocab >= (1ll << 40))
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_lm_head: problem too large");
+  spexis::LmParams p{};
+  p.h = hidden;
+  p.w = weight;
+  p.logits = logits;
+  p.stats = stats;
+  p.M = rows;
+  p.V = vocab;
+  p.d = hidden_dim;
+  p.ntiles = (int)tiles;
+  p.mgroups = (int)groups;
+  p.c = (float)(1.4426950408889634 / (double)temperature);
+  return hip_result(spexis::launch_lm_head(p, (hipStream_t)stream), "spexis_lm_head");
 }
 
 }  // extern "C"

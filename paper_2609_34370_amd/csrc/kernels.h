@@ -46,6 +46,20 @@ __host__ __device__ inline int64_t attn_ws_bytes(int nwaves, int rmax, int D) {
   return (int64_t)nwaves * (2 * attn_slot_floats(rmax, D) * 4 + kAttnHdrInts * 4);
 }
 
+// LM-head projection logits = h W^T with the row statistics of its 128-column tiles.
+struct LmParams {
+  const void* h;         // [M][d] bf16
+  const void* w;         // [V][d] bf16
+  float* logits;         // [M][V] fp32 (null: not written)
+  float* stats;          // [M][ntiles][2]: max of x*c and sum of 2^(x*c - max) over each tile
+  int M, V, d, ntiles, mgroups;
+  float c;               // log2(e) / temperature
+};
+
+constexpr int kLmRows = 320;   // rows of h per workgroup (ten 32-row MFMA tiles)
+constexpr int kLmCols = 128;   // vocabulary columns per workgroup (four waves of 32)
+constexpr int kLmK = 64;       // K per pipeline step (four MFMA k-steps)
+
 struct AcceptParams {
   int kind;              // 0 probs, 1 logits
   int B, V, max_k, T;
@@ -68,6 +82,9 @@ struct AcceptParams {
   float* lse_part;       // [B][max_k+1][2 target/draft][nsub][2] (max, sum of 2^(y-max)) (logits mode)
   int32_t* counts;       // [kAcceptMaxRounds+1] sequences entering round r (r >= 1; logits mode)
   int32_t* lists;        // [kAcceptMaxRounds][B][4] those sequences: b, first target row, first draft row, k
+  const float* ext_tstats;   // logits mode with given statistics: [T][ext_parts][2] for the target
+  const float* ext_dstats;   // rows, [T-B][ext_parts][2] for the draft rows (max of y*c, sum of
+  int ext_parts;             // 2^(y*c - max) per column tile); null / 0: computed here
   float* tin;            // [B][max_k][4] test inputs of position i: target and draft logit of x_i,
                          // u_i, and 1 if x_i is a valid id (logits mode; gathered by the stats pass)
   float* max_part;       // [B][nsub][2] (max w, max p) of the sampled row(s)
@@ -80,6 +97,7 @@ constexpr int kAcceptSub = 4096;     // vocab entries per partial result (one wo
 
 hipError_t launch_append(const AppendParams& p, hipStream_t s);
 hipError_t launch_attention(const AttnParams& p, hipStream_t s);
+hipError_t launch_lm_head(const LmParams& p, hipStream_t s);
 hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V, float c, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s);
 

@@ -1,0 +1,207 @@
+// LM-head projection in front of acceptance, with the softmax statistics fused into its
+// epilogue.  The verifying stage owns an LM head (Implementation); its logits are the target
+// rows acceptance reads (Sec. 4, Related Work [sd]).  For bf16 h [M][d] and W [V][d]:
+//   logits[m][v] = sum_j h[m][j] W[v][j]   (fp32 accumulation, fp32 output)
+// and for every row and 128-column tile, at temperature T (c = log2(e)/T):
+//   stats = (max_v x*c, sum_v 2^(x*c - max))   over the tile's columns v < V.
+// Acceptance combines the tiles of a row into its normaliser without reading the row again.
+//
+// Work decomposition: one workgroup per (vocabulary tile of 128 columns, group of up to 320
+// rows of h).  Each of its four waves owns 32 columns and all the group's rows: ten 32x32
+// accumulator tiles of v_mfma_f32_32x32x16_bf16 (A operand: h rows, B operand: W rows).
+//   * W, the stream that matters (V*d*2 bytes, read once), goes straight from HBM into each
+//     wave's registers, four K-steps of 64 ahead.  A lane owns 32 consecutive K values of its
+//     column per step (64 contiguous bytes): the contraction order over K is free as long as
+//     h uses the same, so lane half h takes K = 32h + 8s .. +7 at MFMA step s.
+//   * h is shared by the four waves: it goes through LDS, one step per stage, fetched into
+//     registers two steps ahead.  Wait counts retire in issue order, and with that distance
+//     the wait for h never waits for a W load that is not needed next anyway.
+//   * Workgroups of one vocabulary tile and consecutive row groups are dispatched to the same
+//     XCD one after another, so a W tile read for one row group is an L2 hit for the next.
+#include "common.h"
+#include "kernels.h"
+
+namespace spexis {
+
+namespace {
+
+constexpr int kRT = kLmRows / 32;   // row tiles per workgroup
+constexpr int kWDepth = 4;          // W steps in flight
+constexpr int kAChunks = kLmRows * (kLmK / 8) / 256;   // 16-byte h chunks per thread per step (10)
+
+// W rows are read once: non-temporal loads keep them from evicting h out of L2.
+template <bool kStream>
+__device__ __forceinline__ u32x4 ldw(const uint16_t* p) {
+  if (kStream) return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return *reinterpret_cast<const u32x4*>(p);
+}
+
+}  // namespace
+
+template <bool kStream, int NRT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1)))
+void lm_head_kernel(LmParams p) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 31, half = lane >> 5;
+  const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
+  const int mg = local % p.mgroups;
+  const int nt = (local / p.mgroups) * 8 + xcd;
+  if (nt >= p.ntiles) return;
+  const int m0 = mg * kLmRows, n0 = nt * kLmCols;
+  const int rows = min(kLmRows, p.M - m0);
+  const int v = n0 + 32 * wave + col;
+  const int nsteps = p.d / kLmK;
+  const uint16_t* wrow = reinterpret_cast<const uint16_t*>(p.w) + (int64_t)min(v, p.V - 1) * p.d + 32 * half;
+  const uint16_t* hbase = reinterpret_cast<const uint16_t*>(p.h) + (int64_t)m0 * p.d;
+
+  // h in LDS: stage x, row r, 16-byte chunk kc of the step stored at position kc ^ ((r >> 1) & 7),
+  // so that the 16 rows one ds_read_b128 pass serves hit 16 distinct 16-byte bank groups
+  __shared__ u32x4 sm_a[2][kLmRows * 8];
+  u32x4 areg[2][kAChunks];   // h chunks of the next two steps, in flight
+  auto load_a = [&](u32x4 (&dst)[kAChunks], int j) {
+    j = min(j, nsteps - 1);   // past the end: re-read the last step (kept unconditional)
+#pragma unroll
+    for (int u = 0; u < kAChunks; ++u) {
+      const int q = threadIdx.x + 256 * u;
+      const int r = min(q >> 3, rows - 1), kc = q & 7;
+      dst[u] = *reinterpret_cast<const u32x4*>(hbase + (int64_t)r * p.d + j * kLmK + 8 * kc);
+    }
+  };
+  auto store_a = [&](const u32x4 (&src)[kAChunks], int stage) {
+#pragma unroll
+    for (int u = 0; u < kAChunks; ++u) {
+      const int q = threadIdx.x + 256 * u;
+      const int r = q >> 3, kc = q & 7;
+      sm_a[stage][r * 8 + (kc ^ ((r >> 1) & 7))] = src[u];
+    }
+  };
+  u32x4 wb[kWDepth][4];
+  auto load_w = [&](u32x4 (&dst)[4], int j) {
+    const uint16_t* src = wrow + (int64_t)min(j, nsteps - 1) * kLmK;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) dst[s] = ldw<kStream>(src + 8 * s);
+  };
+
+  f32x16 acc[NRT];
+#pragma unroll
+  for (int t = 0; t < NRT; ++t)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[t][e] = 0.f;
+
+  // prologue: h steps 0 and 1, W steps 0..3, stage 0 in LDS
+  load_a(areg[0], 0);
+  load_a(areg[1], 1);
+#pragma unroll
+  for (int b = 0; b < kWDepth; ++b) load_w(wb[b], b);
+  store_a(areg[0], 0);
+  load_a(areg[0], 2);
+  __syncthreads();
+
+  // The A fragments of k-step s+1 are read from LDS while the MFMAs of k-step s run.
+  auto frag = [&](int stage, int t, int s) {
+    const int m = 32 * t + col;
+    return sm_a[stage][m * 8 + ((4 * half + s) ^ ((m >> 1) & 7))];
+  };
+  auto compute = [&](const u32x4 (&w)[4], int stage) {
+    u32x4 fa[2][NRT];
+#pragma unroll
+    for (int t = 0; t < NRT; ++t) fa[0][t] = frag(stage, t, 0);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (s + 1 < 4) {
+#pragma unroll
+        for (int t = 0; t < NRT; ++t) fa[(s + 1) & 1][t] = frag(stage, t, s + 1);
+      }
+      const bf16x8 bop = as_bf16x8(w[s]);
+#pragma unroll
+      for (int t = 0; t < NRT; ++t)
+        acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fa[s & 1][t]), bop, acc[t], 0, 0, 0);
+    }
+  };
+
+  // step j: compute from stage j%2 and W buffer j%4; refill that W buffer with step j+4; move
+  // h step j+1 (fetched two steps ago) into the other stage; fetch h step j+3 into its registers
+  for (int j = 0; j < nsteps; j += kWDepth) {
+#pragma unroll
+    for (int jj = 0; jj < kWDepth; ++jj) {
+      compute(wb[jj], jj & 1);
+      load_w(wb[jj], j + jj + kWDepth);
+      store_a(areg[(jj + 1) & 1], (jj + 1) & 1);
+      load_a(areg[(jj + 1) & 1], j + jj + 3);
+      __syncthreads();
+    }
+  }
+
+  // ---- epilogue: logits, and each row's statistics over this workgroup's 128 columns
+  const bool live = v < p.V;
+  if (p.logits && live) {
+#pragma unroll
+    for (int t = 0; t < NRT; ++t) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int r = 32 * t + 8 * (i >> 2) + 4 * half + (i & 3);
+        if (r < rows) p.logits[(int64_t)(m0 + r) * p.V + v] = acc[t][i];
+      }
+    }
+  }
+  // Row statistics: each wave transposes one 32x32 tile at a time through its part of the
+  // (now free) h stages, then lane r < 32 reduces row r over the wave's 32 columns.
+  __shared__ float sm_m[4][kLmRows], sm_z[4][kLmRows];
+  constexpr int kTS = 36;   // floats per transposed row (16-byte aligned, padded)
+  float* tile = reinterpret_cast<float*>(&sm_a[0][0]) + wave * 32 * kTS;
+#pragma unroll
+  for (int t = 0; t < NRT; ++t) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      tile[(8 * (i >> 2) + 4 * half + (i & 3)) * kTS + col] = live ? acc[t][i] * p.c : -INFINITY;
+    if (lane < 32) {
+      f32x4 x[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) x[q] = *reinterpret_cast<const f32x4*>(tile + lane * kTS + 4 * q);
+      float mx = -INFINITY;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) mx = fmaxf(fmaxf(mx, fmaxf(x[q][0], x[q][1])), fmaxf(x[q][2], x[q][3]));
+      float e = 0.f;
+      if (mx != -INFINITY) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) e += fast_exp2(x[q][u] - mx);
+      }
+      sm_m[wave][32 * t + lane] = mx;
+      sm_z[wave][32 * t + lane] = e;
+    }
+  }
+  __syncthreads();
+  for (int r = threadIdx.x; r < rows; r += 256) {
+    const float M = fmaxf(fmaxf(sm_m[0][r], sm_m[1][r]), fmaxf(sm_m[2][r], sm_m[3][r]));
+    float Z = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+      if (sm_m[w][r] != -INFINITY) Z += sm_z[w][r] * fast_exp2(sm_m[w][r] - M);
+    *reinterpret_cast<f32x2*>(p.stats + ((int64_t)(m0 + r) * p.ntiles + nt) * 2) = f32x2{M, Z};
+  }
+}
+
+template <int NRT>
+static hipError_t launch_lm_nrt(const LmParams& p, hipStream_t s) {
+  // grid: tiles of 8 vocabulary tiles (one per XCD) x row groups, row groups innermost
+  const int64_t grid = (int64_t)((p.ntiles + 7) / 8) * 8 * p.mgroups;
+  if (p.mgroups == 1)
+    hipLaunchKernelGGL((lm_head_kernel<true, NRT>), dim3((unsigned)grid), dim3(256), 0, s, p);
+  else
+    hipLaunchKernelGGL((lm_head_kernel<false, NRT>), dim3((unsigned)grid), dim3(256), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_lm_head(const LmParams& p, hipStream_t s) {
+  // row tiles computed per workgroup: the smallest instantiated count covering the rows (a
+  // group of fewer rows repeats its last row in the padding tiles, whose results are dropped)
+  const int need = p.M >= kLmRows ? kRT : (p.M + 31) / 32;
+  if (need <= 1) return launch_lm_nrt<1>(p, s);
+  if (need <= 2) return launch_lm_nrt<2>(p, s);
+  if (need <= 4) return launch_lm_nrt<4>(p, s);
+  if (need <= 6) return launch_lm_nrt<6>(p, s);
+  return launch_lm_nrt<kRT>(p, s);
+}
+
+}  // namespace spexis

@@ -68,6 +68,13 @@ def lib():
     L.spexis_accept_workspace_size.restype = sz
     L.spexis_accept.argtypes = [i32, i32, i32, i32, f32, i32, P, P, P, P, P, P, P, P, P, P, P, sz, P]
     L.spexis_accept.restype = ctypes.c_int
+    L.spexis_lm_head.argtypes = [P, P, i32, i32, i32, f32, P, P, P]
+    L.spexis_lm_head.restype = ctypes.c_int
+    L.spexis_lm_head_tiles.argtypes, L.spexis_lm_head_tiles.restype = [i32], i32
+    L.spexis_lm_head_stats_size.argtypes, L.spexis_lm_head_stats_size.restype = [i32, i32], sz
+    L.spexis_accept_with_stats.argtypes = [i32, i32, i32, f32, i32, P, P, P, P, P, i32, P, P, P, P, P, P, P, P, sz,
+                                           P]
+    L.spexis_accept_with_stats.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -144,6 +151,41 @@ def spexis_accept(kind, query_start_loc, target, draft, draft_ids, u_accept, u_s
     _check(lib().spexis_accept(
         kind, num_seqs, vocab, max_k, ctypes.c_float(temperature), total_tokens, _ptr(query_start_loc, torch.int32),
         _ptr(target, torch.float32), _ptr(draft, torch.float32) if nd > 0 else None,
+        _ptr(draft_ids, torch.int32) if nd > 0 else None, _ptr(u_accept, torch.float32) if nd > 0 else None,
+        _ptr(u_sample, torch.float32), _ptr(accepted_len, torch.int32), _ptr(out_tokens, torch.int32),
+        _ptr(row_status, torch.int32), _ptr(seq_lens_inout, torch.int32), _ptr(workspace), ws_bytes,
+        _stream(stream)))
+
+
+def spexis_lm_head_tiles(vocab: int) -> int:
+    return int(lib().spexis_lm_head_tiles(vocab))
+
+
+def spexis_lm_head_stats_size(rows: int, vocab: int) -> int:
+    return int(lib().spexis_lm_head_stats_size(rows, vocab))
+
+
+def spexis_lm_head(hidden, weight, stats, logits=None, temperature=1.0, stream=None) -> None:
+    rows, hidden_dim = hidden.shape
+    vocab = weight.shape[0]
+    assert weight.shape[1] == hidden_dim
+    _check(lib().spexis_lm_head(_ptr(hidden, torch.bfloat16), _ptr(weight, torch.bfloat16), rows, vocab, hidden_dim,
+                                ctypes.c_float(temperature), _ptr(logits, torch.float32),
+                                _ptr(stats, torch.float32), _stream(stream)))
+
+
+def spexis_accept_with_stats(query_start_loc, target_logits, draft_logits, target_stats, draft_stats, draft_ids,
+                             u_accept, u_sample, max_k, accepted_len, out_tokens, row_status, workspace,
+                             temperature=1.0, seq_lens_inout=None, stream=None) -> None:
+    num_seqs = query_start_loc.shape[0] - 1
+    total_tokens, vocab = target_logits.shape
+    tiles = target_stats.shape[1]
+    nd = total_tokens - num_seqs
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().spexis_accept_with_stats(
+        num_seqs, vocab, max_k, ctypes.c_float(temperature), total_tokens, _ptr(query_start_loc, torch.int32),
+        _ptr(target_logits, torch.float32), _ptr(draft_logits, torch.float32) if nd > 0 else None,
+        _ptr(target_stats, torch.float32), _ptr(draft_stats, torch.float32) if nd > 0 else None, tiles,
         _ptr(draft_ids, torch.int32) if nd > 0 else None, _ptr(u_accept, torch.float32) if nd > 0 else None,
         _ptr(u_sample, torch.float32), _ptr(accepted_len, torch.int32), _ptr(out_tokens, torch.int32),
         _ptr(row_status, torch.int32), _ptr(seq_lens_inout, torch.int32), _ptr(workspace), ws_bytes,
