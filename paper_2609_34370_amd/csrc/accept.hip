@@ -428,6 +428,34 @@ __global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p, 
   }
 }
 
+// Given per-tile statistics of `rows` rows reduced to one (max, sum) per row, in the order
+// row_stats uses (so a consumer of the reduced row gets the same M and 1/Z), one wave per row.
+__global__ __launch_bounds__(kThreads) void accept_combine_kernel(const float* src, int parts, int rows,
+                                                                  float* dst) {
+  const int lane = threadIdx.x % kWave;
+  const int row = blockIdx.x * kWaves + threadIdx.x / kWave;
+  if (row >= rows) return;
+  const float* part = src + (int64_t)row * parts * 2;
+  const Part2 f = part_first(part, parts, lane, -INFINITY, 0.f);
+  float mm = f.a;
+  for (int x = lane + kWave; x < parts; x += kWave) mm = fmaxf(mm, part[2 * x]);
+  mm = wave_max(mm);
+  float zz = 0.f;
+  int nan = 0;
+  if (lane < parts) {
+    nan |= f.b != f.b;
+    if (f.a != -INFINITY) zz += f.b * fast_exp2(f.a - mm);
+  }
+  for (int x = lane + kWave; x < parts; x += kWave) {
+    const float z = part[2 * x + 1];
+    nan |= z != z;
+    if (part[2 * x] != -INFINITY) zz += z * fast_exp2(part[2 * x] - mm);
+  }
+  zz = wave_sum(zz);
+  nan = wave_or(nan);
+  if (lane == 0) *reinterpret_cast<f32x2*>(dst + (int64_t)row * 2) = f32x2{mm, nan ? NAN : zz};
+}
+
 // The inputs of every test, when the statistics are given and no stats pass gathers them.
 __global__ __launch_bounds__(kThreads) void accept_gather_kernel(AcceptParams p) {
   const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
@@ -734,20 +762,49 @@ hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V
   return hipGetLastError();
 }
 
+// The sampling passes every mode ends with: fixed-point sums, then the search.
+static hipError_t launch_sampling(const AcceptParams& p, hipStream_t s) {
+  const unsigned items = (unsigned)((int64_t)p.B * p.nsub);
+  hipLaunchKernelGGL(accept_sum_kernel, dim3(items), dim3(kThreads), 0, s, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(accept_search_kernel, dim3(p.B), dim3(kThreads), 0, s, p);
+  return hipGetLastError();
+}
+
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
   const unsigned items = (unsigned)((int64_t)p.B * p.nsub);
   hipError_t e;
   if (p.kind == 1 && p.ext_tstats) {
-    // statistics given: gather the tests' inputs, then one round over every position
-    if (p.max_k > 0) {
-      const int64_t n = (int64_t)p.B * p.max_k;
+    // Statistics given: reduce each row's tiles once (into the statistics area of the
+    // workspace, which the host checked is large enough), gather the tests' inputs, then one
+    // round over every position.
+    AcceptParams q = p;
+    if (p.ext_parts > 1) {
+      q.ext_tstats = p.lse_part;
+      q.ext_dstats = p.lse_part + 2 * (int64_t)p.T;
+      q.ext_parts = 1;
+      hipLaunchKernelGGL(accept_combine_kernel, dim3((unsigned)((p.T + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
+                         p.ext_tstats, p.ext_parts, p.T, p.lse_part);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      if (p.T > p.B) {
+        hipLaunchKernelGGL(accept_combine_kernel, dim3((unsigned)((p.T - p.B + kWaves - 1) / kWaves)),
+                           dim3(kThreads), 0, s, p.ext_dstats, p.ext_parts, p.T - p.B,
+                           p.lse_part + 2 * (int64_t)p.T);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+      }
+    }
+    if (q.max_k > 0) {
+      const int64_t n = (int64_t)q.B * q.max_k;
       hipLaunchKernelGGL(accept_gather_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0,
-                         s, p);
+                         s, q);
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(accept_decide_kernel, dim3(items), dim3(kThreads), 0, s, p, 0, 0, p.max_k + 1);
+    hipLaunchKernelGGL(accept_decide_kernel, dim3(items), dim3(kThreads), 0, s, q, 0, 0, q.max_k + 1);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-  } else if (p.kind == 1) {
+    return launch_sampling(q, s);
+  }
+  if (p.kind == 1) {
     // Rounds of doubling width until position max_k is covered.  A round costs a few
     // microseconds of launch and latency, a row 4V bytes: when all the target rows together
     // stream in well under that many rounds' worth of time, one round reads every row;
@@ -773,10 +830,7 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
     hipLaunchKernelGGL(accept_max_kernel, dim3(items), dim3(kThreads), 0, s, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(accept_sum_kernel, dim3(items), dim3(kThreads), 0, s, p);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(accept_search_kernel, dim3(p.B), dim3(kThreads), 0, s, p);
-  return hipGetLastError();
+  return launch_sampling(p, s);
 }
 
 }  // namespace spexis

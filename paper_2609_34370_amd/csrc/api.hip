@@ -309,6 +309,10 @@ int spexis_accept_with_stats(int32_t num_seqs, int32_t vocab, int32_t max_k, flo
   if (!target_stats || (has_drafts && !draft_stats))
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept_with_stats: null statistics");
   if (stats_tiles <= 0) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept_with_stats: stats_tiles <= 0");
+  // the per-row reductions of the statistics live in the workspace's statistics area
+  if (num_seqs > 0 && max_k >= 0 && total_tokens > (int64_t)num_seqs * (max_k + 1))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT,
+                "spexis_accept_with_stats: total_tokens %d > num_seqs * (max_k + 1)", total_tokens);
   return accept_impl("spexis_accept_with_stats", SPEXIS_INPUT_LOGITS, num_seqs, vocab, max_k, temperature,
                      total_tokens, query_start_loc, target_logits, draft_logits, target_stats,
                      has_drafts ? draft_stats : target_stats, stats_tiles, draft_ids, u_accept, u_sample,
