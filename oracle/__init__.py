@@ -51,6 +51,8 @@ def lib():
         L.oracle_attention.restype = ctypes.c_int
         L.oracle_softmax.argtypes = [P, i64, i32, f32, P]
         L.oracle_lm_head.argtypes = [P, P, i64, i32, i32, f32, P, P, P]
+        L.oracle_select_drafts.argtypes = [i32, P, P, f32, P, P, P]
+        L.oracle_select_drafts.restype = ctypes.c_int
         L.oracle_softmax.restype = None
         L.oracle_accept.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, P, P]
         L.oracle_accept.restype = None
@@ -133,6 +135,22 @@ def lm_head(h: np.ndarray, W: np.ndarray, temperature: float = 1.0, want_logits:
     lib().oracle_lm_head(_p(hh), _p(ww), rows, V, d, ctypes.c_float(temperature),
                          _p(logits) if want_logits else None, _p(mx), _p(z))
     return logits, mx, z
+
+
+def select_drafts(qsl, conf, alpha: float):
+    """Selective speculation: (kept_k [B], kept_qsl [B+1], keep [N]) for draft confidences conf [N]
+    of the batch qsl (drafts of sequence b at qsl[b]-b ..)."""
+    qsl = _c(qsl, np.int32)
+    B = len(qsl) - 1
+    N = int(qsl[-1]) - B
+    cf = _c(conf, np.float32) if N > 0 else np.zeros(1, np.float32)
+    kept_k = np.empty(B, np.int32)
+    kept_qsl = np.empty(B + 1, np.int32)
+    keep = np.empty(max(N, 1), np.int32)
+    rc = lib().oracle_select_drafts(B, _p(qsl), _p(cf), ctypes.c_float(alpha), _p(kept_k), _p(kept_qsl), _p(keep))
+    if rc != 0:
+        raise ValueError("oracle_select_drafts: bad arguments")
+    return kept_k, kept_qsl, keep[:N]
 
 
 def accept(qsl, target: np.ndarray, draft: np.ndarray, draft_ids, u_accept, u_sample, max_k: int = None,

@@ -17,6 +17,8 @@
  *   oracle_softmax     -- temperature softmax of fp32 logits, in fp64, rounded to fp32.
  *   oracle_lm_head     -- the output projection in front of acceptance (logits = h W^T over
  *                         bf16 inputs, in fp64) and each row's softmax statistics.
+ *   oracle_select_drafts -- acceptance-guided selective speculation: drop the alpha fraction of
+ *                         the batch's draft tokens with the lowest confidence (Sec. 5).
  *   oracle_accept      -- speculative-sampling acceptance (accept x_i with probability
  *                         min(1, p_i(x_i)/q_i(x_i)); on the first rejection sample from the
  *                         normalised residual max(0, p - q); otherwise sample the bonus token
@@ -213,6 +215,70 @@ void oracle_lm_head(const uint16_t* h, const uint16_t* W, int64_t rows, int32_t 
     free(hr);
     free(lr);
   }
+}
+
+/* ------------------------------------------------------ selective speculation */
+
+/*
+ * Acceptance-guided selective speculation (Sec. 5, "Acceptance-Guided Selective Speculation"):
+ * the draft tokens of a batch are ranked by confidence and a fixed fraction alpha of them, the
+ * lowest ranked, is dropped; speculation continues on the rest.
+ *   - sequence b has k_b = qsl[b+1]-qsl[b]-1 drafts, draft i at index qsl[b]-b+i, with
+ *     confidence conf[...] (the draft model's probability of the token it drafted; NaN or
+ *     values outside [0, 1] are clamped into [0, 1], NaN to 0);
+ *   - a draft's score is the confidence of its whole prefix, the fp32 product
+ *     s_i = s_{i-1} * conf_i taken in order (s_{-1} = 1): a later draft is verified only if
+ *     every earlier one is kept, so the product is what survives;
+ *   - the N = sum k_b drafts are ordered by score, higher first, equal scores by lower index
+ *     first; the last m = floor(alpha * N) of that order are dropped (alpha in [0, 1));
+ *   - each sequence keeps the drafts before its first dropped one: kept_k[b], keep[i] = 1 for
+ *     the kept drafts, and kept_qsl is the query_start_loc of the reduced batch.
+ * Returns 0, or -1 on bad sizes.
+ */
+typedef struct {
+  float score;
+  int32_t idx;
+} oracle_ranked;
+
+static int ranked_order(const void* pa, const void* pb) {
+  const oracle_ranked* a = (const oracle_ranked*)pa;
+  const oracle_ranked* b = (const oracle_ranked*)pb;
+  if (a->score != b->score) return a->score > b->score ? -1 : 1;
+  return a->idx < b->idx ? -1 : (a->idx > b->idx ? 1 : 0);
+}
+
+int oracle_select_drafts(int32_t B, const int32_t* qsl, const float* conf, float alpha, int32_t* kept_k,
+                         int32_t* kept_qsl, int32_t* keep) {
+  if (B < 0 || !(alpha >= 0.0f) || !(alpha < 1.0f)) return -1;
+  const int32_t N = qsl[B] - B;
+  if (N < 0) return -1;
+  oracle_ranked* r = (oracle_ranked*)malloc(sizeof(oracle_ranked) * (size_t)(N > 0 ? N : 1));
+  for (int32_t b = 0; b < B; ++b) {
+    const int32_t k = qsl[b + 1] - qsl[b] - 1, d0 = qsl[b] - b;
+    float s = 1.0f;
+    for (int32_t i = 0; i < k; ++i) {
+      float c = conf[d0 + i];
+      c = isnan(c) ? 0.0f : (c < 0.0f ? 0.0f : (c > 1.0f ? 1.0f : c));
+      s = s * c; /* fp32 product, round to nearest */
+      r[d0 + i].score = s;
+      r[d0 + i].idx = d0 + i;
+    }
+  }
+  qsort(r, (size_t)N, sizeof(oracle_ranked), ranked_order);
+  const int64_t m = (int64_t)floor((double)alpha * (double)N);
+  for (int32_t i = 0; i < N; ++i) keep[i] = 0;
+  for (int64_t j = 0; j < N - m; ++j) keep[r[j].idx] = 1;
+  kept_qsl[0] = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    const int32_t k = qsl[b + 1] - qsl[b] - 1, d0 = qsl[b] - b;
+    int32_t kk = 0;
+    while (kk < k && keep[d0 + kk]) ++kk;
+    for (int32_t i = kk; i < k; ++i) keep[d0 + i] = 0;
+    kept_k[b] = kk;
+    kept_qsl[b + 1] = kept_qsl[b] + kk + 1;
+  }
+  free(r);
+  return 0;
 }
 
 /* ---------------------------------------------------------------- accept */
