@@ -97,12 +97,17 @@ def main():
     ap.add_argument("--ingest-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic.json from two rocprofv3 --pmc counter_collection.csv files "
                          "(FETCH_SIZE, WRITE_SIZE) of runs with --copy-probe N (pass the same N); needs no GPU")
-    ap.add_argument("--component", choices=["step", "lm_head"], default="step",
+    ap.add_argument("--component", choices=["step", "lm_head", "select"], default="step",
                     help="lm_head: time spexis_lm_head and acceptance from its fused statistics at the "
-                         "workload's shape instead of the verification step (prints its own JSON line)")
+                         "workload's shape instead of the verification step; select: time selective "
+                         "speculation and measure the acceptance rate of the kept drafts (each prints its "
+                         "own JSON line)")
+    ap.add_argument("--alpha", type=float, nargs="+", default=[0.15, 0.3])
     args = ap.parse_args()
     if args.component == "lm_head":
         return bench_lm_head(args)
+    if args.component == "select":
+        return bench_select(args)
     if args.ingest_traffic:
         if args.copy_probe <= 0:
             raise SystemExit("--ingest-traffic needs --copy-probe N: the copy size the counter runs used")
@@ -303,6 +308,69 @@ def bench_lm_head(args):
         f"({gbs / HBM_PEAK_GBS:.1%}), {tfl:.0f} TFLOP/s ({tfl / MFMA_BF16_TFLOPS:.1%}); accept {us_acc:.1f} us, "
         f"with given statistics {us_acc_stats:.1f} us")
     print(json.dumps(line), flush=True)
+
+
+def bench_select(args):
+    """Selective speculation at the workload's batch: latency of spexis_select_drafts, and the
+    speculation accuracy of the drafts it keeps.  Confidences are the draft probabilities of the
+    drawn drafts, q_i(x_i), from the workload's synthetic draft rows.  A kept set is a prefix of
+    each sequence's drafts and acceptance is sequential, so the kept drafts of sequence b that
+    verification accepts number min(a_b, kept_k_b), where a_b is the accepted length over all
+    drafts: Theta_alpha = sum_b min(a_b, kept_k_b) / sum_b kept_k_b against Theta = sum a_b / sum k_b."""
+    import torch
+
+    from paper_2609_34370_amd import spexis as sx
+    from paper_2609_34370_amd import workloads as wl
+    from paper_2609_34370_amd.step import VerifyStep
+
+    spec = wl.WORKLOADS[args.workload]
+    batch = wl.make_batch(spec, seed=args.seed)
+    attn = wl.make_attention_inputs(spec, batch, device="cuda", seed=args.seed)
+    acc = wl.make_accept_inputs(spec, batch, device="cuda", seed=args.seed)
+    step = VerifyStep(batch, attn, acc, kind=sx.SPEXIS_INPUT_LOGITS)
+    step.accept()
+    a = step.accept_outputs()[0].astype(np.int64)
+    q = torch.softmax(acc.draft_logits / acc.temperature, dim=1)
+    conf = q.gather(1, acc.draft_ids.long().view(-1, 1)).view(-1).contiguous()
+    B, N = batch.B, batch.T - batch.B
+    kept_k = torch.empty(B, dtype=torch.int32, device="cuda")
+    kept_qsl = torch.empty(B + 1, dtype=torch.int32, device="cuda")
+    keep = torch.empty(max(N, 1), dtype=torch.int32, device="cuda")
+    k = batch.k.astype(np.int64)
+    theta = float(np.minimum(a, k).sum() / max(k.sum(), 1))
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(args.steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / args.steps
+
+    rows = []
+    for alpha in args.alpha:
+        us = timed(lambda: sx.spexis_select_drafts(step.qsl, conf, alpha, kept_k, kept_qsl, keep[:N]))
+        kk = kept_k.cpu().numpy().astype(np.int64)
+        theta_a = float(np.minimum(a, kk).sum() / max(kk.sum(), 1))
+        rows.append({"alpha": alpha, "us": round(us, 2), "kept_drafts": int(kk.sum()), "drafts": int(N),
+                     "theta": round(theta, 4), "theta_alpha": round(theta_a, 4),
+                     "accepted_kept": int(np.minimum(a, kk).sum()), "accepted_all": int(np.minimum(a, k).sum())})
+        log(f"[select] alpha={alpha}: {us:.1f} us; kept {kk.sum()}/{N} drafts; theta {theta:.4f} -> "
+            f"theta_alpha {theta_a:.4f}; accepted {np.minimum(a, kk).sum()}/{np.minimum(a, k).sum()}")
+    # the largest supported batch: 1024 sequences x 16 drafts
+    qsl_max = torch.arange(0, 17 * 1025, 17, dtype=torch.int32, device="cuda")
+    conf_max = torch.rand(16384, generator=torch.Generator(device="cuda").manual_seed(1), device="cuda")
+    km, kqm, keepm = (torch.empty(1024, dtype=torch.int32, device="cuda"),
+                      torch.empty(1025, dtype=torch.int32, device="cuda"),
+                      torch.empty(16384, dtype=torch.int32, device="cuda"))
+    us_max = timed(lambda: sx.spexis_select_drafts(qsl_max, conf_max, 0.3, km, kqm, keepm))
+    log(f"[select] 16384 drafts (1024 x 16): {us_max:.1f} us")
+    print(json.dumps({"component": "spexis_select_drafts", "workload": spec.name, "batch": B, "drafts": N,
+                      "alphas": rows, "us_16384_drafts": round(us_max, 2), "data": "synthetic"}), flush=True)
 
 
 ATTN_KERNELS = ("verify_attn_kernel", "attn_merge_kernel")   # the launches of spexis_verify_attention

@@ -13,6 +13,7 @@
  *   spexis_accept            ratio tests, residual / bonus sampling, outputs
  *   spexis_lm_head           logits = h W^T with fused softmax statistics (next to accept)
  *   spexis_accept_with_stats acceptance from logits whose statistics are known
+ *   spexis_select_drafts     selective speculation: drop the least confident drafts first
  *   spexis_softmax_rows      temperature softmax of logit rows (probability inputs)
  *
  * Conventions shared by every entry point
@@ -249,6 +250,28 @@ int spexis_accept_with_stats(int32_t num_seqs, int32_t vocab, int32_t max_k, flo
                              int32_t* accepted_len, int32_t* out_tokens, int32_t* row_status,
                              int32_t* seq_lens_inout, void* workspace, size_t workspace_bytes,
                              void* stream);
+
+/*
+ * spexis_select_drafts -- acceptance-guided selective speculation (Sec. 5): rank the batch's
+ * draft tokens by confidence and drop the lowest-ranked fraction alpha before verification.
+ *   - draft i of sequence b (index qsl[b]-b+i, i < k_b = qsl[b+1]-qsl[b]-1) has confidence
+ *     draft_conf[...], typically the draft model's probability of the token it drafted; NaN
+ *     counts as 0 and values are clamped into [0, 1];
+ *   - its score is the confidence of its prefix, the fp32 product of the confidences of drafts
+ *     0..i of its sequence taken in order (a draft is verified only after every earlier one);
+ *   - the N = T - B drafts are ordered by score, higher first, equal scores lower index first;
+ *     the last m = floor(alpha * N) are dropped, and every sequence keeps the drafts before its
+ *     first dropped one.
+ * Outputs: kept_k [B] (drafts kept per sequence), kept_query_start_loc [B+1] (the
+ * query_start_loc of the reduced batch, kept_k[b] + 1 tokens per sequence), keep [N] (1 for a
+ * kept draft, else 0).
+ *   total_tokens  host: T = qsl[B];  alpha: host, in [0, 1)
+ * No workspace: one workgroup holds the scores in LDS.  draft_conf and keep may be NULL when
+ * T == B.  Supported: T - B <= 16384.  Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP.
+ */
+int spexis_select_drafts(int32_t num_seqs, int32_t total_tokens, const int32_t* query_start_loc,
+                         const float* draft_conf, float alpha, int32_t* kept_k,
+                         int32_t* kept_query_start_loc, int32_t* keep, void* stream);
 
 #ifdef __cplusplus
 }

@@ -319,6 +319,33 @@ int spexis_accept_with_stats(int32_t num_seqs, int32_t vocab, int32_t max_k, flo
                      accepted_len, out_tokens, row_status, seq_lens_inout, workspace, workspace_bytes, stream);
 }
 
+int spexis_select_drafts(int32_t num_seqs, int32_t total_tokens, const int32_t* query_start_loc,
+                         const float* draft_conf, float alpha, int32_t* kept_k, int32_t* kept_query_start_loc,
+                         int32_t* keep, void* stream) {
+  if (!query_start_loc || !kept_k || !kept_query_start_loc)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_select_drafts: null pointer");
+  if (num_seqs < 0 || total_tokens < num_seqs)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_select_drafts: bad size");
+  if (!(alpha >= 0.f) || !(alpha < 1.f))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_select_drafts: alpha must be in [0, 1)");
+  const int32_t N = total_tokens - num_seqs;
+  if (N > spexis::kSelectMaxDrafts)
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_select_drafts: %d drafts > %d", N, spexis::kSelectMaxDrafts);
+  if (N > 0 && (!draft_conf || !keep)) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_select_drafts: null pointer");
+  if (num_seqs == 0) return ok();
+  spexis::SelectParams p{};
+  p.qsl = query_start_loc;
+  p.conf = draft_conf;
+  p.B = num_seqs;
+  p.T = total_tokens;
+  p.N = N;
+  p.m = (int)std::floor((double)alpha * (double)N);
+  p.kept_k = kept_k;
+  p.kept_qsl = kept_query_start_loc;
+  p.keep = keep;
+  return hip_result(spexis::launch_select(p, (hipStream_t)stream), "spexis_select_drafts");
+}
+
 size_t spexis_lm_head_stats_size(int32_t rows, int32_t vocab) {
   if (rows <= 0 || vocab <= 0) return 0;
   return (size_t)rows * spexis_lm_head_tiles(vocab) * 2 * sizeof(float);

@@ -49,19 +49,29 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
   return v;
 }
-__device__ __forceinline__ int wave_sum_i32(int v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+// DPP lane controls: row_shr:n (n = 1..15), broadcast of lane 15 of each row into the next
+// row, broadcast of lane 31 into rows 2 and 3, and quad permutations.
+constexpr int kDppRowShr = 0x110;
+constexpr int kDppRowBcast15 = 0x142;
+constexpr int kDppRowBcast31 = 0x143;
+constexpr int kDppQuadXor1 = 0xB1;   // quad_perm [1, 0, 3, 2]
+constexpr int kDppQuadXor2 = 0x4E;   // quad_perm [2, 3, 0, 1]
+// Inclusive prefix sum over the lanes of a wave, in DPP moves only (no LDS round trips):
+// shifts by 1, 2, 4 and 8 within each row of 16 lanes (lanes shifted in from outside the row
+// add 0), then row r adds the total of row r-1 (rows 1, 3) and rows 2, 3 add lane 31.
+__device__ __forceinline__ int wave_incl_scan_i32(int v, int lane) {
+  (void)lane;
+  v += __builtin_amdgcn_update_dpp(0, v, kDppRowShr + 1, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, kDppRowShr + 2, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, kDppRowShr + 4, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, kDppRowShr + 8, 0xF, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, kDppRowBcast15, 0xA, 0xF, false);
+  v += __builtin_amdgcn_update_dpp(0, v, kDppRowBcast31, 0xC, 0xF, false);
   return v;
 }
-// Inclusive prefix sum over the lanes of a wave.
-__device__ __forceinline__ int wave_incl_scan_i32(int v, int lane) {
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const int u = __shfl_up(v, o, kWave);
-    if (lane >= o) v += u;
-  }
-  return v;
+// Sum over the lanes of a wave (the same value in every lane).
+__device__ __forceinline__ int wave_sum_i32(int v) {
+  return __builtin_amdgcn_readlane(wave_incl_scan_i32(v, 0), kWave - 1);
 }
 __device__ __forceinline__ int wave_or(int v) {
 #pragma unroll

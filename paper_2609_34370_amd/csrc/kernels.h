@@ -60,6 +60,18 @@ constexpr int kLmRows = 320;   // rows of h per workgroup (ten 32-row MFMA tiles
 constexpr int kLmCols = 128;   // vocabulary columns per workgroup (four waves of 32)
 constexpr int kLmK = 64;       // K per pipeline step (four MFMA k-steps)
 
+// Selective speculation over a batch of B sequences, T query tokens, N = T - B drafts.
+struct SelectParams {
+  const int32_t* qsl;
+  const float* conf;     // [N] draft confidences
+  int B, T, N, m;        // m = floor(alpha * N) drafts dropped
+  int32_t* kept_k;       // [B]
+  int32_t* kept_qsl;     // [B+1]
+  int32_t* keep;         // [N]
+};
+
+constexpr int kSelectMaxDrafts = 16384;
+
 struct AcceptParams {
   int kind;              // 0 probs, 1 logits
   int B, V, max_k, T;
@@ -98,6 +110,7 @@ constexpr int kAcceptSub = 4096;     // vocab entries per partial result (one wo
 hipError_t launch_append(const AppendParams& p, hipStream_t s);
 hipError_t launch_attention(const AttnParams& p, hipStream_t s);
 hipError_t launch_lm_head(const LmParams& p, hipStream_t s);
+hipError_t launch_select(const SelectParams& p, hipStream_t s);
 hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V, float c, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s);
 

@@ -75,6 +75,8 @@ def lib():
     L.spexis_accept_with_stats.argtypes = [i32, i32, i32, f32, i32, P, P, P, P, P, i32, P, P, P, P, P, P, P, P, sz,
                                            P]
     L.spexis_accept_with_stats.restype = ctypes.c_int
+    L.spexis_select_drafts.argtypes = [i32, i32, P, P, f32, P, P, P, P]
+    L.spexis_select_drafts.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -190,3 +192,13 @@ def spexis_accept_with_stats(query_start_loc, target_logits, draft_logits, targe
         _ptr(u_sample, torch.float32), _ptr(accepted_len, torch.int32), _ptr(out_tokens, torch.int32),
         _ptr(row_status, torch.int32), _ptr(seq_lens_inout, torch.int32), _ptr(workspace), ws_bytes,
         _stream(stream)))
+
+
+def spexis_select_drafts(query_start_loc, draft_conf, alpha, kept_k, kept_query_start_loc, keep,
+                         stream=None) -> None:
+    num_seqs = query_start_loc.shape[0] - 1
+    n = draft_conf.shape[0]
+    _check(lib().spexis_select_drafts(
+        num_seqs, num_seqs + n, _ptr(query_start_loc, torch.int32), _ptr(draft_conf, torch.float32) if n else None,
+        ctypes.c_float(alpha), _ptr(kept_k, torch.int32), _ptr(kept_query_start_loc, torch.int32),
+        _ptr(keep, torch.int32) if n else None, _stream(stream)))
