@@ -53,6 +53,8 @@ def lib():
         L.oracle_lm_head.argtypes = [P, P, i64, i32, i32, f32, P, P, P]
         L.oracle_select_drafts.argtypes = [i32, P, P, f32, P, P, P]
         L.oracle_select_drafts.restype = ctypes.c_int
+        L.oracle_lookahead.argtypes = [i32, P, P, P, i32, ctypes.c_double, i32, P, P, P, P]
+        L.oracle_lookahead.restype = ctypes.c_int
         L.oracle_softmax.restype = None
         L.oracle_accept.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, P, P]
         L.oracle_accept.restype = None
@@ -151,6 +153,20 @@ def select_drafts(qsl, conf, alpha: float):
     if rc != 0:
         raise ValueError("oracle_select_drafts: bad arguments")
     return kept_k, kept_qsl, keep[:N]
+
+
+def lookahead(cur_len, remaining, precision, pp: int, theta: float, iters: int = 64):
+    """Algorithm 1: (mem, e_gen, e_nfin, e_lfin), each fp64 [iters], for the running requests'
+    current lengths, predicted remaining lengths and prediction precisions."""
+    n = len(cur_len)
+    cl = _c(cur_len, np.int64) if n else np.zeros(1, np.int64)
+    rm = _c(remaining, np.int32) if n else np.zeros(1, np.int32)
+    pr = _c(precision, np.float64) if n else np.zeros(1, np.float64)
+    out = [np.empty(iters, np.float64) for _ in range(4)]
+    rc = lib().oracle_lookahead(n, _p(cl), _p(rm), _p(pr), pp, ctypes.c_double(theta), iters, *[_p(o) for o in out])
+    if rc != 0:
+        raise ValueError("oracle_lookahead: bad arguments")
+    return tuple(out)
 
 
 def accept(qsl, target: np.ndarray, draft: np.ndarray, draft_ids, u_accept, u_sample, max_k: int = None,

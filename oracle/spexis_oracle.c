@@ -24,6 +24,7 @@
  *                         normalised residual max(0, p - q); otherwise sample the bonus token
  *                         from p_k), with every decision taken in exact arithmetic so that any
  *                         correct implementation reaches the same integers.
+ *   oracle_lookahead   -- the look-ahead KV-memory estimate of Algorithm 1 (Sec. 5).
  *
  * Cache layout (the library's documented format, restated here independently):
  *   K pool: bf16 [num_blocks][Hkv][D/8][bs][8]
@@ -411,6 +412,62 @@ void oracle_accept(int32_t B, int32_t V, int32_t max_k, const int32_t* qsl, cons
     if (token < 0) row_status[b] = ORACLE_EMPTY_ROW;
     tok[a] = token;
   }
+}
+
+/*
+ * Look-ahead memory estimate (Sec. 5, Remaining-Length-Aware Scheduling; Algorithm 1): the
+ * expected KV-cache tokens held by the running requests over the next `iters` decoding
+ * iterations of a pipeline of depth pp whose speculation is accepted with probability theta.
+ * Per request, a rejection costs pp iterations and an acceptance one; after i iterations with w
+ * rejections, t = i - pp*w tokens were accepted and k = t + w generated, with probability
+ *   p(i, w) = C(k, t) * theta^t * (1 - theta)^w,       w = 0 .. floor(i / pp).
+ * For every i = 1 .. iters (all sums in fp64, in the order written):
+ *   E_gen  = sum_w k * p(i, w)                                   generated tokens per request
+ *   Pfin_r = prec[r] * sum_w [k >= remaining[r]] * p(i, w)       completion probability of r
+ *   E_nfin = sum_r Pfin_r,  E_lfin = sum_r cur_len[r] * Pfin_r
+ *   mem[i-1] = L_total + (n - E_nfin) * E_gen - E_lfin,          L_total = sum_r cur_len[r].
+ * prec[r] is the precision of the length prediction for request r's predicted remaining length
+ * (the paper's E(tau)).  e_gen, e_nfin and e_lfin may be NULL; otherwise they receive the
+ * per-iteration intermediates.  Returns 0, or -1 on bad arguments.
+ */
+int oracle_lookahead(int32_t n, const int64_t* cur_len, const int32_t* remaining, const double* prec,
+                     int32_t pp, double theta, int32_t iters, double* mem, double* e_gen, double* e_nfin,
+                     double* e_lfin) {
+  if (n < 0 || pp < 1 || iters < 1 || !(theta >= 0.0 && theta <= 1.0) || !mem) return -1;
+  if (n > 0 && (!cur_len || !remaining || !prec)) return -1;
+  double l_total = 0.0;
+  for (int32_t r = 0; r < n; ++r) l_total += (double)cur_len[r];
+  for (int32_t i = 1; i <= iters; ++i) {
+    const int32_t w_max = i / pp;
+    double gen = 0.0;
+    for (int32_t w = 0; w <= w_max; ++w) {
+      const int32_t t = i - pp * w, k = t + w;
+      double binom = 1.0;                       /* C(t + w, t) = prod_{j=1..t} (w + j) / j */
+      for (int32_t j = 1; j <= t; ++j) binom = binom * (double)(w + j) / (double)j;
+      const double p = binom * pow(theta, t) * pow(1.0 - theta, w);
+      gen += (double)k * p;
+    }
+    double nfin = 0.0, lfin = 0.0;
+    for (int32_t r = 0; r < n; ++r) {
+      double s = 0.0;
+      for (int32_t w = 0; w <= w_max; ++w) {
+        const int32_t t = i - pp * w, k = t + w;
+        if (k >= remaining[r]) {
+          double binom = 1.0;
+          for (int32_t j = 1; j <= t; ++j) binom = binom * (double)(w + j) / (double)j;
+          s += binom * pow(theta, t) * pow(1.0 - theta, w);
+        }
+      }
+      const double pfin = prec[r] * s;
+      nfin += pfin;
+      lfin += (double)cur_len[r] * pfin;
+    }
+    mem[i - 1] = l_total + ((double)n - nfin) * gen - lfin;
+    if (e_gen) e_gen[i - 1] = gen;
+    if (e_nfin) e_nfin[i - 1] = nfin;
+    if (e_lfin) e_lfin[i - 1] = lfin;
+  }
+  return 0;
 }
 
 /* Number of OpenMP threads the parallel loops above use (for reporting). */
