@@ -97,17 +97,19 @@ def main():
     ap.add_argument("--ingest-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic.json from two rocprofv3 --pmc counter_collection.csv files "
                          "(FETCH_SIZE, WRITE_SIZE) of runs with --copy-probe N (pass the same N); needs no GPU")
-    ap.add_argument("--component", choices=["step", "lm_head", "select"], default="step",
+    ap.add_argument("--component", choices=["step", "lm_head", "select", "lookahead"], default="step",
                     help="lm_head: time spexis_lm_head and acceptance from its fused statistics at the "
                          "workload's shape instead of the verification step; select: time selective "
-                         "speculation and measure the acceptance rate of the kept drafts (each prints its "
-                         "own JSON line)")
+                         "speculation and measure the acceptance rate of the kept drafts; lookahead: time "
+                         "Algorithm 1's memory estimate (each prints its own JSON line)")
     ap.add_argument("--alpha", type=float, nargs="+", default=[0.15, 0.3])
     args = ap.parse_args()
     if args.component == "lm_head":
         return bench_lm_head(args)
     if args.component == "select":
         return bench_select(args)
+    if args.component == "lookahead":
+        return bench_lookahead(args)
     if args.ingest_traffic:
         if args.copy_probe <= 0:
             raise SystemExit("--ingest-traffic needs --copy-probe N: the copy size the counter runs used")
@@ -371,6 +373,42 @@ def bench_select(args):
     log(f"[select] 16384 drafts (1024 x 16): {us_max:.1f} us")
     print(json.dumps({"component": "spexis_select_drafts", "workload": spec.name, "batch": B, "drafts": N,
                       "alphas": rows, "us_16384_drafts": round(us_max, 2), "data": "synthetic"}), flush=True)
+
+
+def bench_lookahead(args):
+    """Algorithm 1's look-ahead memory estimate over 64 iterations for running batches of the
+    workload's size and larger (request lengths from the workload's context distribution,
+    remaining lengths on the ordinal thresholds, precision 0.83, depth 4, theta 0.7)."""
+    import torch
+
+    from paper_2609_34370_amd import spexis as sx
+    from paper_2609_34370_amd import workloads as wl
+
+    spec = wl.WORKLOADS[args.workload]
+    rows = []
+    for n in (spec.batch, 4096, 65536):
+        rng = np.random.default_rng(n)
+        batch = wl.make_batch(wl.spec_with(spec.wid, batch=min(n, spec.batch)), seed=args.seed)
+        ell = torch.as_tensor(np.resize(batch.ctx_lens.astype(np.int64), n), device="cuda")
+        tau = torch.as_tensor(rng.choice(np.array([4, 8, 16, 32, 64, 1 << 30], np.int32), n), device="cuda")
+        prec = torch.where(tau < (1 << 30), 0.83, 0.0).to(torch.float64)
+        mem = torch.empty(64, dtype=torch.float64, device="cuda")
+        call = lambda: sx.spexis_lookahead_memory(ell, tau, prec, 4, 0.7, mem)
+        for _ in range(args.warmup):
+            call()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(args.steps):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / args.steps
+        m = mem.cpu().numpy()
+        rows.append({"requests": n, "us": round(us, 2), "mem_1": round(float(m[0]), 1), "mem_64": round(float(m[63]), 1)})
+        log(f"[lookahead] {n} requests: {us:.1f} us per call; estimate {m[0]:.0f} -> {m[63]:.0f} tokens")
+    print(json.dumps({"component": "spexis_lookahead_memory", "workload": spec.name, "iters": 64, "pp": 4,
+                      "theta": 0.7, "runs": rows, "data": "synthetic"}), flush=True)
 
 
 ATTN_KERNELS = ("verify_attn_kernel", "attn_merge_kernel")   # the launches of spexis_verify_attention

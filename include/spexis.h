@@ -14,6 +14,7 @@
  *   spexis_lm_head           logits = h W^T with fused softmax statistics (next to accept)
  *   spexis_accept_with_stats acceptance from logits whose statistics are known
  *   spexis_select_drafts     selective speculation: drop the least confident drafts first
+ *   spexis_lookahead_memory  look-ahead KV-memory estimate of the running requests (Algorithm 1)
  *   spexis_softmax_rows      temperature softmax of logit rows (probability inputs)
  *
  * Conventions shared by every entry point
@@ -272,6 +273,30 @@ int spexis_accept_with_stats(int32_t num_seqs, int32_t vocab, int32_t max_k, flo
 int spexis_select_drafts(int32_t num_seqs, int32_t total_tokens, const int32_t* query_start_loc,
                          const float* draft_conf, float alpha, int32_t* kept_k,
                          int32_t* kept_query_start_loc, int32_t* keep, void* stream);
+
+/*
+ * spexis_lookahead_memory -- the look-ahead memory estimate of Algorithm 1 (Sec. 5,
+ * Remaining-Length-Aware Scheduling): the expected KV-cache tokens the running requests hold
+ * in each of the next `iters` decoding iterations, which the scheduler compares with the cache
+ * size before admitting a new request.
+ *   For iteration i = 1 .. iters and w = 0 .. floor(i / pp) rejections, t = i - pp*w accepted
+ *   and k = t + w generated tokens have probability p(i, w) = C(k, t) theta^t (1 - theta)^w;
+ *   E_gen(i) = sum_w k p(i, w);  Pfin_r(i) = precision[r] * sum_{w : k >= remaining[r]} p(i, w);
+ *   mem[i-1] = sum_r cur_len[r] + (n - sum_r Pfin_r) E_gen - sum_r cur_len[r] Pfin_r.
+ *   num_requests   n >= 0, the running requests
+ *   cur_len        [n] int64, current length of each request (tokens in the cache)
+ *   remaining      [n] int32, predicted remaining length (the ordinal thresholds 4, 8, .., 64,
+ *                  or a large value for "more than 64")
+ *   precision      [n] fp64, the precision of that prediction, the paper's E(tau)
+ *   pp, theta      host: pipeline depth >= 1 and speculation accuracy in [0, 1]
+ *   iters          host: look-ahead iterations, 1 .. 1024 (the paper uses 64)
+ *   mem            [iters] fp64 output; e_gen, e_nfin, e_lfin: optional [iters] fp64 outputs of
+ *                  E_gen, sum_r Pfin_r and sum_r cur_len[r] Pfin_r (NULL to skip)
+ * All fp64.  No workspace.  Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP.
+ */
+int spexis_lookahead_memory(int32_t num_requests, const int64_t* cur_len, const int32_t* remaining,
+                            const double* precision, int32_t pp, double theta, int32_t iters,
+                            double* mem, double* e_gen, double* e_nfin, double* e_lfin, void* stream);
 
 #ifdef __cplusplus
 }

@@ -346,6 +346,34 @@ int spexis_select_drafts(int32_t num_seqs, int32_t total_tokens, const int32_t* 
   return hip_result(spexis::launch_select(p, (hipStream_t)stream), "spexis_select_drafts");
 }
 
+int spexis_lookahead_memory(int32_t num_requests, const int64_t* cur_len, const int32_t* remaining,
+                            const double* precision, int32_t pp, double theta, int32_t iters, double* mem,
+                            double* e_gen, double* e_nfin, double* e_lfin, void* stream) {
+  if (!mem) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lookahead_memory: null pointer");
+  if (num_requests < 0 || pp < 1 || iters < 1)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lookahead_memory: bad size");
+  if (!(theta >= 0.0 && theta <= 1.0))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lookahead_memory: theta must be in [0, 1]");
+  if (iters > spexis::kLookaheadMaxIters)
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_lookahead_memory: %d iterations > %d", iters,
+                spexis::kLookaheadMaxIters);
+  if (num_requests > 0 && (!cur_len || !remaining || !precision))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lookahead_memory: null pointer");
+  spexis::LookaheadParams p{};
+  p.cur_len = cur_len;
+  p.remaining = remaining;
+  p.prec = precision;
+  p.n = num_requests;
+  p.pp = pp;
+  p.iters = iters;
+  p.theta = theta;
+  p.mem = mem;
+  p.e_gen = e_gen;
+  p.e_nfin = e_nfin;
+  p.e_lfin = e_lfin;
+  return hip_result(spexis::launch_lookahead(p, (hipStream_t)stream), "spexis_lookahead_memory");
+}
+
 size_t spexis_lm_head_stats_size(int32_t rows, int32_t vocab) {
   if (rows <= 0 || vocab <= 0) return 0;
   return (size_t)rows * spexis_lm_head_tiles(vocab) * 2 * sizeof(float);

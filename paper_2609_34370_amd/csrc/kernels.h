@@ -72,6 +72,20 @@ struct SelectParams {
 
 constexpr int kSelectMaxDrafts = 16384;
 
+struct LookaheadParams {
+  const int64_t* cur_len;    // [n] current length of each running request
+  const int32_t* remaining;  // [n] predicted remaining length
+  const double* prec;        // [n] precision of that prediction
+  int n, pp, iters;
+  double theta;
+  double* mem;               // [iters]
+  double* e_gen;             // [iters] or null
+  double* e_nfin;            // [iters] or null
+  double* e_lfin;            // [iters] or null
+};
+
+constexpr int kLookaheadMaxIters = 1024;
+
 struct AcceptParams {
   int kind;              // 0 probs, 1 logits
   int B, V, max_k, T;
@@ -111,6 +125,7 @@ hipError_t launch_append(const AppendParams& p, hipStream_t s);
 hipError_t launch_attention(const AttnParams& p, hipStream_t s);
 hipError_t launch_lm_head(const LmParams& p, hipStream_t s);
 hipError_t launch_select(const SelectParams& p, hipStream_t s);
+hipError_t launch_lookahead(const LookaheadParams& p, hipStream_t s);
 hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V, float c, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s);
 

@@ -77,6 +77,8 @@ def lib():
     L.spexis_accept_with_stats.restype = ctypes.c_int
     L.spexis_select_drafts.argtypes = [i32, i32, P, P, f32, P, P, P, P]
     L.spexis_select_drafts.restype = ctypes.c_int
+    L.spexis_lookahead_memory.argtypes = [i32, P, P, P, i32, ctypes.c_double, i32, P, P, P, P, P]
+    L.spexis_lookahead_memory.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -202,3 +204,14 @@ def spexis_select_drafts(query_start_loc, draft_conf, alpha, kept_k, kept_query_
         num_seqs, num_seqs + n, _ptr(query_start_loc, torch.int32), _ptr(draft_conf, torch.float32) if n else None,
         ctypes.c_float(alpha), _ptr(kept_k, torch.int32), _ptr(kept_query_start_loc, torch.int32),
         _ptr(keep, torch.int32) if n else None, _stream(stream)))
+
+
+def spexis_lookahead_memory(cur_len, remaining, precision, pp, theta, mem, e_gen=None, e_nfin=None, e_lfin=None,
+                            stream=None) -> None:
+    """Algorithm 1's look-ahead memory estimate for len(mem) iterations (fp64 outputs)."""
+    n = cur_len.shape[0]
+    opt = lambda t: _ptr(t, torch.float64) if t is not None else None
+    _check(lib().spexis_lookahead_memory(
+        n, _ptr(cur_len, torch.int64) if n else None, _ptr(remaining, torch.int32) if n else None,
+        _ptr(precision, torch.float64) if n else None, pp, ctypes.c_double(theta), mem.shape[0],
+        _ptr(mem, torch.float64), opt(e_gen), opt(e_nfin), opt(e_lfin), _stream(stream)))
