@@ -15,6 +15,8 @@
  *   spexis_accept_with_stats acceptance from logits whose statistics are known
  *   spexis_select_drafts     selective speculation: drop the least confident drafts first
  *   spexis_lookahead_memory  look-ahead KV-memory estimate of the running requests (Algorithm 1)
+ *   spexis_linear            a linear layer of the drafting adapter (bf16, fp32 accumulation)
+ *   spexis_sample_tokens     one token per row of logits or probabilities, with its probability
  *   spexis_softmax_rows      temperature softmax of logit rows (probability inputs)
  *
  * Conventions shared by every entry point
@@ -273,6 +275,51 @@ int spexis_accept_with_stats(int32_t num_seqs, int32_t vocab, int32_t max_k, flo
 int spexis_select_drafts(int32_t num_seqs, int32_t total_tokens, const int32_t* query_start_loc,
                          const float* draft_conf, float alpha, int32_t* kept_k,
                          int32_t* kept_query_start_loc, int32_t* keep, void* stream);
+
+/*
+ * spexis_linear -- a linear layer of the drafting adapter (Implementation: the adapter is a
+ * linear layer and an attention layer followed by the LM head), also its attention layer's
+ * input and output projections:
+ *   y[r][o] = bf16( sum_j x[r][j] * W[o][j]  (+ residual[r][o]) )
+ * with fp32 accumulation (the order over j is the library's) and one round to nearest even.
+ *   x         [rows][in_features] bf16;  weight [out_features][in_features] bf16 (row-major)
+ *   residual  [rows][out_features] bf16 or NULL;  y: [rows][out_features] bf16 output (may not
+ *             alias x or weight; may alias residual)
+ *   workspace >= spexis_linear_workspace_size(rows, out_features, in_features) bytes (0 when
+ *             the problem fills the chip without splitting K; then it may be NULL)
+ * Supported: in_features % 256 == 0.  Errors: INVALID_ARGUMENT, UNSUPPORTED,
+ * WORKSPACE_TOO_SMALL, HIP.
+ */
+int spexis_linear(const void* x, const void* weight, const void* residual, int32_t rows, int32_t out_features,
+                  int32_t in_features, void* y, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace spexis_linear needs for this problem (0 if none). */
+size_t spexis_linear_workspace_size(int32_t rows, int32_t out_features, int32_t in_features);
+
+/*
+ * spexis_sample_tokens -- draws one token per row from softmax(logits / T) (kind LOGITS) or from
+ * the given fp32 probabilities (kind PROBS), and returns the token's probability.  Drafting uses
+ * it on the adapter's LM-head rows (Implementation): the token is the draft x, its probability
+ * q(x) the draft's confidence that selective speculation ranks (Sec. 5).  The draw is the bonus
+ * sampling of spexis_accept with no drafts: the exact fixed-point inverse CDF with the row's
+ * uniform, so PROBS input gives the same token as any exact implementation of that rule.
+ *   rows, vocab     R >= 0 rows of V entries;  input [R][V] fp32
+ *   stats           optional (LOGITS only): [R][stats_tiles][2] from spexis_lm_head at the same
+ *                   temperature; then no pass over the rows computes their normalisers
+ *   u               [R] fp32 uniforms in [0, 1)
+ *   tokens          [R] int32 output (-1 for a row that cannot be sampled)
+ *   token_prob      [R] fp32 output or NULL: the probability of the token (0 when none); in
+ *                   LOGITS mode computed as in spexis_accept (2^(x c - M) / Z, c = log2(e) / T)
+ *   row_status      [R] int32 output, SPEXIS_ROW_* as in spexis_accept
+ *   workspace       >= spexis_sample_workspace_size(R, V) bytes
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED (V > 2^22), WORKSPACE_TOO_SMALL, HIP.
+ */
+int spexis_sample_tokens(int32_t kind, int32_t rows, int32_t vocab, float temperature, const float* input,
+                         const float* stats, int32_t stats_tiles, const float* u, int32_t* tokens, float* token_prob,
+                         int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace spexis_sample_tokens needs. */
+size_t spexis_sample_workspace_size(int32_t rows, int32_t vocab);
 
 /*
  * spexis_lookahead_memory -- the look-ahead memory estimate of Algorithm 1 (Sec. 5,

@@ -53,6 +53,7 @@ def lib():
         L.oracle_lm_head.argtypes = [P, P, i64, i32, i32, f32, P, P, P]
         L.oracle_select_drafts.argtypes = [i32, P, P, f32, P, P, P]
         L.oracle_select_drafts.restype = ctypes.c_int
+        L.oracle_linear.argtypes = [P, P, P, i64, i32, i32, P]
         L.oracle_lookahead.argtypes = [i32, P, P, P, i32, ctypes.c_double, i32, P, P, P, P]
         L.oracle_lookahead.restype = ctypes.c_int
         L.oracle_softmax.restype = None
@@ -153,6 +154,46 @@ def select_drafts(qsl, conf, alpha: float):
     if rc != 0:
         raise ValueError("oracle_select_drafts: bad arguments")
     return kept_k, kept_qsl, keep[:N]
+
+
+def linear(x: np.ndarray, W: np.ndarray, residual=None):
+    """fp64 y = x W^T (+ residual) of bf16 bit arrays x [rows, in], W [out, in], residual [rows, out]."""
+    xx = _c(x, np.uint16)
+    ww = _c(W, np.uint16)
+    rows, n_in = xx.shape
+    n_out, n_in2 = ww.shape
+    assert n_in == n_in2
+    rr = _c(residual, np.uint16) if residual is not None else None
+    if rr is not None:
+        assert rr.shape == (rows, n_out)
+    y = np.empty((rows, n_out), np.float64)
+    lib().oracle_linear(_p(xx), _p(ww), _p(rr) if rr is not None else None, rows, n_out, n_in, _p(y))
+    return y
+
+
+def to_bf16(x) -> np.ndarray:
+    """Bits of the bf16 nearest to each value (ties to even), through fp32."""
+    f = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    rounded = f + np.uint32(0x7FFF) + ((f >> np.uint32(16)) & np.uint32(1))
+    return (rounded >> np.uint32(16)).astype(np.uint16)
+
+
+def bf16_value(bits) -> np.ndarray:
+    """fp64 values of bf16 bit patterns."""
+    return (np.asarray(bits, np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+
+
+def sample(probs: np.ndarray, u):
+    """One token per fp32 probability row by the exact inverse CDF of acceptance with no drafts,
+    and its probability: (tokens [R], token_prob [R], row_status [R])."""
+    pr = _c(probs, np.float32)
+    R, V = pr.shape
+    qsl = np.arange(R + 1, dtype=np.int32)
+    _, toks, status, _ = accept(qsl, pr, np.zeros((0, V), np.float32), np.zeros(0, np.int32), np.zeros(0, np.float32),
+                                u, max_k=0)
+    tok = toks[:, 0].copy()
+    prob = np.where(tok >= 0, pr[np.arange(R), np.maximum(tok, 0)], np.float32(0)).astype(np.float32)
+    return tok, prob, status
 
 
 def lookahead(cur_len, remaining, precision, pp: int, theta: float, iters: int = 64):

@@ -17,6 +17,7 @@
  *   oracle_softmax     -- temperature softmax of fp32 logits, in fp64, rounded to fp32.
  *   oracle_lm_head     -- the output projection in front of acceptance (logits = h W^T over
  *                         bf16 inputs, in fp64) and each row's softmax statistics.
+ *   oracle_linear      -- a linear layer of the drafting adapter (y = x W^T + residual, fp64).
  *   oracle_select_drafts -- acceptance-guided selective speculation: drop the alpha fraction of
  *                         the batch's draft tokens with the lowest confidence (Sec. 5).
  *   oracle_accept      -- speculative-sampling acceptance (accept x_i with probability
@@ -215,6 +216,32 @@ void oracle_lm_head(const uint16_t* h, const uint16_t* W, int64_t rows, int32_t 
     if (logits) memcpy(logits + r * V, lr, sizeof(double) * (size_t)V);
     free(hr);
     free(lr);
+  }
+}
+
+/* ------------------------------------------------------------ linear layer */
+
+/*
+ * A linear layer of the drafting adapter (Implementation: a linear layer and an attention
+ * layer, then the LM head): for bf16 inputs x [rows][in] and weights W [out][in], and an
+ * optional bf16 residual R [rows][out],
+ *   y[r][o] = sum_j x[r][j] * W[o][j]  (+ R[r][o])             (fp64, exact products)
+ * y is fp64 [rows][out]; residual may be NULL.
+ */
+void oracle_linear(const uint16_t* x, const uint16_t* W, const uint16_t* residual, int64_t rows, int32_t out,
+                   int32_t in, double* y) {
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t r = 0; r < rows; ++r) {
+    double* xr = (double*)malloc(sizeof(double) * (size_t)in);
+    for (int32_t j = 0; j < in; ++j) xr[j] = bf16_to_double(x[r * in + j]);
+    for (int32_t o = 0; o < out; ++o) {
+      double acc = 0.0;
+      const uint16_t* wo = W + (int64_t)o * in;
+      for (int32_t j = 0; j < in; ++j) acc += xr[j] * bf16_to_double(wo[j]);
+      if (residual) acc += bf16_to_double(residual[r * out + o]);
+      y[r * out + o] = acc;
+    }
+    free(xr);
   }
 }
 

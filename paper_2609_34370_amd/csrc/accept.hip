@@ -58,8 +58,8 @@ __device__ __forceinline__ Geom load_geom(const AcceptParams& p, int b) {
 // Rows of sequence b: first target row t0, first draft row d0, draft count k (clamped so that
 // every row index stays inside its buffer); n = its query tokens (the sequence is valid iff n >= 1).
 __device__ __forceinline__ Geom seq_geom(const AcceptParams& p, int b, int& n) {
-  const int a0 = clampi(p.qsl[b], 0, p.T);
-  const int a1 = clampi(p.qsl[b + 1], a0, p.T);
+  const int a0 = p.qsl ? clampi(p.qsl[b], 0, p.T) : b;
+  const int a1 = p.qsl ? clampi(p.qsl[b + 1], a0, p.T) : b + 1;
   n = a1 - a0;
   const int nd = p.T - p.B > 0 ? p.T - p.B : 0;
   int k = n - 1;
@@ -190,6 +190,7 @@ __device__ __forceinline__ float* lse_slot(const AcceptParams& p, int b, int i, 
 __device__ void write_outputs(const AcceptParams& p, int b, const Geom& g, int a, int token, int status) {
   int32_t* row = p.out_tokens + (int64_t)b * (p.max_k + 1);
   for (int i = 0; i <= p.max_k; ++i) row[i] = i < a ? p.ids[g.d0 + i] : (i == a ? token : -1);
+  if (p.tok_prob && token < 0) p.tok_prob[b] = 0.f;
   p.accepted_len[b] = a;
   p.row_status[b] = status;
   if (p.seq_lens_inout) p.seq_lens_inout[b] -= g.k - a;
@@ -199,6 +200,7 @@ __device__ void write_outputs(const AcceptParams& p, int b, const Geom& g, int a
 __device__ void write_invalid(const AcceptParams& p, int b, int n) {
   int32_t* row = p.out_tokens + (int64_t)b * (p.max_k + 1);
   for (int i = 0; i <= p.max_k; ++i) row[i] = -1;
+  if (p.tok_prob) p.tok_prob[b] = 0.f;
   p.accepted_len[b] = 0;
   p.row_status[b] = n >= 1 ? SPEXIS_ROW_BAD_TOKEN : SPEXIS_ROW_BAD_VALUE;
   p.st_mode[b] = kDone;
@@ -696,14 +698,17 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
   const uint64_t hi = pre + mine;
   if (pre <= tt && tt < hi) {
     int token = base;
+    float prob = 0.f;
 #pragma unroll
     for (int e = 0; e < kRun; ++e) {
       if (tt < pre + wv[e]) {
         token = base + e;
+        prob = prob_of(r, pv[e], p.c, false);
         break;
       }
       pre += wv[e];
     }
+    if (p.tok_prob) p.tok_prob[b] = prob;
     write_outputs(p, b, g, a, token, SPEXIS_ROW_OK);
   }
 }

@@ -226,13 +226,15 @@ int accept_impl(const char* who, int32_t kind, int32_t num_seqs, int32_t vocab, 
                 const float* target_stats, const float* draft_stats, int32_t stats_parts,
                 const int32_t* draft_ids, const float* u_accept, const float* u_sample, int32_t* accepted_len,
                 int32_t* out_tokens, int32_t* row_status, int32_t* seq_lens_inout, void* workspace,
-                size_t workspace_bytes, void* stream) {
+                size_t workspace_bytes, void* stream, float* tok_prob = nullptr) {
+  // query_start_loc == nullptr (internal callers only): every sequence is one row, no drafts
   if (kind != SPEXIS_INPUT_PROBS && kind != SPEXIS_INPUT_LOGITS)
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: kind %d is neither PROBS nor LOGITS", who, kind);
   if (num_seqs < 0 || vocab <= 0 || max_k < 0 || total_tokens < num_seqs)
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: bad size", who);
   const bool has_drafts = total_tokens > num_seqs;
-  if (!query_start_loc || !target || !u_sample || !accepted_len || !out_tokens || !row_status ||
+  if ((!query_start_loc && total_tokens != num_seqs) || !target || !u_sample || !accepted_len || !out_tokens ||
+      !row_status ||
       (has_drafts && (!draft || !draft_ids || !u_accept)))
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: null pointer", who);
   if (kind == SPEXIS_INPUT_LOGITS && (!(temperature > 0.f) || !std::isfinite(temperature)))
@@ -266,6 +268,7 @@ int accept_impl(const char* who, int32_t kind, int32_t num_seqs, int32_t vocab, 
   p.out_tokens = out_tokens;
   p.row_status = row_status;
   p.seq_lens_inout = seq_lens_inout;
+  p.tok_prob = tok_prob;
   p.geo = reinterpret_cast<int32_t*>(ws + lay.geo);
   p.st_a = reinterpret_cast<int32_t*>(ws + lay.st_a);
   p.st_mode = reinterpret_cast<int32_t*>(ws + lay.st_mode);
@@ -319,6 +322,32 @@ int spexis_accept_with_stats(int32_t num_seqs, int32_t vocab, int32_t max_k, flo
                      accepted_len, out_tokens, row_status, seq_lens_inout, workspace, workspace_bytes, stream);
 }
 
+size_t spexis_sample_workspace_size(int32_t rows, int32_t vocab) {
+  if (rows <= 0 || vocab <= 0) return 0;
+  return accept_layout(rows, vocab, 0).total + (size_t)round_up((int64_t)rows * 4, 256);
+}
+
+int spexis_sample_tokens(int32_t kind, int32_t rows, int32_t vocab, float temperature, const float* input,
+                         const float* stats, int32_t stats_tiles, const float* u, int32_t* tokens, float* token_prob,
+                         int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream) {
+  if (rows < 0 || vocab <= 0) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_sample_tokens: bad size");
+  if (!input || !u || !tokens || !row_status)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_sample_tokens: null pointer");
+  if (stats && kind != SPEXIS_INPUT_LOGITS)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_sample_tokens: statistics need logits");
+  if (stats && stats_tiles <= 0) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_sample_tokens: stats_tiles <= 0");
+  if (rows == 0) return ok();
+  const size_t need = spexis_sample_workspace_size(rows, vocab);
+  if (!workspace || workspace_bytes < need)
+    return fail(SPEXIS_ERR_WORKSPACE_TOO_SMALL, "spexis_sample_tokens: workspace %zu bytes < %zu needed",
+                workspace_bytes, need);
+  const size_t acc_bytes = accept_layout(rows, vocab, 0).total;
+  int32_t* accepted = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + acc_bytes);
+  return accept_impl("spexis_sample_tokens", kind, rows, vocab, 0, temperature, rows, nullptr, input, nullptr,
+                     stats, stats, stats ? stats_tiles : 0, nullptr, nullptr, u, accepted, tokens, row_status,
+                     nullptr, workspace, acc_bytes, stream, token_prob);
+}
+
 int spexis_select_drafts(int32_t num_seqs, int32_t total_tokens, const int32_t* query_start_loc,
                          const float* draft_conf, float alpha, int32_t* kept_k, int32_t* kept_query_start_loc,
                          int32_t* keep, void* stream) {
@@ -344,6 +373,40 @@ int spexis_select_drafts(int32_t num_seqs, int32_t total_tokens, const int32_t* 
   p.kept_qsl = kept_query_start_loc;
   p.keep = keep;
   return hip_result(spexis::launch_select(p, (hipStream_t)stream), "spexis_select_drafts");
+}
+
+size_t spexis_linear_workspace_size(int32_t rows, int32_t out_features, int32_t in_features) {
+  if (rows <= 0 || out_features <= 0 || in_features <= 0 || in_features % 256 != 0) return 0;
+  spexis::LinearParams p{};
+  spexis::linear_plan(rows, out_features, in_features, p);
+  return p.S > 1 ? (size_t)p.S * rows * out_features * sizeof(float) : 0;
+}
+
+int spexis_linear(const void* x, const void* weight, const void* residual, int32_t rows, int32_t out_features,
+                  int32_t in_features, void* y, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!x || !weight || !y) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_linear: null pointer");
+  if (rows < 0 || out_features <= 0 || in_features <= 0)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_linear: bad size");
+  if (in_features % 256 != 0)
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_linear: in_features %d is not a multiple of 256", in_features);
+  if (rows == 0) return ok();
+  if ((int64_t)rows * in_features >= (1ll << 40) || (int64_t)out_features * in_features >= (1ll << 40) ||
+      (int64_t)rows * out_features >= (1ll << 36))
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_linear: problem too large");
+  spexis::LinearParams p{};
+  spexis::linear_plan(rows, out_features, in_features, p);
+  if ((int64_t)(p.ntiles * (int64_t)p.S + 7) / 8 * 8 * p.mgroups >= (1ll << 31))
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_linear: problem too large");
+  const size_t need = spexis_linear_workspace_size(rows, out_features, in_features);
+  if (need > 0 && (!workspace || workspace_bytes < need))
+    return fail(SPEXIS_ERR_WORKSPACE_TOO_SMALL, "spexis_linear: workspace %zu bytes < %zu needed", workspace_bytes,
+                need);
+  p.x = x;
+  p.w = weight;
+  p.res = residual;
+  p.y = y;
+  p.part = static_cast<float*>(workspace);
+  return hip_result(spexis::launch_linear(p, (hipStream_t)stream), "spexis_linear");
 }
 
 int spexis_lookahead_memory(int32_t num_requests, const int64_t* cur_len, const int32_t* remaining,

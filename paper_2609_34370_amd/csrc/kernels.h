@@ -72,6 +72,20 @@ struct SelectParams {
 
 constexpr int kSelectMaxDrafts = 16384;
 
+struct LinearParams {
+  const void* x;     // bf16 [M][K]
+  const void* w;     // bf16 [N][K]
+  const void* res;   // bf16 [M][N] or null
+  void* y;           // bf16 [M][N]
+  float* part;       // fp32 [S][M][N] when S > 1
+  int M, N, K;
+  int nrt;           // row tiles of 32 per workgroup (1, 2 or 4)
+  int ntiles;        // column tiles of 32
+  int mgroups;       // row groups of 32 * nrt
+  int S;             // K split over workgroups
+  int kw;            // K values per wave
+};
+
 struct LookaheadParams {
   const int64_t* cur_len;    // [n] current length of each running request
   const int32_t* remaining;  // [n] predicted remaining length
@@ -91,7 +105,7 @@ struct AcceptParams {
   int B, V, max_k, T;
   int nsub;              // ceil(V / kAcceptSub): partial results are kept per sub-chunk
   float c;               // log2(e) / temperature (logits mode)
-  const int32_t* qsl;
+  const int32_t* qsl;    // null: sequence b is row b alone (no drafts; plain sampling)
   const float* target;
   const float* draft;
   const int32_t* ids;
@@ -101,6 +115,7 @@ struct AcceptParams {
   int32_t* out_tokens;
   int32_t* row_status;
   int32_t* seq_lens_inout;
+  float* tok_prob;       // [B] or null: probability of the emitted token under p at its position
   // workspace views
   int32_t* geo;          // [B][4] first target row, first draft row, k, valid
   int32_t* st_a;         // [B] final a_b
@@ -126,6 +141,8 @@ hipError_t launch_attention(const AttnParams& p, hipStream_t s);
 hipError_t launch_lm_head(const LmParams& p, hipStream_t s);
 hipError_t launch_select(const SelectParams& p, hipStream_t s);
 hipError_t launch_lookahead(const LookaheadParams& p, hipStream_t s);
+void linear_plan(int M, int N, int K, LinearParams& p);
+hipError_t launch_linear(const LinearParams& p, hipStream_t s);
 hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V, float c, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s);
 

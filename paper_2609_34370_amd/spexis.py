@@ -77,6 +77,14 @@ def lib():
     L.spexis_accept_with_stats.restype = ctypes.c_int
     L.spexis_select_drafts.argtypes = [i32, i32, P, P, f32, P, P, P, P]
     L.spexis_select_drafts.restype = ctypes.c_int
+    L.spexis_sample_tokens.argtypes = [i32, i32, i32, f32, P, P, i32, P, P, P, P, P, sz, P]
+    L.spexis_sample_tokens.restype = ctypes.c_int
+    L.spexis_sample_workspace_size.argtypes = [i32, i32]
+    L.spexis_sample_workspace_size.restype = sz
+    L.spexis_linear.argtypes = [P, P, P, i32, i32, i32, P, P, sz, P]
+    L.spexis_linear.restype = ctypes.c_int
+    L.spexis_linear_workspace_size.argtypes = [i32, i32, i32]
+    L.spexis_linear_workspace_size.restype = sz
     L.spexis_lookahead_memory.argtypes = [i32, P, P, P, i32, ctypes.c_double, i32, P, P, P, P, P]
     L.spexis_lookahead_memory.restype = ctypes.c_int
     _lib = L
@@ -215,3 +223,35 @@ def spexis_lookahead_memory(cur_len, remaining, precision, pp, theta, mem, e_gen
         n, _ptr(cur_len, torch.int64) if n else None, _ptr(remaining, torch.int32) if n else None,
         _ptr(precision, torch.float64) if n else None, pp, ctypes.c_double(theta), mem.shape[0],
         _ptr(mem, torch.float64), opt(e_gen), opt(e_nfin), opt(e_lfin), _stream(stream)))
+
+
+def spexis_linear_workspace_size(rows: int, out_features: int, in_features: int) -> int:
+    return int(lib().spexis_linear_workspace_size(rows, out_features, in_features))
+
+
+def spexis_linear(x, weight, y, residual=None, workspace=None, stream=None) -> None:
+    """y = bf16(x weight^T (+ residual)) for bf16 x [rows, in], weight [out, in]."""
+    rows, n_in = x.shape
+    n_out = weight.shape[0]
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().spexis_linear(_ptr(x, torch.bfloat16), _ptr(weight, torch.bfloat16),
+                               _ptr(residual, torch.bfloat16) if residual is not None else None, rows, n_out, n_in,
+                               _ptr(y, torch.bfloat16), _ptr(workspace) if workspace is not None else None, ws_bytes,
+                               _stream(stream)))
+
+
+def spexis_sample_workspace_size(rows: int, vocab: int) -> int:
+    return int(lib().spexis_sample_workspace_size(rows, vocab))
+
+
+def spexis_sample_tokens(kind, inputs, u, tokens, row_status, workspace, token_prob=None, stats=None,
+                         temperature=1.0, stream=None) -> None:
+    """One token per row of `inputs` [rows, V] (logits or probabilities), with its probability."""
+    rows, V = inputs.shape
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().spexis_sample_tokens(
+        kind, rows, V, ctypes.c_float(temperature), _ptr(inputs, torch.float32),
+        _ptr(stats, torch.float32) if stats is not None else None, stats.shape[1] if stats is not None else 0,
+        _ptr(u, torch.float32), _ptr(tokens, torch.int32),
+        _ptr(token_prob, torch.float32) if token_prob is not None else None, _ptr(row_status, torch.int32),
+        _ptr(workspace), ws_bytes, _stream(stream)))

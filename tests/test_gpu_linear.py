@@ -1,0 +1,89 @@
+"""GPU parity of the adapter's linear layer (spexis_linear) against the oracle.
+
+The oracle computes y = x W^T (+ R) in fp64 from the same bf16 bits; the GPU accumulates in
+fp32 (in its own order) and rounds once to bf16.  Bar per element:
+    |gpu - oracle| <= 2^-8 |oracle| + 4 K 2^-24 sum_j |x_j W_j| + 1e-30
+(one bf16 rounding of a value that carries the worst-case error of an fp32 sum of K exact
+products, with room for the summation order).
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_34370_amd import spexis as sx
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def bf16_pair(shape, seed, scale):
+    g = torch.Generator().manual_seed(seed)
+    t = (torch.randn(shape, generator=g) * scale).to(torch.bfloat16)
+    return t, t.view(torch.int16).numpy().view(np.uint16)
+
+
+def run(x, w, res=None, alias=False):
+    rows, n_out = x.shape[0], w.shape[0]
+    y = res.clone().cuda() if alias else torch.empty((rows, n_out), dtype=torch.bfloat16, device="cuda")
+    ws_n = sx.spexis_linear_workspace_size(rows, n_out, x.shape[1])
+    ws = torch.empty(max(ws_n, 1), dtype=torch.uint8, device="cuda")
+    sx.spexis_linear(x.cuda(), w.cuda(), y, residual=(y if alias else res.cuda()) if res is not None else None,
+                     workspace=ws)
+    torch.cuda.synchronize()
+    return y.float().cpu().double().numpy(), ws_n
+
+
+def check(rows, n_out, n_in, with_res, seed, sample=None, alias=False):
+    x, xb = bf16_pair((rows, n_in), seed, 1.0)
+    w, wb = bf16_pair((n_out, n_in), seed + 1, 0.03)
+    r, rb = bf16_pair((rows, n_out), seed + 2, 1.0) if with_res else (None, None)
+    got, ws_n = run(x, w, r, alias)
+    sel = np.arange(rows) if sample is None else np.asarray(sample)
+    ref = oracle.linear(xb[sel], wb, rb[sel] if with_res else None)
+    mag = np.abs(x.double().numpy()[sel]) @ np.abs(w.double().numpy()).T
+    bound = 2.0 ** -8 * np.abs(ref) + 4 * n_in * 2.0 ** -24 * mag + 1e-30
+    err = np.abs(got[sel] - ref)
+    say(f"[linear] {rows}x{n_in} @ {n_out}x{n_in} res={with_res}: workspace {ws_n} B, max err/bound "
+        f"{(err / bound).max():.3f}")
+    assert (err <= bound).all()
+
+
+@pytest.mark.parametrize("rows,n_out,n_in,res", [(1, 64, 256, False), (37, 100, 512, True), (64, 4096, 1024, True),
+                                                 (200, 1000, 768, False), (129, 333, 2048, True),
+                                                 (33, 31, 4096, False)])
+def test_linear_matches_oracle(rows, n_out, n_in, res):
+    check(rows, n_out, n_in, res, rows + n_out)
+
+
+def test_linear_adapter_shapes_sampled_rows():
+    # the adapter at the llama3-8b-layer workload: 64 exit states, hidden 4096; q/k/v 6144 wide
+    check(64, 4096, 4096, True, 11, sample=[0, 17, 63])
+    check(64, 6144, 4096, False, 12, sample=[5, 40])
+    check(512, 4096, 4096, True, 13, sample=[0, 255, 511])
+
+
+def test_linear_output_may_alias_residual():
+    check(48, 256, 512, True, 14, alias=True)
+    check(64, 4096, 1024, True, 15, alias=True)   # K split: the reduce pass reads the residual
+
+
+def test_linear_rejects_bad_arguments():
+    x = torch.zeros((4, 100), dtype=torch.bfloat16, device="cuda")
+    w = torch.zeros((8, 100), dtype=torch.bfloat16, device="cuda")
+    y = torch.empty((4, 8), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(sx.SpexisError) as e:
+        sx.spexis_linear(x, w, y)
+    assert e.value.code == sx.SPEXIS_ERR_UNSUPPORTED
+    x = torch.zeros((64, 1024), dtype=torch.bfloat16, device="cuda")
+    w = torch.zeros((4096, 1024), dtype=torch.bfloat16, device="cuda")
+    y = torch.empty((64, 4096), dtype=torch.bfloat16, device="cuda")
+    assert sx.spexis_linear_workspace_size(64, 4096, 1024) > 0
+    with pytest.raises(sx.SpexisError) as e:
+        sx.spexis_linear(x, w, y)
+    assert e.value.code == sx.SPEXIS_ERR_WORKSPACE_TOO_SMALL

@@ -1,0 +1,125 @@
+"""GPU parity of plain sampling (spexis_sample_tokens), the draft draw of the drafting step.
+
+Probability input: tokens, probabilities and statuses bit-exact against the oracle on the same
+fp32 rows (both take the exact fixed-point inverse CDF).  Logit input: the GPU's probabilities
+come from its own exp2 (within 1e-5 of the oracle's fp64 softmax), so a token may differ only
+where the uniform lies within 1e-4 of a boundary of the oracle's CDF (at most 1% of rows), and
+the returned probability is within 1e-5 relative of the oracle's probability of that token.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_34370_amd import spexis as sx
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def gpu_sample(kind, rows_t, u, stats=None, T=1.0):
+    R, V = rows_t.shape
+    tok = torch.empty(R, dtype=torch.int32, device="cuda")
+    prob = torch.empty(R, dtype=torch.float32, device="cuda")
+    st = torch.empty(R, dtype=torch.int32, device="cuda")
+    ws = torch.empty(sx.spexis_sample_workspace_size(R, V), dtype=torch.uint8, device="cuda")
+    sx.spexis_sample_tokens(kind, rows_t, torch.as_tensor(u, device="cuda"), tok, st, ws, token_prob=prob,
+                            stats=stats, temperature=T)
+    torch.cuda.synchronize()
+    return tok.cpu().numpy(), prob.cpu().numpy(), st.cpu().numpy()
+
+
+def near_boundary(p_row, u, tol=1e-4):
+    cdf = np.cumsum(p_row.astype(np.float64))
+    cdf /= cdf[-1]
+    return np.abs(cdf - float(u)).min() <= tol
+
+
+def check_logits(logits, u, T, tok, prob, st):
+    p = oracle.softmax(logits, T)
+    rt, rp, rs = oracle.sample(p, u)
+    assert (st == rs).all()
+    diff = np.flatnonzero(tok != rt)
+    assert len(diff) <= max(1, len(tok) // 100), diff
+    for r in diff:
+        assert near_boundary(p[r], u[r]), (r, tok[r], rt[r])
+    ok = tok >= 0
+    np.testing.assert_allclose(prob[ok], p[np.flatnonzero(ok), tok[ok]], rtol=1e-5, atol=1e-12)
+    return len(diff)
+
+
+@pytest.mark.parametrize("R,V", [(1, 1), (7, 5), (64, 1000), (300, 4099), (16, 128256)])
+def test_sample_probabilities_bit_exact(R, V):
+    rng = np.random.default_rng(R * 7 + V)
+    logits = (rng.standard_normal((R, V)) * 3).astype(np.float32)
+    p = oracle.softmax(logits, 1.0)
+    u = rng.random(R, dtype=np.float32)
+    tok, prob, st = gpu_sample(sx.SPEXIS_INPUT_PROBS, torch.as_tensor(p, device="cuda"), u)
+    rt, rp, rs = oracle.sample(p, u)
+    np.testing.assert_array_equal(tok, rt)
+    np.testing.assert_array_equal(prob, rp)
+    np.testing.assert_array_equal(st, rs)
+
+
+def test_sample_probability_edge_rows():
+    V = 300
+    rows = np.full((5, V), 1.0 / V, np.float32)
+    rows[1] = 0
+    rows[1, 123] = 1.0                         # one-hot
+    rows[2, 7] = np.nan                        # refused
+    rows[3] = 0                                # empty
+    u = np.array([0.0, 0.999, 0.5, 0.5, np.nextafter(np.float32(1), np.float32(0))], np.float32)
+    tok, prob, st = gpu_sample(sx.SPEXIS_INPUT_PROBS, torch.as_tensor(rows, device="cuda"), u)
+    rt, rp, rs = oracle.sample(rows, u)
+    np.testing.assert_array_equal(tok, rt)
+    np.testing.assert_array_equal(prob, rp)
+    np.testing.assert_array_equal(st, rs)
+    assert tok[1] == 123 and tok[0] == 0 and tok[4] == V - 1
+
+
+@pytest.mark.parametrize("R,V,T", [(50, 1000, 1.0), (256, 32000, 0.7), (8, 152064, 1.3)])
+def test_sample_logits_agrees_with_oracle(R, V, T):
+    rng = np.random.default_rng(R + V)
+    logits = (rng.standard_normal((R, V)) * 4).astype(np.float32)
+    u = rng.random(R, dtype=np.float32)
+    tok, prob, st = gpu_sample(sx.SPEXIS_INPUT_LOGITS, torch.as_tensor(logits, device="cuda"), u, T=T)
+    n = check_logits(logits, u, T, tok, prob, st)
+    say(f"[sample] logits R={R} V={V} T={T}: {n} tokens within 1e-4 of a boundary differ")
+
+
+def test_sample_from_lm_head_statistics():
+    # draft rows straight from the LM head with its fused statistics (no pass over the rows)
+    rows, V, d, T = 64, 20000, 512, 0.8
+    g = torch.Generator().manual_seed(3)
+    h = (torch.randn((rows, d), generator=g)).to(torch.bfloat16)
+    w = (torch.randn((V, d), generator=g) * 0.08).to(torch.bfloat16)
+    tiles = sx.spexis_lm_head_tiles(V)
+    logits = torch.empty((rows, V), dtype=torch.float32, device="cuda")
+    stats = torch.empty((rows, tiles, 2), dtype=torch.float32, device="cuda")
+    sx.spexis_lm_head(h.cuda(), w.cuda(), stats, logits=logits, temperature=T)
+    u = np.random.default_rng(4).random(rows, dtype=np.float32)
+    tok, prob, st = gpu_sample(sx.SPEXIS_INPUT_LOGITS, logits, u, stats=stats, T=T)
+    tok2, prob2, st2 = gpu_sample(sx.SPEXIS_INPUT_LOGITS, logits, u, T=T)
+    n = check_logits(logits.cpu().numpy(), u, T, tok, prob, st)
+    say(f"[sample] from LM-head statistics: {n} boundary differences; "
+        f"{int((tok != tok2).sum())} differ from the own-statistics path")
+    assert (tok != tok2).sum() <= 1
+
+
+def test_sample_rejects_bad_arguments():
+    x = torch.ones((4, 10), device="cuda")
+    u = torch.full((4,), 0.5, device="cuda")
+    t = torch.empty(4, dtype=torch.int32, device="cuda")
+    s = torch.empty(4, dtype=torch.int32, device="cuda")
+    with pytest.raises(sx.SpexisError) as e:
+        sx.spexis_sample_tokens(sx.SPEXIS_INPUT_PROBS, x, u, t, s, torch.empty(8, dtype=torch.uint8, device="cuda"))
+    assert e.value.code == sx.SPEXIS_ERR_WORKSPACE_TOO_SMALL
+    ws = torch.empty(sx.spexis_sample_workspace_size(4, 10), dtype=torch.uint8, device="cuda")
+    with pytest.raises(sx.SpexisError) as e:
+        sx.spexis_sample_tokens(sx.SPEXIS_INPUT_PROBS, x, u, t, s, ws, stats=torch.zeros((4, 1, 2), device="cuda"))
+    assert e.value.code == sx.SPEXIS_ERR_INVALID_ARGUMENT
