@@ -97,11 +97,12 @@ def main():
     ap.add_argument("--ingest-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic.json from two rocprofv3 --pmc counter_collection.csv files "
                          "(FETCH_SIZE, WRITE_SIZE) of runs with --copy-probe N (pass the same N); needs no GPU")
-    ap.add_argument("--component", choices=["step", "lm_head", "select", "lookahead"], default="step",
+    ap.add_argument("--component", choices=["step", "lm_head", "select", "lookahead", "draft"], default="step",
                     help="lm_head: time spexis_lm_head and acceptance from its fused statistics at the "
                          "workload's shape instead of the verification step; select: time selective "
                          "speculation and measure the acceptance rate of the kept drafts; lookahead: time "
-                         "Algorithm 1's memory estimate (each prints its own JSON line)")
+                         "Algorithm 1's memory estimate; draft: time one drafting step (each prints its own "
+                         "JSON line)")
     ap.add_argument("--alpha", type=float, nargs="+", default=[0.15, 0.3])
     args = ap.parse_args()
     if args.component == "lm_head":
@@ -110,6 +111,8 @@ def main():
         return bench_select(args)
     if args.component == "lookahead":
         return bench_lookahead(args)
+    if args.component == "draft":
+        return bench_draft(args)
     if args.ingest_traffic:
         if args.copy_probe <= 0:
             raise SystemExit("--ingest-traffic needs --copy-probe N: the copy size the counter runs used")
@@ -225,7 +228,6 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-HIDDEN = {1: 512, 2: 4096, 3: 4096, 4: 4096, 5: 3584}   # hidden size of the model behind each workload
 MFMA_BF16_TFLOPS = 2500.0
 
 
@@ -243,7 +245,7 @@ def bench_lm_head(args):
     batch = wl.make_batch(spec, seed=args.seed)
     attn = wl.make_attention_inputs(spec, batch, device="cuda", seed=args.seed)
     acc = wl.make_accept_inputs(spec, batch, device="cuda", seed=args.seed)
-    d, V, T = HIDDEN[spec.wid], spec.vocab, batch.T
+    d, V, T = wl.HIDDEN[spec.wid], spec.vocab, batch.T
     g = torch.Generator(device="cuda").manual_seed(260934370)
     h = torch.randn((T, d), generator=g, device="cuda").to(torch.bfloat16)
     w = (torch.randn((V, d), generator=g, device="cuda") * 0.02).to(torch.bfloat16)
@@ -265,8 +267,9 @@ def bench_lm_head(args):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / steps   # us
 
+    w = sx.spexis_pack_weight(w)   # once per weight, outside the timed region
     us_lm = timed(lambda: sx.spexis_lm_head(h, w, stats, logits=logits, temperature=temp), args.steps, args.warmup)
-    us_lm_stats = timed(lambda: sx.spexis_lm_head(h, w, stats, temperature=temp), args.steps, args.warmup)
+    us_lm_stats = timed(lambda: sx.spexis_lm_head(h, w, stats, temperature=temp, vocab=V), args.steps, args.warmup)
     # Acceptance on logits this LM head produced: target rows from h, draft rows from h plus
     # noise (a draft model sharing the head), drafts drawn from the draft rows (input generation,
     # untimed).  Timed: acceptance computing its own statistics, and from the fused ones.
@@ -409,6 +412,67 @@ def bench_lookahead(args):
         log(f"[lookahead] {n} requests: {us:.1f} us per call; estimate {m[0]:.0f} -> {m[63]:.0f} tokens")
     print(json.dumps({"component": "spexis_lookahead_memory", "workload": spec.name, "iters": 64, "pp": 4,
                       "theta": 0.7, "runs": rows, "data": "synthetic"}), flush=True)
+
+
+def bench_draft(args):
+    """One drafting step at the workload's batch (one draft token per sequence): adapter linear
+    and q/k/v projections, append and attention over the adapter's paged cache (contexts of the
+    workload), output projection with residual, LM head with fused statistics, draft draw.
+    Synthetic bf16 weights; inputs resident in HBM.  Per phase: HIP events on the stream."""
+    import torch
+
+    from paper_2609_34370_amd import workloads as wl
+    from paper_2609_34370_amd.draft import DraftStep
+
+    spec = wl.WORKLOADS[args.workload]
+    base = wl.make_batch(spec, seed=args.seed)
+    batch = wl.make_batch(spec, seed=args.seed, ctx_lens=base.ctx_lens, k=np.zeros(base.B, np.int32))
+    cache = wl.make_attention_inputs(spec, batch, device="cuda", seed=args.seed)
+    ad = wl.make_adapter_inputs(spec, batch, device="cuda", seed=args.seed)
+    step = DraftStep(batch, cache, ad)
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        step.run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step.run()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    phases = (("adapter_in", step.adapter_in), ("attention", step.attention), ("adapter_out", step.adapter_out),
+              ("lm_head", step.lm_head), ("sample", step.sample))
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(phases) + 1)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        for j, (_, fn) in enumerate(phases):
+            fn()
+            ev[i][j + 1].record(stream)
+    torch.cuda.synchronize()
+    us = {name: float(np.mean([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(args.steps)])) * 1e3
+          for j, (name, _) in enumerate(phases)}
+    B, d, V = batch.B, ad.h.shape[1], spec.vocab
+    hq, hkv, D = spec.num_q_heads, spec.num_kv_heads, spec.head_dim
+    w_bytes = {"adapter_in": (d * d + (hq + 2 * hkv) * D * d) * 2, "adapter_out": d * hq * D * 2,
+               "lm_head": V * d * 2 + B * V * 4}
+    kv_bytes = int(batch.seq_lens.astype(np.int64).sum()) * hkv * D * 2 * 2
+    total = sum(w_bytes.values()) + kv_bytes
+    lm_gbs = w_bytes["lm_head"] / (us["lm_head"] * 1e-6) / 1e9
+    at_gbs = kv_bytes / (us["attention"] * 1e-6) / 1e9
+    tok = step.tokens.cpu().numpy()
+    conf = step.conf.cpu().numpy()
+    log(f"[draft] {spec.name}: step {ms * 1e3:.1f} us; " + ", ".join(f"{k} {v:.1f} us" for k, v in us.items()))
+    log(f"[draft] LM head {w_bytes['lm_head'] / 1e9:.3f} GB -> {lm_gbs:.0f} GB/s ({lm_gbs / HBM_PEAK_GBS:.1%}); "
+        f"attention {kv_bytes / 1e9:.3f} GB -> {at_gbs:.0f} GB/s; whole step {total / 1e9:.3f} GB -> "
+        f"{total / (ms * 1e-3) / 1e9:.0f} GB/s; confidence median {np.median(conf):.2e}")
+    print(json.dumps({"component": "draft_step", "workload": spec.name, "batch": B, "hidden": d, "vocab": V,
+                      "us_per_step": round(ms * 1e3, 2), "phases_us": {k: round(v, 2) for k, v in us.items()},
+                      "draft_tokens_per_s": round(B / (ms * 1e-3), 1),
+                      "lm_head": {"bytes": w_bytes["lm_head"], "achieved": round(lm_gbs, 1), "peak": HBM_PEAK_GBS,
+                                  "unit": "GB/s", "frac": round(lm_gbs / HBM_PEAK_GBS, 4)},
+                      "attention": {"bytes": kv_bytes, "achieved": round(at_gbs, 1), "unit": "GB/s"},
+                      "bytes_per_step": total, "valid_tokens": int((tok >= 0).sum()), "data": "synthetic"}),
+          flush=True)
 
 
 ATTN_KERNELS = ("verify_attn_kernel", "attn_merge_kernel")   # the launches of spexis_verify_attention

@@ -16,6 +16,7 @@
  *   spexis_select_drafts     selective speculation: drop the least confident drafts first
  *   spexis_lookahead_memory  look-ahead KV-memory estimate of the running requests (Algorithm 1)
  *   spexis_linear            a linear layer of the drafting adapter (bf16, fp32 accumulation)
+ *   spexis_pack_weight       weight layout of the two projections above (done once per weight)
  *   spexis_sample_tokens     one token per row of logits or probabilities, with its probability
  *   spexis_softmax_rows      temperature softmax of logit rows (probability inputs)
  *
@@ -219,7 +220,8 @@ int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k,
  *   stats[m][t] = (max x*c, sum 2^(x*c - max)) over columns v of tile t = v / 128, v < vocab,
  *                 x = logits[m][v], c = log2(e) / temperature
  *
- *   hidden   [rows][hidden_dim] bf16 (read);  weight [vocab][hidden_dim] bf16 (read)
+ *   hidden   [rows][hidden_dim] bf16 (read);  weight [vocab][hidden_dim] bf16 packed by
+ *            spexis_pack_weight (read)
  *   logits   [rows][vocab] fp32 (written), or NULL to write only the statistics
  *   stats    [rows][spexis_lm_head_tiles(vocab)][2] fp32 (written)
  * Supported: hidden_dim a multiple of 256.  Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP.
@@ -277,12 +279,28 @@ int spexis_select_drafts(int32_t num_seqs, int32_t total_tokens, const int32_t* 
                          int32_t* kept_query_start_loc, int32_t* keep, void* stream);
 
 /*
+ * spexis_pack_weight -- lays out a bf16 weight W [rows][cols] (row-major) for spexis_lm_head and
+ * spexis_linear, once per weight: tiles of 32 rows x 64 columns, 4 KB each, in (row tile, column
+ * tile) order; inside a tile the element (r, 64c + 32h + 8s + e) sits at ((s*2 + h)*32 + r)*8 + e,
+ * the operand order of the matrix-core instruction, so that the projections read W as
+ * contiguous 1 KB runs.  Rows past `rows` are zero.
+ *   weight  [rows][cols] bf16, device;  packed: spexis_packed_weight_size(rows, cols) bytes,
+ *           device, written; may not alias weight
+ * Supported: cols % 64 == 0.  Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP.
+ */
+int spexis_pack_weight(const void* weight, int32_t rows, int32_t cols, void* packed, void* stream);
+
+/* Bytes of a packed weight: ceil(rows / 32) * 32 * cols * 2 (0 for unsupported sizes). */
+size_t spexis_packed_weight_size(int32_t rows, int32_t cols);
+
+/*
  * spexis_linear -- a linear layer of the drafting adapter (Implementation: the adapter is a
  * linear layer and an attention layer followed by the LM head), also its attention layer's
  * input and output projections:
  *   y[r][o] = bf16( sum_j x[r][j] * W[o][j]  (+ residual[r][o]) )
  * with fp32 accumulation (the order over j is the library's) and one round to nearest even.
- *   x         [rows][in_features] bf16;  weight [out_features][in_features] bf16 (row-major)
+ *   x         [rows][in_features] bf16;  weight: [out_features][in_features] bf16 packed by
+ *             spexis_pack_weight
  *   residual  [rows][out_features] bf16 or NULL;  y: [rows][out_features] bf16 output (may not
  *             alias x or weight; may alias residual)
  *   workspace >= spexis_linear_workspace_size(rows, out_features, in_features) bytes (0 when

@@ -196,6 +196,31 @@ def sample(probs: np.ndarray, u):
     return tok, prob, status
 
 
+def draft_step(h, w_in, w_q, w_k, w_v, w_o, w_lm, k_pool, v_pool, num_blocks, num_kv_heads, num_q_heads,
+               block_size, head_dim, seq_lens, block_tables, temperature, u):
+    """The drafting adapter's forward and the draft draw for one query token per sequence, in
+    the adapter's order (a linear layer, an attention layer, the LM head), every intermediate
+    rounded to bf16 as the tensors that hold it; the pools are updated in place.  All weights
+    and states are bf16 bit arrays.  Returns a dict of the intermediates and (tokens, conf,
+    status)."""
+    B = len(seq_lens)
+    qsl = np.arange(B + 1, dtype=np.int32)
+    x = to_bf16(linear(h, w_in))
+    q = to_bf16(linear(x, w_q))
+    k = to_bf16(linear(x, w_k))
+    v = to_bf16(linear(x, w_v))
+    append_kv(k_pool, v_pool, num_blocks, num_kv_heads, block_size, head_dim, qsl, seq_lens, block_tables,
+              k.reshape(B, num_kv_heads, head_dim), v.reshape(B, num_kv_heads, head_dim))
+    o = attention(k_pool, v_pool, num_blocks, num_kv_heads, block_size, head_dim, qsl, seq_lens, block_tables,
+                  q.reshape(B, num_q_heads, head_dim), num_q_heads, 1.0 / np.sqrt(head_dim))
+    o = to_bf16(o.reshape(B, num_q_heads * head_dim))
+    y = to_bf16(linear(o, w_o, x))
+    logits, _, _ = lm_head(y, w_lm, temperature)
+    p = softmax(logits.astype(np.float32), temperature)
+    tok, conf, status = sample(p, u)
+    return dict(x=x, q=q, k=k, v=v, o=o, y=y, logits=logits, probs=p, tokens=tok, conf=conf, status=status)
+
+
 def lookahead(cur_len, remaining, precision, pp: int, theta: float, iters: int = 64):
     """Algorithm 1: (mem, e_gen, e_nfin, e_lfin), each fp64 [iters], for the running requests'
     current lengths, predicted remaining lengths and prediction precisions."""

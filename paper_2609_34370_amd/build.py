@@ -12,7 +12,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libspexis.so")
-SOURCES = ["append.hip", "attention.hip", "accept.hip", "lm_head.hip", "select.hip", "lookahead.hip", "linear.hip", "api.hip"]
+SOURCES = ["append.hip", "attention.hip", "accept.hip", "lm_head.hip", "select.hip", "lookahead.hip", "linear.hip", "pack.hip", "api.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -375,6 +375,21 @@ int spexis_select_drafts(int32_t num_seqs, int32_t total_tokens, const int32_t* 
   return hip_result(spexis::launch_select(p, (hipStream_t)stream), "spexis_select_drafts");
 }
 
+size_t spexis_packed_weight_size(int32_t rows, int32_t cols) {
+  if (rows <= 0 || cols <= 0 || cols % 64 != 0) return 0;
+  return (size_t)((rows + 31) / 32) * 32 * (size_t)cols * 2;
+}
+
+int spexis_pack_weight(const void* weight, int32_t rows, int32_t cols, void* packed, void* stream) {
+  if (!weight || !packed) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_pack_weight: null pointer");
+  if (rows <= 0 || cols <= 0) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_pack_weight: bad size");
+  if (cols % 64 != 0)
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_pack_weight: cols %d is not a multiple of 64", cols);
+  if ((int64_t)((rows + 31) / 32) * (cols / 64) * 256 >= (1ll << 40))
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_pack_weight: too large");
+  return hip_result(spexis::launch_pack_weight(weight, rows, cols, packed, (hipStream_t)stream), "spexis_pack_weight");
+}
+
 size_t spexis_linear_workspace_size(int32_t rows, int32_t out_features, int32_t in_features) {
   if (rows <= 0 || out_features <= 0 || in_features <= 0 || in_features % 256 != 0) return 0;
   spexis::LinearParams p{};

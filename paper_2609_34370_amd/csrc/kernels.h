@@ -47,7 +47,7 @@ __host__ __device__ inline int64_t attn_ws_bytes(int nwaves, int rmax, int D) {
 }
 
 // LM-head projection logits = h W^T with the row statistics of its 128-column tiles.
-struct LmParams {
+struct LmParams {  // w: packed (launch_pack_weight)
   const void* h;         // [M][d] bf16
   const void* w;         // [V][d] bf16
   float* logits;         // [M][V] fp32 (null: not written)
@@ -74,7 +74,7 @@ constexpr int kSelectMaxDrafts = 16384;
 
 struct LinearParams {
   const void* x;     // bf16 [M][K]
-  const void* w;     // bf16 [N][K]
+  const void* w;     // bf16 [N][K], packed (launch_pack_weight)
   const void* res;   // bf16 [M][N] or null
   void* y;           // bf16 [M][N]
   float* part;       // fp32 [S][M][N] when S > 1
@@ -142,6 +142,9 @@ hipError_t launch_lm_head(const LmParams& p, hipStream_t s);
 hipError_t launch_select(const SelectParams& p, hipStream_t s);
 hipError_t launch_lookahead(const LookaheadParams& p, hipStream_t s);
 void linear_plan(int M, int N, int K, LinearParams& p);
+hipError_t launch_pack_weight(const void* w, int N, int K, void* out, hipStream_t s);
+// packed weight tile (32 rows x 64 K values, 2048 elements) holding rows 32n.., K values 64c..
+constexpr int kPackTile = 2048;
 hipError_t launch_linear(const LinearParams& p, hipStream_t s);
 hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V, float c, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s);

@@ -12,8 +12,8 @@
 //     kernel adds the partials in order, adds the residual and rounds to bf16;
 //   * both MFMA operands (v_mfma_f32_32x32x16_bf16) are loaded straight into registers, 64 K
 //     values per chunk: lane half h takes K = 32h + 8s .. +7 at MFMA step s for its row of x and
-//     its column of W alike (the contraction order is free when both sides use it), so each lane
-//     reads 64 contiguous bytes per row per chunk;
+//     its column of W alike (the contraction order is free when both sides use it).  W is
+//     packed (pack.hip), so a wave's operand load reads 1 KB of contiguous memory;
 //   * workgroups of one (column tile, K split) and consecutive row groups go to one XCD in turn,
 //     so a W tile read for one row group is an L2 hit for the next.
 #include "common.h"
@@ -49,7 +49,11 @@ __global__ __launch_bounds__(kThreads) void linear_kernel(LinearParams p) {
   const int kbase = split * (p.K / p.S) + wave * p.kw + 32 * half;
   const int nch = p.kw / kCh;
 
-  const uint16_t* wp = reinterpret_cast<const uint16_t*>(p.w) + (int64_t)min(n0 + col, p.N - 1) * p.K + kbase;
+  // W is packed (pack.hip): the wave's columns are tile row `tile`, its K range starts at chunk
+  // kbase / 64, and lane l reads 16 contiguous bytes at s * 512 + 8 l of each 4 KB tile
+  const int kchunks = p.K / kCh;
+  const uint16_t* wp = reinterpret_cast<const uint16_t*>(p.w) +
+                       ((int64_t)tile * kchunks + (split * (p.K / p.S) + wave * p.kw) / kCh) * kPackTile + 8 * lane;
   const uint16_t* xp[NRT];
 #pragma unroll
   for (int t = 0; t < NRT; ++t)
@@ -57,9 +61,10 @@ __global__ __launch_bounds__(kThreads) void linear_kernel(LinearParams p) {
 
   u32x4 wb[DEPTH][4], xa[DEPTH][NRT][4];
   auto load = [&](int d, int j) {   // chunk j into buffer d (past the end: the last chunk again)
-    const int off = min(j, nch - 1) * kCh;
+    const int jc = min(j, nch - 1);
+    const int off = jc * kCh;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) wb[d][s] = *reinterpret_cast<const u32x4*>(wp + off + 8 * s);
+    for (int s = 0; s < 4; ++s) wb[d][s] = *reinterpret_cast<const u32x4*>(wp + (int64_t)jc * kPackTile + 512 * s);
 #pragma unroll
     for (int t = 0; t < NRT; ++t)
 #pragma unroll

@@ -10,12 +10,15 @@
 // rows of h).  Each of its four waves owns 32 columns and all the group's rows: ten 32x32
 // accumulator tiles of v_mfma_f32_32x32x16_bf16 (A operand: h rows, B operand: W rows).
 //   * W, the stream that matters (V*d*2 bytes, read once), goes straight from HBM into each
-//     wave's registers, four K-steps of 64 ahead.  A lane owns 32 consecutive K values of its
-//     column per step (64 contiguous bytes): the contraction order over K is free as long as
-//     h uses the same, so lane half h takes K = 32h + 8s .. +7 at MFMA step s.
+//     wave's registers, DEPTH K-steps of 64 ahead.  It is packed (pack.hip) so that each operand
+//     load of a wave reads 1 KB of contiguous memory; lane half h takes K = 32h + 8s .. +7 of
+//     its column at MFMA step s (the contraction order over K is free as long as h uses the
+//     same).
 //   * h is shared by the four waves: it goes through LDS, one step per stage, fetched into
-//     registers two steps ahead.  Wait counts retire in issue order, and with that distance
-//     the wait for h never waits for a W load that is not needed next anyway.
+//     registers NA steps ahead (NA register sets).  Wait counts retire in issue order: the wait
+//     for h step i+1 leaves the NA steps of W loaded after it in flight, and W runs DEPTH >=
+//     NA + 2 steps ahead, so the compute of step i+1 never waits for its W.  Few row tiles leave
+//     registers for NA = 4, DEPTH = 8; the full 320-row group uses NA = 2, DEPTH = 4.
 //   * Workgroups of one vocabulary tile and consecutive row groups are dispatched to the same
 //     XCD one after another, so a W tile read for one row group is an L2 hit for the next.
 #include "common.h"
@@ -26,8 +29,6 @@ namespace spexis {
 namespace {
 
 constexpr int kRT = kLmRows / 32;   // row tiles per workgroup
-constexpr int kWDepth = 4;          // W steps in flight
-constexpr int kAChunks = kLmRows * (kLmK / 8) / 256;   // 16-byte h chunks per thread per step (10)
 
 // W rows are read once: non-temporal loads keep them from evicting h out of L2.
 template <bool kStream>
@@ -38,9 +39,10 @@ __device__ __forceinline__ u32x4 ldw(const uint16_t* p) {
 
 }  // namespace
 
-template <bool kStream, int NRT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1)))
+template <bool kStream, int NRT, int NA, int DEPTH, int WPE>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE)))
 void lm_head_kernel(LmParams p) {
+  static_assert(DEPTH >= NA + 2 && DEPTH % NA == 0 && DEPTH % 2 == 0, "pipeline shape");
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 31, half = lane >> 5;
   const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
   const int mg = local % p.mgroups;
@@ -50,13 +52,21 @@ void lm_head_kernel(LmParams p) {
   const int rows = min(kLmRows, p.M - m0);
   const int v = n0 + 32 * wave + col;
   const int nsteps = p.d / kLmK;
-  const uint16_t* wrow = reinterpret_cast<const uint16_t*>(p.w) + (int64_t)min(v, p.V - 1) * p.d + 32 * half;
+  // this wave's 32 columns are packed tile row (n0 + 32 wave) / 32 (clamped for the columns past V,
+  // whose results are dropped); lane l reads 16 contiguous bytes at s * 512 + 8 l of each tile
+  const int wtile = min(4 * nt + wave, (p.V + 31) / 32 - 1);
+  const uint16_t* wrow = reinterpret_cast<const uint16_t*>(p.w) + (int64_t)wtile * nsteps * kPackTile + 8 * lane;
   const uint16_t* hbase = reinterpret_cast<const uint16_t*>(p.h) + (int64_t)m0 * p.d;
 
   // h in LDS: stage x, row r, 16-byte chunk kc of the step stored at position kc ^ ((r >> 1) & 7),
   // so that the 16 rows one ds_read_b128 pass serves hit 16 distinct 16-byte bank groups
-  __shared__ u32x4 sm_a[2][kLmRows * 8];
-  u32x4 areg[2][kAChunks];   // h chunks of the next two steps, in flight
+  // only the NRT row tiles the group computes are staged: 32 * NRT rows * 8 chunks = NRT chunks
+  // per thread per step
+  constexpr int kAChunks = NRT;
+  // (at least 72 rows: the epilogue transposes 4 x 32 x 36 floats through this space)
+  constexpr int kStage = (32 * NRT > 72 ? 32 * NRT : 72) * 8;
+  __shared__ u32x4 sm_a[2][kStage];
+  u32x4 areg[NA][kAChunks];   // h chunks of the next NA steps, in flight
   auto load_a = [&](u32x4 (&dst)[kAChunks], int j) {
     j = min(j, nsteps - 1);   // past the end: re-read the last step (kept unconditional)
 #pragma unroll
@@ -74,11 +84,11 @@ void lm_head_kernel(LmParams p) {
       sm_a[stage][r * 8 + (kc ^ ((r >> 1) & 7))] = src[u];
     }
   };
-  u32x4 wb[kWDepth][4];
+  u32x4 wb[DEPTH][4];
   auto load_w = [&](u32x4 (&dst)[4], int j) {
-    const uint16_t* src = wrow + (int64_t)min(j, nsteps - 1) * kLmK;
+    const uint16_t* src = wrow + (int64_t)min(j, nsteps - 1) * kPackTile;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) dst[s] = ldw<kStream>(src + 8 * s);
+    for (int s = 0; s < 4; ++s) dst[s] = ldw<kStream>(src + 512 * s);
   };
 
   f32x16 acc[NRT];
@@ -87,13 +97,13 @@ void lm_head_kernel(LmParams p) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[t][e] = 0.f;
 
-  // prologue: h steps 0 and 1, W steps 0..3, stage 0 in LDS
+  // prologue: h step 0 into stage 0, W steps 0 .. DEPTH-1, h steps 1 .. NA into registers
   load_a(areg[0], 0);
-  load_a(areg[1], 1);
 #pragma unroll
-  for (int b = 0; b < kWDepth; ++b) load_w(wb[b], b);
+  for (int b = 0; b < DEPTH; ++b) load_w(wb[b], b);
   store_a(areg[0], 0);
-  load_a(areg[0], 2);
+#pragma unroll
+  for (int a = 1; a <= NA; ++a) load_a(areg[a % NA], a);
   __syncthreads();
 
   // The A fragments of k-step s+1 are read from LDS while the MFMAs of k-step s run.
@@ -118,15 +128,16 @@ void lm_head_kernel(LmParams p) {
     }
   };
 
-  // step j: compute from stage j%2 and W buffer j%4; refill that W buffer with step j+4; move
-  // h step j+1 (fetched two steps ago) into the other stage; fetch h step j+3 into its registers
-  for (int j = 0; j < nsteps; j += kWDepth) {
+  // step i: compute from stage i%2 and W buffer i%DEPTH; move h step i+1 (fetched NA steps ago)
+  // into the other stage and fetch h step i+1+NA into the same registers; refill the W buffer
+  // with step i+DEPTH
+  for (int j = 0; j < nsteps; j += DEPTH) {
 #pragma unroll
-    for (int jj = 0; jj < kWDepth; ++jj) {
-      compute(wb[jj], jj & 1);
-      load_w(wb[jj], j + jj + kWDepth);
-      store_a(areg[(jj + 1) & 1], (jj + 1) & 1);
-      load_a(areg[(jj + 1) & 1], j + jj + 3);
+    for (int jj = 0; jj < DEPTH; ++jj) {
+      if (j + jj < nsteps) compute(wb[jj], jj & 1);
+      store_a(areg[(jj + 1) % NA], (jj + 1) & 1);
+      load_a(areg[(jj + 1) % NA], j + jj + 1 + NA);
+      load_w(wb[jj], j + jj + DEPTH);
       __syncthreads();
     }
   }
@@ -145,7 +156,7 @@ void lm_head_kernel(LmParams p) {
   }
   // Row statistics: each wave transposes one 32x32 tile at a time through its part of the
   // (now free) h stages, then lane r < 32 reduces row r over the wave's 32 columns.
-  __shared__ float sm_m[4][kLmRows], sm_z[4][kLmRows];
+  __shared__ float sm_m[4][32 * NRT], sm_z[4][32 * NRT];
   constexpr int kTS = 36;   // floats per transposed row (16-byte aligned, padded)
   float* tile = reinterpret_cast<float*>(&sm_a[0][0]) + wave * 32 * kTS;
 #pragma unroll
@@ -182,14 +193,14 @@ void lm_head_kernel(LmParams p) {
   }
 }
 
-template <int NRT>
+template <int NRT, int NA, int DEPTH, int WPE>
 static hipError_t launch_lm_nrt(const LmParams& p, hipStream_t s) {
   // grid: tiles of 8 vocabulary tiles (one per XCD) x row groups, row groups innermost
   const int64_t grid = (int64_t)((p.ntiles + 7) / 8) * 8 * p.mgroups;
   if (p.mgroups == 1)
-    hipLaunchKernelGGL((lm_head_kernel<true, NRT>), dim3((unsigned)grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((lm_head_kernel<true, NRT, NA, DEPTH, WPE>), dim3((unsigned)grid), dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL((lm_head_kernel<false, NRT>), dim3((unsigned)grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((lm_head_kernel<false, NRT, NA, DEPTH, WPE>), dim3((unsigned)grid), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
@@ -197,11 +208,12 @@ hipError_t launch_lm_head(const LmParams& p, hipStream_t s) {
   // row tiles computed per workgroup: the smallest instantiated count covering the rows (a
   // group of fewer rows repeats its last row in the padding tiles, whose results are dropped)
   const int need = p.M >= kLmRows ? kRT : (p.M + 31) / 32;
-  if (need <= 1) return launch_lm_nrt<1>(p, s);
-  if (need <= 2) return launch_lm_nrt<2>(p, s);
-  if (need <= 4) return launch_lm_nrt<4>(p, s);
-  if (need <= 6) return launch_lm_nrt<6>(p, s);
-  return launch_lm_nrt<kRT>(p, s);
+  // (few row tiles: two workgroups per CU, so each SIMD has a second wave to cover latency)
+  if (need <= 1) return launch_lm_nrt<1, 4, 8, 2>(p, s);
+  if (need <= 2) return launch_lm_nrt<2, 4, 8, 2>(p, s);
+  if (need <= 4) return launch_lm_nrt<4, 4, 8, 1>(p, s);
+  if (need <= 6) return launch_lm_nrt<6, 2, 4, 1>(p, s);
+  return launch_lm_nrt<kRT, 2, 4, 1>(p, s);
 }
 
 }  // namespace spexis

@@ -81,6 +81,10 @@ def lib():
     L.spexis_sample_tokens.restype = ctypes.c_int
     L.spexis_sample_workspace_size.argtypes = [i32, i32]
     L.spexis_sample_workspace_size.restype = sz
+    L.spexis_pack_weight.argtypes = [P, i32, i32, P, P]
+    L.spexis_pack_weight.restype = ctypes.c_int
+    L.spexis_packed_weight_size.argtypes = [i32, i32]
+    L.spexis_packed_weight_size.restype = sz
     L.spexis_linear.argtypes = [P, P, P, i32, i32, i32, P, P, sz, P]
     L.spexis_linear.restype = ctypes.c_int
     L.spexis_linear_workspace_size.argtypes = [i32, i32, i32]
@@ -177,10 +181,14 @@ def spexis_lm_head_stats_size(rows: int, vocab: int) -> int:
     return int(lib().spexis_lm_head_stats_size(rows, vocab))
 
 
-def spexis_lm_head(hidden, weight, stats, logits=None, temperature=1.0, stream=None) -> None:
+def spexis_lm_head(hidden, weight, stats, logits=None, temperature=1.0, vocab=None, stream=None) -> None:
+    """weight: packed by spexis_pack_weight; vocab defaults to the stats / logits shape."""
     rows, hidden_dim = hidden.shape
-    vocab = weight.shape[0]
-    assert weight.shape[1] == hidden_dim
+    if vocab is None:
+        vocab = logits.shape[1] if logits is not None else None
+    if vocab is None:
+        raise ValueError("vocab is needed when logits is None")
+    assert weight.numel() * 2 == spexis_packed_weight_size(vocab, hidden_dim), "weight must be packed"
     _check(lib().spexis_lm_head(_ptr(hidden, torch.bfloat16), _ptr(weight, torch.bfloat16), rows, vocab, hidden_dim,
                                 ctypes.c_float(temperature), _ptr(logits, torch.float32),
                                 _ptr(stats, torch.float32), _stream(stream)))
@@ -230,9 +238,11 @@ def spexis_linear_workspace_size(rows: int, out_features: int, in_features: int)
 
 
 def spexis_linear(x, weight, y, residual=None, workspace=None, stream=None) -> None:
-    """y = bf16(x weight^T (+ residual)) for bf16 x [rows, in], weight [out, in]."""
+    """y = bf16(x weight^T (+ residual)) for bf16 x [rows, in] and a packed weight [out, in]
+    (spexis_pack_weight); out is y's width."""
     rows, n_in = x.shape
-    n_out = weight.shape[0]
+    n_out = y.shape[1]
+    assert weight.numel() * 2 == spexis_packed_weight_size(n_out, n_in), "weight must be packed"
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check(lib().spexis_linear(_ptr(x, torch.bfloat16), _ptr(weight, torch.bfloat16),
                                _ptr(residual, torch.bfloat16) if residual is not None else None, rows, n_out, n_in,
@@ -255,3 +265,20 @@ def spexis_sample_tokens(kind, inputs, u, tokens, row_status, workspace, token_p
         _ptr(u, torch.float32), _ptr(tokens, torch.int32),
         _ptr(token_prob, torch.float32) if token_prob is not None else None, _ptr(row_status, torch.int32),
         _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def spexis_packed_weight_size(rows: int, cols: int) -> int:
+    return int(lib().spexis_packed_weight_size(rows, cols))
+
+
+def spexis_pack_weight(weight, stream=None) -> torch.Tensor:
+    """The packed layout of a bf16 weight [rows, cols] (a new flat bf16 tensor), for
+    spexis_lm_head and spexis_linear; allocated here, once per weight."""
+    rows, cols = weight.shape
+    n = spexis_packed_weight_size(rows, cols)
+    if n == 0:
+        raise SpexisError(SPEXIS_ERR_UNSUPPORTED, f"cannot pack a [{rows}, {cols}] weight")
+    out = torch.empty(n // 2, dtype=torch.bfloat16, device=weight.device)
+    _check(lib().spexis_pack_weight(_ptr(weight, torch.bfloat16), rows, cols, _ptr(out, torch.bfloat16),
+                                    _stream(stream)))
+    return out

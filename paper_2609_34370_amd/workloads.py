@@ -271,3 +271,46 @@ def subset_batch(batch: Batch, seqs) -> tuple:
     sub = Batch(batch.spec, L.astype(np.int32), kk.astype(np.int32), qsl, batch.seq_lens[seqs].astype(np.int32),
                 batch.block_tables[seqs], batch.num_blocks)
     return sub, trows, drows
+
+
+# hidden size of the model behind each workload (equal to Hq * D for all of them)
+HIDDEN = {1: 512, 2: 4096, 3: 4096, 4: 4096, 5: 3584}
+
+
+@dataclasses.dataclass
+class AdapterInputs:
+    """Synthetic weights and inputs of one drafting step (the adapter: a linear layer, an
+    attention layer with q/k/v and output projections, then the LM head)."""
+    h: torch.Tensor        # [B, d] bf16 exit hidden states
+    w_in: torch.Tensor     # [d, d] bf16
+    w_q: torch.Tensor      # [Hq*D, d]
+    w_k: torch.Tensor      # [Hkv*D, d]
+    w_v: torch.Tensor      # [Hkv*D, d]
+    w_o: torch.Tensor      # [d, Hq*D]
+    w_lm: torch.Tensor     # [V, d]
+    u: torch.Tensor        # [B] fp32 uniforms of the draft draw
+    temperature: float
+
+
+def make_adapter_inputs(spec: WorkloadSpec, batch: Batch, device="cpu", seed: Optional[int] = None) -> AdapterInputs:
+    """N(0, 1) exit states; every weight N(0, 1/fan_in) (activations stay O(1)) except the LM
+    head, N(0, 4/d) (logits of standard deviation about 2)."""
+    seed = BASE_SEED + 100 + spec.wid if seed is None else seed
+    d, hq, hkv, D = HIDDEN[spec.wid], spec.num_q_heads, spec.num_kv_heads, spec.head_dim
+    g = _gen(device, seed)
+
+    def w(rows, cols, std):
+        return (torch.randn((rows, cols), generator=g, device=device) * std).to(torch.bfloat16)
+
+    h = torch.randn((batch.B, d), generator=g, device=device).to(torch.bfloat16)
+    w_in = w(d, d, d ** -0.5)
+    w_q = w(hq * D, d, d ** -0.5)
+    w_k = w(hkv * D, d, d ** -0.5)
+    w_v = w(hkv * D, d, d ** -0.5)
+    w_o = w(d, hq * D, (hq * D) ** -0.5)
+    w_lm = torch.empty((spec.vocab, d), dtype=torch.bfloat16, device=device)
+    for r in range(0, spec.vocab, 16384):   # in chunks: the fp32 draw of the whole head is large
+        e = min(spec.vocab, r + 16384)
+        w_lm[r:e] = (torch.randn((e - r, d), generator=g, device=device) * (2.0 / d ** 0.5)).to(torch.bfloat16)
+    u = torch.rand(batch.B, generator=g, device=device)
+    return AdapterInputs(h, w_in, w_q, w_k, w_v, w_o, w_lm, u, spec.temperature)

@@ -1,0 +1,86 @@
+"""The drafting step on the GPU (DraftStep: adapter linear, q/k/v, append, attention, output
+projection with residual, LM head, draw) against the oracle's adapter forward.
+
+Each call of the chain has its own parity test against the oracle; this test checks that the
+chain is wired as the adapter is defined.  Both sides round every intermediate to bf16, but from
+sums in different orders, so an intermediate can differ by one bf16 step and the differences
+travel down the chain.  Criteria: the first projection within one bf16 step of the oracle's; the
+final logits within 2% of their RMS for 99.9% of entries (a wiring mistake -- a wrong weight,
+a missing residual, a transposed head -- moves them by O(1) of it).  The draft token must be a
+draw of the oracle's inverse CDF at the same uniform, up to the distance between the two
+distributions: with p_o the oracle's probabilities and p_g the softmax of the GPU's logits, an
+inverse-CDF draw at u from p_g lands on a token whose oracle CDF interval comes within
+eps = sum_v |p_g - p_o| of u.  (At a large vocabulary every token carries ~1e-5 of the mass, so
+differences of a fraction of a percent in the logits move a draw to a neighbouring token; the
+criterion allows exactly that much.)  The confidence is within 1e-5 of p_g at the token.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_34370_amd import workloads as wl
+from paper_2609_34370_amd.draft import DraftStep
+from paper_2609_34370_amd.step import bf16_to_u16
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.mark.parametrize("wid,B", [(1, 64), (2, 16)])
+def test_draft_step_matches_oracle(wid, B):
+    spec = wl.spec_with(wid, batch=B)
+    base = wl.make_batch(spec)
+    batch = wl.make_batch(spec, ctx_lens=base.ctx_lens, k=np.zeros(B, np.int32))
+    cache = wl.make_attention_inputs(spec, batch, device="cuda")
+    kp, vp = bf16_to_u16(cache.k_pool).copy(), bf16_to_u16(cache.v_pool).copy()
+    ad = wl.make_adapter_inputs(spec, batch, device="cuda")
+    say(f"[draft] workload {wid} B={B} d={ad.h.shape[1]} V={spec.vocab}")
+    step = DraftStep(batch, cache, ad)
+    step.run()
+    torch.cuda.synchronize()
+    u16 = bf16_to_u16
+    ref = oracle.draft_step(u16(ad.h), u16(ad.w_in), u16(ad.w_q), u16(ad.w_k), u16(ad.w_v), u16(ad.w_o),
+                            u16(ad.w_lm), kp, vp, batch.num_blocks, spec.num_kv_heads, spec.num_q_heads,
+                            spec.block_size, spec.head_dim, batch.seq_lens, batch.block_tables, ad.temperature,
+                            ad.u.cpu().numpy())
+    x = step.x.float().cpu().double().numpy()
+    rx = oracle.bf16_value(ref["x"])
+    assert (np.abs(x - rx) <= 2.0 ** -7 * np.abs(rx) + 1e-30).all()
+    logits = step.logits.cpu().double().numpy()
+    rms = np.sqrt((ref["logits"] ** 2).mean())
+    d = np.abs(logits - ref["logits"])
+    say(f"  logits: RMS {rms:.3f}, max |diff| {d.max():.4f}, 99.9th pct {np.quantile(d, 0.999):.4f}")
+    assert np.quantile(d, 0.999) <= 0.02 * rms
+    tok, conf, st = step.tokens.cpu().numpy(), step.conf.cpu().numpy(), step.status.cpu().numpy()
+    assert (st == 0).all() and (ref["status"] == 0).all()
+    u = ad.u.cpu().numpy().astype(np.float64)
+    T = ad.temperature
+    same = 0
+    for b in range(B):
+        po = ref["probs"][b].astype(np.float64)
+        po /= po.sum()
+        z = logits[b] / T
+        pg = np.exp(z - z.max())
+        pg /= pg.sum()
+        eps = np.abs(pg - po).sum() + 1e-6
+        cdf = np.cumsum(po)
+        t = int(tok[b])
+        lo = cdf[t - 1] if t > 0 else 0.0
+        assert lo - eps <= u[b] <= cdf[t] + eps, (b, t, int(ref["tokens"][b]), eps)
+        assert abs(conf[b] - pg[t]) <= 1e-5 * pg[t] + 1e-12
+        same += t == int(ref["tokens"][b])
+    say(f"  tokens equal to the oracle's for {same}/{B}")
+    # the pools differ from the oracle's (appended in place) only in the step's new rows, by at
+    # most a bf16 step or so (k and v themselves carry the rounding differences of x)
+    for gpu_pool, ref_pool in ((cache.k_pool, kp), (cache.v_pool, vp)):
+        g = bf16_to_u16(gpu_pool)
+        diff = np.flatnonzero(g != ref_pool)
+        assert len(diff) <= B * spec.num_kv_heads * spec.head_dim
+        a, b = oracle.bf16_value(g[diff]), oracle.bf16_value(ref_pool[diff])
+        assert (np.abs(a - b) <= 2.0 ** -6 * np.abs(b) + 1e-3).all()

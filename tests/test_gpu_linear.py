@@ -33,7 +33,7 @@ def run(x, w, res=None, alias=False):
     y = res.clone().cuda() if alias else torch.empty((rows, n_out), dtype=torch.bfloat16, device="cuda")
     ws_n = sx.spexis_linear_workspace_size(rows, n_out, x.shape[1])
     ws = torch.empty(max(ws_n, 1), dtype=torch.uint8, device="cuda")
-    sx.spexis_linear(x.cuda(), w.cuda(), y, residual=(y if alias else res.cuda()) if res is not None else None,
+    sx.spexis_linear(x.cuda(), sx.spexis_pack_weight(w.cuda()), y, residual=(y if alias else res.cuda()) if res is not None else None,
                      workspace=ws)
     torch.cuda.synchronize()
     return y.float().cpu().double().numpy(), ws_n
@@ -74,16 +74,45 @@ def test_linear_output_may_alias_residual():
 
 
 def test_linear_rejects_bad_arguments():
-    x = torch.zeros((4, 100), dtype=torch.bfloat16, device="cuda")
-    w = torch.zeros((8, 100), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(sx.SpexisError) as e:   # cols not a multiple of 64: no packed layout
+        sx.spexis_pack_weight(torch.zeros((8, 100), dtype=torch.bfloat16, device="cuda"))
+    assert e.value.code == sx.SPEXIS_ERR_UNSUPPORTED
+    x = torch.zeros((4, 320), dtype=torch.bfloat16, device="cuda")
+    w = sx.spexis_pack_weight(torch.zeros((8, 320), dtype=torch.bfloat16, device="cuda"))
     y = torch.empty((4, 8), dtype=torch.bfloat16, device="cuda")
-    with pytest.raises(sx.SpexisError) as e:
+    with pytest.raises(sx.SpexisError) as e:   # in_features not a multiple of 256
         sx.spexis_linear(x, w, y)
     assert e.value.code == sx.SPEXIS_ERR_UNSUPPORTED
     x = torch.zeros((64, 1024), dtype=torch.bfloat16, device="cuda")
-    w = torch.zeros((4096, 1024), dtype=torch.bfloat16, device="cuda")
+    w = sx.spexis_pack_weight(torch.zeros((4096, 1024), dtype=torch.bfloat16, device="cuda"))
     y = torch.empty((64, 4096), dtype=torch.bfloat16, device="cuda")
     assert sx.spexis_linear_workspace_size(64, 4096, 1024) > 0
     with pytest.raises(sx.SpexisError) as e:
         sx.spexis_linear(x, w, y)
     assert e.value.code == sx.SPEXIS_ERR_WORKSPACE_TOO_SMALL
+
+
+def packed_reference(w_bits: np.ndarray) -> np.ndarray:
+    """The documented packed layout, restated on the host: tile (n, c) of 32 rows x 64 columns at
+    (n * C + c) * 2048, element (r, 64c + 32h + 8s + e) at ((s * 2 + h) * 32 + r) * 8 + e."""
+    N, K = w_bits.shape
+    Np, C = (N + 31) // 32, K // 64
+    out = np.zeros(Np * C * 2048, np.uint16)
+    for n in range(Np):
+        for c in range(C):
+            base = (n * C + c) * 2048
+            for r in range(32):
+                if 32 * n + r >= N:
+                    continue
+                for h in range(2):
+                    for s in range(4):
+                        at = base + ((s * 2 + h) * 32 + r) * 8
+                        out[at:at + 8] = w_bits[32 * n + r, 64 * c + 32 * h + 8 * s:64 * c + 32 * h + 8 * s + 8]
+    return out
+
+
+@pytest.mark.parametrize("N,K", [(1, 64), (33, 128), (100, 256), (64, 512)])
+def test_pack_weight_layout(N, K):
+    w, wb = bf16_pair((N, K), N + K, 1.0)
+    got = sx.spexis_pack_weight(w.cuda()).view(torch.int16).cpu().numpy().view(np.uint16)
+    np.testing.assert_array_equal(got, packed_reference(wb))

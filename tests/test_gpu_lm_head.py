@@ -38,7 +38,7 @@ def run_lm_head(h, w, T, want_logits=True):
     tiles = sx.spexis_lm_head_tiles(V)
     stats = torch.empty((rows, tiles, 2), dtype=torch.float32, device="cuda")
     logits = torch.empty((rows, V), dtype=torch.float32, device="cuda") if want_logits else None
-    sx.spexis_lm_head(h.cuda(), w.cuda(), stats, logits=logits, temperature=T)
+    sx.spexis_lm_head(h.cuda(), sx.spexis_pack_weight(w.cuda()), stats, logits=logits, temperature=T, vocab=V)
     torch.cuda.synchronize()
     return (logits.cpu().numpy() if want_logits else None), stats.cpu().numpy()
 
@@ -126,8 +126,9 @@ def test_accept_with_fused_statistics_agrees_with_oracle():
     dl = torch.empty((Td, V), dtype=torch.float32, device="cuda")
     ts = torch.empty((Tt, tiles, 2), dtype=torch.float32, device="cuda")
     ds = torch.empty((Td, tiles, 2), dtype=torch.float32, device="cuda")
-    sx.spexis_lm_head(ht.cuda(), w.cuda(), ts, logits=tl, temperature=T)
-    sx.spexis_lm_head(hd.cuda(), w.cuda(), ds, logits=dl, temperature=T)
+    wp = sx.spexis_pack_weight(w.cuda())
+    sx.spexis_lm_head(ht.cuda(), wp, ts, logits=tl, temperature=T)
+    sx.spexis_lm_head(hd.cuda(), wp, ds, logits=dl, temperature=T)
     dev = lambda x: torch.as_tensor(x, device="cuda")
     acc = torch.empty(B, dtype=torch.int32, device="cuda")
     tok = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")

@@ -101,7 +101,7 @@ def test_sample_from_lm_head_statistics():
     tiles = sx.spexis_lm_head_tiles(V)
     logits = torch.empty((rows, V), dtype=torch.float32, device="cuda")
     stats = torch.empty((rows, tiles, 2), dtype=torch.float32, device="cuda")
-    sx.spexis_lm_head(h.cuda(), w.cuda(), stats, logits=logits, temperature=T)
+    sx.spexis_lm_head(h.cuda(), sx.spexis_pack_weight(w.cuda()), stats, logits=logits, temperature=T)
     u = np.random.default_rng(4).random(rows, dtype=np.float32)
     tok, prob, st = gpu_sample(sx.SPEXIS_INPUT_LOGITS, logits, u, stats=stats, T=T)
     tok2, prob2, st2 = gpu_sample(sx.SPEXIS_INPUT_LOGITS, logits, u, T=T)
