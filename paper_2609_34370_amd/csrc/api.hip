@@ -392,9 +392,8 @@ int spexis_pack_weight(const void* weight, int32_t rows, int32_t cols, void* pac
 
 size_t spexis_linear_workspace_size(int32_t rows, int32_t out_features, int32_t in_features) {
   if (rows <= 0 || out_features <= 0 || in_features <= 0 || in_features % 256 != 0) return 0;
-  spexis::LinearParams p{};
-  spexis::linear_plan(rows, out_features, in_features, p);
-  return p.S > 1 ? (size_t)p.S * rows * out_features * sizeof(float) : 0;
+  const int S = spexis::linear_split(rows, out_features, in_features);
+  return S > 1 ? (size_t)S * rows * out_features * sizeof(float) : 0;
 }
 
 int spexis_linear(const void* x, const void* weight, const void* residual, int32_t rows, int32_t out_features,
@@ -405,22 +404,37 @@ int spexis_linear(const void* x, const void* weight, const void* residual, int32
   if (in_features % 256 != 0)
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_linear: in_features %d is not a multiple of 256", in_features);
   if (rows == 0) return ok();
-  if ((int64_t)rows * in_features >= (1ll << 40) || (int64_t)out_features * in_features >= (1ll << 40) ||
-      (int64_t)rows * out_features >= (1ll << 36))
+  const int64_t tiles = (out_features + spexis::kLmCols - 1) / spexis::kLmCols;
+  const int64_t groups = (rows + spexis::kLmRows - 1) / spexis::kLmRows;
+  if ((tiles + 7) / 8 * 8 * groups >= (1ll << 31) || (int64_t)rows * out_features >= (1ll << 36) ||
+      (int64_t)rows * in_features >= (1ll << 40))
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_linear: problem too large");
-  spexis::LinearParams p{};
-  spexis::linear_plan(rows, out_features, in_features, p);
-  if ((int64_t)(p.ntiles * (int64_t)p.S + 7) / 8 * 8 * p.mgroups >= (1ll << 31))
-    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_linear: problem too large");
+  const int S = spexis::linear_split(rows, out_features, in_features);
   const size_t need = spexis_linear_workspace_size(rows, out_features, in_features);
   if (need > 0 && (!workspace || workspace_bytes < need))
     return fail(SPEXIS_ERR_WORKSPACE_TOO_SMALL, "spexis_linear: workspace %zu bytes < %zu needed", workspace_bytes,
                 need);
-  p.x = x;
-  p.w = weight;
+  spexis::LinearParams p{};
+  p.proj.h = x;
+  p.proj.w = weight;
+  p.proj.M = rows;
+  p.proj.V = out_features;
+  p.proj.d = in_features;
+  p.proj.ntiles = (int)tiles;
+  p.proj.mgroups = (int)groups;
+  p.proj.ksplit = S;
+  if (S > 1) {
+    p.proj.logits = static_cast<float*>(workspace);   // [S][rows][out] partials
+  } else {
+    p.proj.y = y;
+    p.proj.res = residual;
+  }
+  p.part = static_cast<float*>(workspace);
   p.res = residual;
   p.y = y;
-  p.part = static_cast<float*>(workspace);
+  p.M = rows;
+  p.N = out_features;
+  p.S = S;
   return hip_result(spexis::launch_linear(p, (hipStream_t)stream), "spexis_linear");
 }
 
@@ -481,8 +495,9 @@ int spexis_lm_head(const void* hidden, const void* weight, int32_t rows, int32_t
   p.d = hidden_dim;
   p.ntiles = (int)tiles;
   p.mgroups = (int)groups;
+  p.ksplit = 1;
   p.c = (float)(1.4426950408889634 / (double)temperature);
-  return hip_result(spexis::launch_lm_head(p, (hipStream_t)stream), "spexis_lm_head");
+  return hip_result(spexis::launch_projection(p, (hipStream_t)stream), "spexis_lm_head");
 }
 
 }  // extern "C"

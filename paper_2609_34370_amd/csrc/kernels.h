@@ -47,12 +47,16 @@ __host__ __device__ inline int64_t attn_ws_bytes(int nwaves, int rmax, int D) {
 }
 
 // LM-head projection logits = h W^T with the row statistics of its 128-column tiles.
-struct LmParams {  // w: packed (launch_pack_weight)
+// The projection out = h W^T shared by the LM head and the adapter's linear layers.
+struct LmParams {
   const void* h;         // [M][d] bf16
-  const void* w;         // [V][d] bf16
-  float* logits;         // [M][V] fp32 (null: not written)
-  float* stats;          // [M][ntiles][2]: max of x*c and sum of 2^(x*c - max) over each tile
+  const void* w;         // [V][d] bf16, packed (launch_pack_weight)
+  float* logits;         // [M][V] fp32 (null: not written); with ksplit > 1, [ksplit][M][V] partials
+  float* stats;          // [M][ntiles][2]: max of x*c and sum of 2^(x*c - max) over each tile (or null)
+  void* y;               // [M][V] bf16 output, bf16(acc + res), instead of logits (ksplit == 1)
+  const void* res;       // [M][V] bf16 residual for y, or null
   int M, V, d, ntiles, mgroups;
+  int ksplit;            // K split over workgroups (grid y); each takes d / ksplit
   float c;               // log2(e) / temperature
 };
 
@@ -72,18 +76,13 @@ struct SelectParams {
 
 constexpr int kSelectMaxDrafts = 16384;
 
+// spexis_linear: the projection kernel, then (K split) the reduce of its partials.
 struct LinearParams {
-  const void* x;     // bf16 [M][K]
-  const void* w;     // bf16 [N][K], packed (launch_pack_weight)
+  LmParams proj;
+  float* part;       // fp32 [S][M][N] when S > 1
   const void* res;   // bf16 [M][N] or null
   void* y;           // bf16 [M][N]
-  float* part;       // fp32 [S][M][N] when S > 1
-  int M, N, K;
-  int nrt;           // row tiles of 32 per workgroup (1, 2 or 4)
-  int ntiles;        // column tiles of 32
-  int mgroups;       // row groups of 32 * nrt
-  int S;             // K split over workgroups
-  int kw;            // K values per wave
+  int M, N, S;
 };
 
 struct LookaheadParams {
@@ -138,14 +137,15 @@ constexpr int kAcceptSub = 4096;     // vocab entries per partial result (one wo
 
 hipError_t launch_append(const AppendParams& p, hipStream_t s);
 hipError_t launch_attention(const AttnParams& p, hipStream_t s);
-hipError_t launch_lm_head(const LmParams& p, hipStream_t s);
+
 hipError_t launch_select(const SelectParams& p, hipStream_t s);
 hipError_t launch_lookahead(const LookaheadParams& p, hipStream_t s);
-void linear_plan(int M, int N, int K, LinearParams& p);
+int linear_split(int M, int N, int K);
 hipError_t launch_pack_weight(const void* w, int N, int K, void* out, hipStream_t s);
 // packed weight tile (32 rows x 64 K values, 2048 elements) holding rows 32n.., K values 64c..
 constexpr int kPackTile = 2048;
 hipError_t launch_linear(const LinearParams& p, hipStream_t s);
+hipError_t launch_projection(const LmParams& p, hipStream_t s);
 hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V, float c, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s);
 

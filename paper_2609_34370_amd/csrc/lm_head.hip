@@ -30,6 +30,15 @@ namespace {
 
 constexpr int kRT = kLmRows / 32;   // row tiles per workgroup
 
+__device__ __forceinline__ uint16_t bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0;   // NaN
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf16_float(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
 // W rows are read once: non-temporal loads keep them from evicting h out of L2.
 template <bool kStream>
 __device__ __forceinline__ u32x4 ldw(const uint16_t* p) {
@@ -51,12 +60,15 @@ void lm_head_kernel(LmParams p) {
   const int m0 = mg * kLmRows, n0 = nt * kLmCols;
   const int rows = min(kLmRows, p.M - m0);
   const int v = n0 + 32 * wave + col;
-  const int nsteps = p.d / kLmK;
+  // K split: workgroup row ks takes K values ks * klen .. +klen-1 (nsteps steps of 64)
+  const int ks = blockIdx.y;
+  const int klen = p.d / p.ksplit, nsteps = klen / kLmK;
   // this wave's 32 columns are packed tile row (n0 + 32 wave) / 32 (clamped for the columns past V,
   // whose results are dropped); lane l reads 16 contiguous bytes at s * 512 + 8 l of each tile
   const int wtile = min(4 * nt + wave, (p.V + 31) / 32 - 1);
-  const uint16_t* wrow = reinterpret_cast<const uint16_t*>(p.w) + (int64_t)wtile * nsteps * kPackTile + 8 * lane;
-  const uint16_t* hbase = reinterpret_cast<const uint16_t*>(p.h) + (int64_t)m0 * p.d;
+  const uint16_t* wrow = reinterpret_cast<const uint16_t*>(p.w) +
+                         ((int64_t)wtile * (p.d / kLmK) + (int64_t)ks * nsteps) * kPackTile + 8 * lane;
+  const uint16_t* hbase = reinterpret_cast<const uint16_t*>(p.h) + (int64_t)m0 * p.d + (int64_t)ks * klen;
 
   // h in LDS: stage x, row r, 16-byte chunk kc of the step stored at position kc ^ ((r >> 1) & 7),
   // so that the 16 rows one ds_read_b128 pass serves hit 16 distinct 16-byte bank groups
@@ -142,18 +154,36 @@ void lm_head_kernel(LmParams p) {
     }
   }
 
-  // ---- epilogue: logits, and each row's statistics over this workgroup's 128 columns
+  // ---- epilogue: logits (or partials, or bf16 outputs), and each row's statistics over this
+  // workgroup's 128 columns
   const bool live = v < p.V;
   if (p.logits && live) {
+    float* out = p.logits + (int64_t)ks * p.M * p.V;
 #pragma unroll
     for (int t = 0; t < NRT; ++t) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int r = 32 * t + 8 * (i >> 2) + 4 * half + (i & 3);
-        if (r < rows) p.logits[(int64_t)(m0 + r) * p.V + v] = acc[t][i];
+        if (r < rows) out[(int64_t)(m0 + r) * p.V + v] = acc[t][i];
       }
     }
   }
+  if (p.y && live) {
+    const uint16_t* res = reinterpret_cast<const uint16_t*>(p.res);
+    uint16_t* y = reinterpret_cast<uint16_t*>(p.y);
+#pragma unroll
+    for (int t = 0; t < NRT; ++t) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int r = 32 * t + 8 * (i >> 2) + 4 * half + (i & 3);
+        if (r < rows) {
+          const int64_t at = (int64_t)(m0 + r) * p.V + v;
+          y[at] = bf16_rne(res ? acc[t][i] + bf16_float(res[at]) : acc[t][i]);
+        }
+      }
+    }
+  }
+  if (!p.stats) return;
   // Row statistics: each wave transposes one 32x32 tile at a time through its part of the
   // (now free) h stages, then lane r < 32 reduces row r over the wave's 32 columns.
   __shared__ float sm_m[4][32 * NRT], sm_z[4][32 * NRT];
@@ -195,16 +225,17 @@ void lm_head_kernel(LmParams p) {
 
 template <int NRT, int NA, int DEPTH, int WPE>
 static hipError_t launch_lm_nrt(const LmParams& p, hipStream_t s) {
-  // grid: tiles of 8 vocabulary tiles (one per XCD) x row groups, row groups innermost
+  // grid: tiles of 8 vocabulary tiles (one per XCD) x row groups, row groups innermost; y: K split
   const int64_t grid = (int64_t)((p.ntiles + 7) / 8) * 8 * p.mgroups;
+  const dim3 g((unsigned)grid, (unsigned)p.ksplit);
   if (p.mgroups == 1)
-    hipLaunchKernelGGL((lm_head_kernel<true, NRT, NA, DEPTH, WPE>), dim3((unsigned)grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((lm_head_kernel<true, NRT, NA, DEPTH, WPE>), g, dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL((lm_head_kernel<false, NRT, NA, DEPTH, WPE>), dim3((unsigned)grid), dim3(256), 0, s, p);
+    hipLaunchKernelGGL((lm_head_kernel<false, NRT, NA, DEPTH, WPE>), g, dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
-hipError_t launch_lm_head(const LmParams& p, hipStream_t s) {
+hipError_t launch_projection(const LmParams& p, hipStream_t s) {
   // row tiles computed per workgroup: the smallest instantiated count covering the rows (a
   // group of fewer rows repeats its last row in the padding tiles, whose results are dropped)
   const int need = p.M >= kLmRows ? kRT : (p.M + 31) / 32;
