@@ -637,13 +637,8 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
   const float fill = r.logits ? -INFINITY : 0.f;
 
   // total and exact threshold; the sub-chunk holding t
-  uint64_t incl = own;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint64_t y = __shfl_up(incl, o, kWave);
-    if (lane >= o) incl += y;
-  }
-  const uint64_t S = __shfl(incl, kWave - 1, kWave);
+  const uint64_t incl = wave_incl_scan_u64(own);
+  const uint64_t S = readlane_u64(incl, kWave - 1);
   const uint64_t t = exact_threshold(p.u_sample[b], S);
   uint64_t excl = incl - own;
   int cstar = -1;
@@ -659,9 +654,9 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
     }
   }
   const uint64_t found = __ballot(cstar >= 0);
-  const int src = found ? __ffsll((unsigned long long)found) - 1 : 0;
-  cstar = __shfl(cstar, src, kWave);
-  tt = __shfl(tt, src, kWave);
+  const int src = __builtin_amdgcn_readfirstlane(found ? __ffsll((unsigned long long)found) - 1 : 0);
+  cstar = __builtin_amdgcn_readlane(cstar, src);
+  tt = readlane_u64(tt, src);
   if (cstar < 0) return;   // unreachable: S > 0 because M > 0 gives a weight >= 2^40
   // wave w owns entries cstar*4096 + 1024 w .. + 1023 of the sub-chunk, lane l 16 of them, in order
   constexpr int kRun = kAcceptSub / (kWaves * kWave);   // 16
@@ -684,12 +679,7 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
     wv[e] = entry_weight(r, p.c, pv[e], qv[e], use_p, s);
     mine += wv[e];
   }
-  uint64_t inc2 = mine;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint64_t y = __shfl_up(inc2, o, kWave);
-    if (lane >= o) inc2 += y;
-  }
+  const uint64_t inc2 = wave_incl_scan_u64(mine);
   __shared__ uint64_t sm_tot[kWaves];
   if (lane == kWave - 1) sm_tot[wave] = inc2;
   __syncthreads();

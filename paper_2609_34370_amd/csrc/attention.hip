@@ -178,8 +178,10 @@ void verify_attn_kernel(AttnParams p) {
     const int tk = min(t0 + col, lc.S - 1);   // past the end: any valid slot, masked later
     const int kblk = (BS == 16 && (tk >> 4) != 2 * lc.t) ? lb : la;
     const uint16_t* kp = kc + ((int64_t)kblk * p.hkv + h) * head_stride + (tk % BS) * 8 + half * BS * 8;
+    // K tiles are read once: non-temporal loads (measured faster than plain loads of K, or than
+    // non-temporal loads of both K and V, on every workload)
 #pragma unroll
-    for (int s = 0; s < KS; ++s) B.k[s] = ld16(kp + s * (2 * BS * 8));
+    for (int s = 0; s < KS; ++s) B.k[s] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kp + s * (2 * BS * 8)));
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
       const int vblk = (BS == 16 && s2 == 1) ? lb : la;

@@ -33,22 +33,6 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Butterfly reductions across the 64 lanes of a wave.
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
-}
-__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
-}
 // DPP lane controls: row_shr:n (n = 1..15), broadcast of lane 15 of each row into the next
 // row, broadcast of lane 31 into rows 2 and 3, and quad permutations.
 constexpr int kDppRowShr = 0x110;
@@ -73,10 +57,71 @@ __device__ __forceinline__ int wave_incl_scan_i32(int v, int lane) {
 __device__ __forceinline__ int wave_sum_i32(int v) {
   return __builtin_amdgcn_readlane(wave_incl_scan_i32(v, 0), kWave - 1);
 }
+// A DPP lane move of a 32-bit value; lanes the move does not write get `old`.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v, uint32_t old) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, kCtrl, kRowMask, 0xF, false);
+}
+// Reductions over the 64 lanes of a wave, in DPP moves (the pattern of the integer scan, so lane
+// 63 ends with the whole wave's result), broadcast with readlane: the result is uniform.
+#define SPEXIS_DPP_REDUCE(v, move, op) \
+  v = op(v, move<kDppRowShr + 1, 0xF>(v));     \
+  v = op(v, move<kDppRowShr + 2, 0xF>(v));     \
+  v = op(v, move<kDppRowShr + 4, 0xF>(v));     \
+  v = op(v, move<kDppRowShr + 8, 0xF>(v));     \
+  v = op(v, move<kDppRowBcast15, 0xA>(v));     \
+  v = op(v, move<kDppRowBcast31, 0xC>(v));
+
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ float dpp_max_move(float v) {
+  return __uint_as_float(dpp_u32<kCtrl, kRowMask>(__float_as_uint(v), 0xFF800000u));   // -inf elsewhere
+}
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ float dpp_sum_move(float v) {
+  return __uint_as_float(dpp_u32<kCtrl, kRowMask>(__float_as_uint(v), 0u));
+}
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ int dpp_or_move(int v) {
+  return (int)dpp_u32<kCtrl, kRowMask>((uint32_t)v, 0u);
+}
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint64_t dpp_u64_move(uint64_t v) {
+  const uint32_t lo = dpp_u32<kCtrl, kRowMask>((uint32_t)v, 0u);
+  const uint32_t hi = dpp_u32<kCtrl, kRowMask>((uint32_t)(v >> 32), 0u);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ float op_max(float a, float b) { return fmaxf(a, b); }
+__device__ __forceinline__ float op_addf(float a, float b) { return a + b; }
+__device__ __forceinline__ int op_or(int a, int b) { return a | b; }
+__device__ __forceinline__ uint64_t op_addu64(uint64_t a, uint64_t b) { return a + b; }
+
+__device__ __forceinline__ float readlane_f32(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+  SPEXIS_DPP_REDUCE(v, dpp_max_move, op_max)
+  return readlane_f32(v, kWave - 1);
+}
+// (the summation order is fixed: every caller of wave_sum on the same values gets the same sum)
+__device__ __forceinline__ float wave_sum(float v) {
+  SPEXIS_DPP_REDUCE(v, dpp_sum_move, op_addf)
+  return readlane_f32(v, kWave - 1);
+}
 __device__ __forceinline__ int wave_or(int v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v |= __shfl_xor(v, o, kWave);
+  SPEXIS_DPP_REDUCE(v, dpp_or_move, op_or)
+  return __builtin_amdgcn_readlane(v, kWave - 1);
+}
+// Inclusive prefix sum of 64-bit values over the lanes of a wave, and the wave's total.
+__device__ __forceinline__ uint64_t wave_incl_scan_u64(uint64_t v) {
+  SPEXIS_DPP_REDUCE(v, dpp_u64_move, op_addu64)
   return v;
 }
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) { return readlane_u64(wave_incl_scan_u64(v), kWave - 1); }
 
 }  // namespace spexis
