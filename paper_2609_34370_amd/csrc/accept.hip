@@ -124,6 +124,8 @@ __device__ __forceinline__ f32x4 load4(const float* row, int e, int V, bool vec,
 // Wave `wave`'s coalesced part of sub-chunk `sub`: lane l holds entries
 // sub*4096 + 1024 wave + 256 j + 4 l + i.  A part inside the row takes the straight-line path,
 // so all its loads are in flight together.
+// kNT: non-temporal loads, for rows read once (the statistics pass).
+template <bool kNT = false>
 __device__ __forceinline__ void load_sub(const float* row, int sub, int wave, int V, bool vec, float fill, int lane,
                                          float (&v)[kPerLane]) {
   const int base = sub * kAcceptSub + wave * kWaveSub;
@@ -131,7 +133,7 @@ __device__ __forceinline__ void load_sub(const float* row, int sub, int wave, in
     const f32x4* src = reinterpret_cast<const f32x4*>(row + base) + lane;
 #pragma unroll
     for (int j = 0; j < kF4; ++j) {
-      const f32x4 x = src[j * kWave];
+      const f32x4 x = kNT ? __builtin_nontemporal_load(src + j * kWave) : src[j * kWave];
 #pragma unroll
       for (int i = 0; i < 4; ++i) v[4 * j + i] = x[i];
     }
@@ -404,7 +406,7 @@ __global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p, 
     }
     const float* row = which ? p.draft + (int64_t)(g.d0 + pos) * p.V : p.target + (int64_t)(g.t0 + pos) * p.V;
     float v[kPerLane];
-    load_sub(row, sub, wave, p.V, (p.V & 3) == 0, -INFINITY, lane, v);
+    load_sub<true>(row, sub, wave, p.V, (p.V & 3) == 0, -INFINITY, lane, v);
     float m, z;
     wave_stats(v, p.c, m, z);
     // the four waves in order: common maximum, rescaled sums; NaN stays NaN

@@ -32,6 +32,18 @@
 
 namespace spexis {
 
+// Lane l and lane l ^ 32 combined, in one cross-half lane swap (v_permlane32_swap): the swap of a
+// value with itself leaves the lower half's value in the first result and the upper half's in the
+// second, in every lane.
+__device__ __forceinline__ float halves_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float halves_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" of the running maxima
 constexpr float kLazy = 8.0f;         // base-2 headroom before the running maximum moves
 constexpr int kWaitVmcnt0 = 0x0F70;   // s_waitcnt operand: vmcnt(0), expcnt and lgkmcnt not waited
@@ -259,7 +271,7 @@ void verify_attn_kernel(AttnParams p) {
     }
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const float lt = l[nt] + __shfl_xor(l[nt], 32, kWave);
+      const float lt = halves_sum(l[nt]);
       const int r = nt * 32 + col;
       if (r >= R) continue;
       if (whole) {
@@ -336,7 +348,7 @@ void verify_attn_kernel(AttnParams p) {
       float mx = x[0];
 #pragma unroll
       for (int e = 1; e < 16; ++e) mx = fmaxf(mx, x[e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      mx = halves_max(mx);
       // Lazy rescaling: the reference maximum moves only when a score exceeds it by more than
       // 2^kLazy, so 2^(x - m) stays <= 2^kLazy and the accumulators are rescaled rarely.
       if (__builtin_amdgcn_ballot_w64(mx > m[nt] + kLazy) != 0) {
