@@ -7,7 +7,7 @@
 // Acceptance combines the tiles of a row into its normaliser without reading the row again.
 //
 // Work decomposition: one workgroup per (vocabulary tile of 128 columns, group of up to 320
-// rows of h).  Each of its four waves owns 32 columns and all the group's rows: ten 32x32
+// rows of h); its four waves split the tile in a grid of waves (below), each holding 32x32
 // accumulator tiles of v_mfma_f32_32x32x16_bf16 (A operand: h rows, B operand: W rows).
 //   * W, the stream that matters (V*d*2 bytes, read once), goes straight from HBM into each
 //     wave's registers, DEPTH K-steps of 64 ahead.  It is packed (pack.hip) so that each operand
@@ -48,34 +48,45 @@ __device__ __forceinline__ u32x4 ldw(const uint16_t* p) {
 
 }  // namespace
 
-template <bool kStream, int NRT, int NA, int DEPTH, int WPE>
+// Waves form a WR x WC grid over the workgroup's (32 * WR * RT) rows x 128 columns: wave
+// (wr, wc) computes RT row tiles x CT column tiles (WC * CT = 4).  One column of waves (WR = 1,
+// CT = 1) suits few rows; for 320-row groups a 2 x 2 grid halves the h fragments each wave reads
+// from LDS per step for the same MFMA work (each W tile is then loaded by two waves, the second
+// load an L1 hit).
+template <bool kStream, int RT, int CT, int WR, int NA, int DEPTH, int WPE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE)))
 void lm_head_kernel(LmParams p) {
   static_assert(DEPTH >= NA + 2 && DEPTH % NA == 0 && DEPTH % 2 == 0, "pipeline shape");
+  constexpr int WC = 4 / WR;
+  static_assert(WR * WC == 4 && WC * CT == 4, "wave grid");
+  constexpr int NRT = WR * RT;   // row tiles of the workgroup
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 31, half = lane >> 5;
+  const int wr = wave / WC, wc = wave % WC;
   const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
   const int mg = local % p.mgroups;
   const int nt = (local / p.mgroups) * 8 + xcd;
   if (nt >= p.ntiles) return;
   const int m0 = mg * kLmRows, n0 = nt * kLmCols;
   const int rows = min(kLmRows, p.M - m0);
-  const int v = n0 + 32 * wave + col;
   // K split: workgroup row ks takes K values ks * klen .. +klen-1 (nsteps steps of 64)
   const int ks = blockIdx.y;
   const int klen = p.d / p.ksplit, nsteps = klen / kLmK;
-  // this wave's 32 columns are packed tile row (n0 + 32 wave) / 32 (clamped for the columns past V,
-  // whose results are dropped); lane l reads 16 contiguous bytes at s * 512 + 8 l of each tile
-  const int wtile = min(4 * nt + wave, (p.V + 31) / 32 - 1);
-  const uint16_t* wrow = reinterpret_cast<const uint16_t*>(p.w) +
-                         ((int64_t)wtile * (p.d / kLmK) + (int64_t)ks * nsteps) * kPackTile + 8 * lane;
+  // column tile c of this wave is packed tile row 4 nt + CT wc + c (clamped for the columns past
+  // V, whose results are dropped); lane l reads 16 contiguous bytes at s * 512 + 8 l of each tile
+  const uint16_t* wrow[CT];
+#pragma unroll
+  for (int c = 0; c < CT; ++c) {
+    const int wtile = min(4 * nt + CT * wc + c, (p.V + 31) / 32 - 1);
+    wrow[c] = reinterpret_cast<const uint16_t*>(p.w) +
+              ((int64_t)wtile * (p.d / kLmK) + (int64_t)ks * nsteps) * kPackTile + 8 * lane;
+  }
   const uint16_t* hbase = reinterpret_cast<const uint16_t*>(p.h) + (int64_t)m0 * p.d + (int64_t)ks * klen;
 
   // h in LDS: stage x, row r, 16-byte chunk kc of the step stored at position kc ^ ((r >> 1) & 7),
-  // so that the 16 rows one ds_read_b128 pass serves hit 16 distinct 16-byte bank groups
-  // only the NRT row tiles the group computes are staged: 32 * NRT rows * 8 chunks = NRT chunks
-  // per thread per step
+  // so that the 16 rows one ds_read_b128 pass serves hit 16 distinct 16-byte bank groups.  Only
+  // the workgroup's NRT row tiles are staged: 32 * NRT rows * 8 chunks = NRT chunks per thread.
+  // (At least 72 rows: the epilogue transposes 4 x 32 x 36 floats through this space.)
   constexpr int kAChunks = NRT;
-  // (at least 72 rows: the epilogue transposes 4 x 32 x 36 floats through this space)
   constexpr int kStage = (32 * NRT > 72 ? 32 * NRT : 72) * 8;
   __shared__ u32x4 sm_a[2][kStage];
   u32x4 areg[NA][kAChunks];   // h chunks of the next NA steps, in flight
@@ -96,18 +107,22 @@ void lm_head_kernel(LmParams p) {
       sm_a[stage][r * 8 + (kc ^ ((r >> 1) & 7))] = src[u];
     }
   };
-  u32x4 wb[DEPTH][4];
-  auto load_w = [&](u32x4 (&dst)[4], int j) {
-    const uint16_t* src = wrow + (int64_t)min(j, nsteps - 1) * kPackTile;
+  u32x4 wb[DEPTH][CT][4];
+  auto load_w = [&](u32x4 (&dst)[CT][4], int j) {
+    const int64_t off = (int64_t)min(j, nsteps - 1) * kPackTile;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) dst[s] = ldw<kStream>(src + 512 * s);
+    for (int c = 0; c < CT; ++c)
+#pragma unroll
+      for (int s = 0; s < 4; ++s) dst[c][s] = ldw<kStream>(wrow[c] + off + 512 * s);
   };
 
-  f32x16 acc[NRT];
+  f32x16 acc[RT][CT];
 #pragma unroll
-  for (int t = 0; t < NRT; ++t)
+  for (int t = 0; t < RT; ++t)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc[t][e] = 0.f;
+    for (int c = 0; c < CT; ++c)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[t][c][e] = 0.f;
 
   // prologue: h step 0 into stage 0, W steps 0 .. DEPTH-1, h steps 1 .. NA into registers
   load_a(areg[0], 0);
@@ -120,23 +135,26 @@ void lm_head_kernel(LmParams p) {
 
   // The A fragments of k-step s+1 are read from LDS while the MFMAs of k-step s run.
   auto frag = [&](int stage, int t, int s) {
-    const int m = 32 * t + col;
+    const int m = 32 * (wr * RT + t) + col;
     return sm_a[stage][m * 8 + ((4 * half + s) ^ ((m >> 1) & 7))];
   };
-  auto compute = [&](const u32x4 (&w)[4], int stage) {
-    u32x4 fa[2][NRT];
+  auto compute = [&](const u32x4 (&w)[CT][4], int stage) {
+    u32x4 fa[2][RT];
 #pragma unroll
-    for (int t = 0; t < NRT; ++t) fa[0][t] = frag(stage, t, 0);
+    for (int t = 0; t < RT; ++t) fa[0][t] = frag(stage, t, 0);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       if (s + 1 < 4) {
 #pragma unroll
-        for (int t = 0; t < NRT; ++t) fa[(s + 1) & 1][t] = frag(stage, t, s + 1);
+        for (int t = 0; t < RT; ++t) fa[(s + 1) & 1][t] = frag(stage, t, s + 1);
       }
-      const bf16x8 bop = as_bf16x8(w[s]);
 #pragma unroll
-      for (int t = 0; t < NRT; ++t)
-        acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fa[s & 1][t]), bop, acc[t], 0, 0, 0);
+      for (int c = 0; c < CT; ++c) {
+        const bf16x8 bop = as_bf16x8(w[c][s]);
+#pragma unroll
+        for (int t = 0; t < RT; ++t)
+          acc[t][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fa[s & 1][t]), bop, acc[t][c], 0, 0, 0);
+      }
     }
   };
 
@@ -155,96 +173,125 @@ void lm_head_kernel(LmParams p) {
   }
 
   // ---- epilogue: logits (or partials, or bf16 outputs), and each row's statistics over this
-  // workgroup's 128 columns
-  const bool live = v < p.V;
-  if (p.logits && live) {
+  // workgroup's 128 columns.  Accumulator value i of lane l in tile (t, c): row
+  // 32 (wr RT + t) + 8 (i / 4) + 4 (l / 32) + i % 4, column 32 (CT wc + c) + l % 32.
+  auto out_row = [&](int t, int i) { return 32 * (wr * RT + t) + 8 * (i >> 2) + 4 * half + (i & 3); };
+  auto out_col = [&](int c) { return n0 + 32 * (CT * wc + c) + col; };
+  if (p.logits) {
     float* out = p.logits + (int64_t)ks * p.M * p.V;
 #pragma unroll
-    for (int t = 0; t < NRT; ++t) {
+    for (int c = 0; c < CT; ++c) {
+      const int v = out_col(c);
+      if (v >= p.V) continue;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int r = 32 * t + 8 * (i >> 2) + 4 * half + (i & 3);
-        if (r < rows) out[(int64_t)(m0 + r) * p.V + v] = acc[t][i];
-      }
+      for (int t = 0; t < RT; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int r = out_row(t, i);
+          if (r < rows) out[(int64_t)(m0 + r) * p.V + v] = acc[t][c][i];
+        }
     }
   }
-  if (p.y && live) {
+  if (p.y) {
     const uint16_t* res = reinterpret_cast<const uint16_t*>(p.res);
     uint16_t* y = reinterpret_cast<uint16_t*>(p.y);
 #pragma unroll
-    for (int t = 0; t < NRT; ++t) {
+    for (int c = 0; c < CT; ++c) {
+      const int v = out_col(c);
+      if (v >= p.V) continue;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int r = 32 * t + 8 * (i >> 2) + 4 * half + (i & 3);
-        if (r < rows) {
-          const int64_t at = (int64_t)(m0 + r) * p.V + v;
-          y[at] = bf16_rne(res ? acc[t][i] + bf16_float(res[at]) : acc[t][i]);
+      for (int t = 0; t < RT; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int r = out_row(t, i);
+          if (r < rows) {
+            const int64_t at = (int64_t)(m0 + r) * p.V + v;
+            y[at] = bf16_rne(res ? acc[t][c][i] + bf16_float(res[at]) : acc[t][c][i]);
+          }
         }
-      }
     }
   }
   if (!p.stats) return;
-  // Row statistics: each wave transposes one 32x32 tile at a time through its part of the
-  // (now free) h stages, then lane r < 32 reduces row r over the wave's 32 columns.
-  __shared__ float sm_m[4][32 * NRT], sm_z[4][32 * NRT];
+  // Row statistics: each wave transposes one 32x32 tile at a time through its part of the (now
+  // free) h stages; lane r < 32 reduces row r over the tile's 32 columns, then over the wave's
+  // CT tiles in order; the WC waves of a row are combined in order at the end.
+  __shared__ float sm_m[WC][32 * NRT], sm_z[WC][32 * NRT];
   constexpr int kTS = 36;   // floats per transposed row (16-byte aligned, padded)
   float* tile = reinterpret_cast<float*>(&sm_a[0][0]) + wave * 32 * kTS;
 #pragma unroll
-  for (int t = 0; t < NRT; ++t) {
+  for (int t = 0; t < RT; ++t) {
+    float wm = -INFINITY, wz = 0.f;
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      tile[(8 * (i >> 2) + 4 * half + (i & 3)) * kTS + col] = live ? acc[t][i] * p.c : -INFINITY;
-    if (lane < 32) {
-      f32x4 x[8];
+    for (int c = 0; c < CT; ++c) {
+      const bool live = out_col(c) < p.V;
 #pragma unroll
-      for (int q = 0; q < 8; ++q) x[q] = *reinterpret_cast<const f32x4*>(tile + lane * kTS + 4 * q);
-      float mx = -INFINITY;
+      for (int i = 0; i < 16; ++i)
+        tile[(8 * (i >> 2) + 4 * half + (i & 3)) * kTS + col] = live ? acc[t][c][i] * p.c : -INFINITY;
+      if (lane < 32) {
+        f32x4 x[8];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) mx = fmaxf(fmaxf(mx, fmaxf(x[q][0], x[q][1])), fmaxf(x[q][2], x[q][3]));
-      float e = 0.f;
-      if (mx != -INFINITY) {
+        for (int q = 0; q < 8; ++q) x[q] = *reinterpret_cast<const f32x4*>(tile + lane * kTS + 4 * q);
+        float mx = -INFINITY;
 #pragma unroll
-        for (int q = 0; q < 8; ++q)
+        for (int q = 0; q < 8; ++q) mx = fmaxf(fmaxf(mx, fmaxf(x[q][0], x[q][1])), fmaxf(x[q][2], x[q][3]));
+        float e = 0.f;
+        if (mx != -INFINITY) {
 #pragma unroll
-          for (int u = 0; u < 4; ++u) e += fast_exp2(x[q][u] - mx);
+          for (int q = 0; q < 8; ++q)
+#pragma unroll
+            for (int u = 0; u < 4; ++u) e += fast_exp2(x[q][u] - mx);
+        }
+        if (c == 0) {
+          wm = mx;
+          wz = e;
+        } else {
+          const float M = fmaxf(wm, mx);
+          wz = (wm != -INFINITY ? wz * fast_exp2(wm - M) : 0.f) + (mx != -INFINITY ? e * fast_exp2(mx - M) : 0.f);
+          wm = M;
+        }
       }
-      sm_m[wave][32 * t + lane] = mx;
-      sm_z[wave][32 * t + lane] = e;
+    }
+    if (lane < 32) {
+      sm_m[wc][32 * (wr * RT + t) + lane] = wm;
+      sm_z[wc][32 * (wr * RT + t) + lane] = wz;
     }
   }
   __syncthreads();
   for (int r = threadIdx.x; r < rows; r += 256) {
-    const float M = fmaxf(fmaxf(sm_m[0][r], sm_m[1][r]), fmaxf(sm_m[2][r], sm_m[3][r]));
+    float M = sm_m[0][r];
+#pragma unroll
+    for (int w = 1; w < WC; ++w) M = fmaxf(M, sm_m[w][r]);
     float Z = 0.f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w)
+    for (int w = 0; w < WC; ++w)
       if (sm_m[w][r] != -INFINITY) Z += sm_z[w][r] * fast_exp2(sm_m[w][r] - M);
     *reinterpret_cast<f32x2*>(p.stats + ((int64_t)(m0 + r) * p.ntiles + nt) * 2) = f32x2{M, Z};
   }
 }
 
-template <int NRT, int NA, int DEPTH, int WPE>
+template <int RT, int CT, int WR, int NA, int DEPTH, int WPE>
 static hipError_t launch_lm_nrt(const LmParams& p, hipStream_t s) {
   // grid: tiles of 8 vocabulary tiles (one per XCD) x row groups, row groups innermost; y: K split
   const int64_t grid = (int64_t)((p.ntiles + 7) / 8) * 8 * p.mgroups;
   const dim3 g((unsigned)grid, (unsigned)p.ksplit);
   if (p.mgroups == 1)
-    hipLaunchKernelGGL((lm_head_kernel<true, NRT, NA, DEPTH, WPE>), g, dim3(256), 0, s, p);
+    hipLaunchKernelGGL((lm_head_kernel<true, RT, CT, WR, NA, DEPTH, WPE>), g, dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL((lm_head_kernel<false, NRT, NA, DEPTH, WPE>), g, dim3(256), 0, s, p);
+    hipLaunchKernelGGL((lm_head_kernel<false, RT, CT, WR, NA, DEPTH, WPE>), g, dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
 hipError_t launch_projection(const LmParams& p, hipStream_t s) {
   // row tiles computed per workgroup: the smallest instantiated count covering the rows (a
-  // group of fewer rows repeats its last row in the padding tiles, whose results are dropped)
+  // group of fewer rows repeats its last row in the padding tiles, whose results are dropped).
+  // Few rows: one column of waves, two workgroups per CU, deep pipelines (the weight stream is
+  // the bound); many rows: a 2 x 2 wave grid (the LDS reads of h are).
   const int need = p.M >= kLmRows ? kRT : (p.M + 31) / 32;
-  // (few row tiles: two workgroups per CU, so each SIMD has a second wave to cover latency)
-  if (need <= 1) return launch_lm_nrt<1, 4, 8, 2>(p, s);
-  if (need <= 2) return launch_lm_nrt<2, 4, 8, 2>(p, s);
-  if (need <= 4) return launch_lm_nrt<4, 4, 8, 1>(p, s);
-  if (need <= 6) return launch_lm_nrt<6, 2, 4, 1>(p, s);
-  return launch_lm_nrt<kRT, 2, 4, 1>(p, s);
+  if (need <= 1) return launch_lm_nrt<1, 1, 1, 4, 8, 2>(p, s);
+  if (need <= 2) return launch_lm_nrt<2, 1, 1, 4, 8, 2>(p, s);
+  if (need <= 4) return launch_lm_nrt<4, 1, 1, 4, 8, 1>(p, s);
+  if (need <= 6) return launch_lm_nrt<3, 2, 2, 2, 4, 1>(p, s);
+  return launch_lm_nrt<kRT / 2, 2, 2, 2, 4, 1>(p, s);
 }
 
 }  // namespace spexis
