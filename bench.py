@@ -119,7 +119,7 @@ def main():
         ingest_traffic(*args.ingest_traffic, workload=args.workload, copy_bytes=args.copy_probe)
         return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+        print(f"bench.py runs on one GPU only: the library has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
 
