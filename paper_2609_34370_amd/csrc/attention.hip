@@ -106,34 +106,52 @@ void verify_attn_kernel(AttnParams p) {
   if (share >= p.nshares) return no_share();
 
   // ---- this wave's share [g0, g0 + cnt) of head h's tile stream
-  int per_lane = 0;
-  for (int base = 0; base < p.num_seqs; base += kWave)
-    if (base + lane < p.num_seqs) per_lane += seq_geo(p, p.qsl, p.seq_lens, base + lane).nt;
-  const int total = __builtin_amdgcn_readfirstlane(wave_sum_i32(per_lane));   // < 2^31 (host)
-  const int even = (total + p.nshares - 1) / p.nshares;
-  const int P = max(p.tiles_per_wave > 0 ? p.tiles_per_wave : kAttnMinTilesPerWave, even);
-  if ((int64_t)share * P >= total) return no_share();
-  const int g0 = share * P;
-  const int cnt = min(P, total - g0);
-  // the sequence holding tile g0, and the stream index of its first tile
-  int before = 0, b0 = 0, f0 = 0;
-  for (int base = 0; base < p.num_seqs; base += kWave) {
-    const int b = base + lane;
-    const int v = b < p.num_seqs ? seq_geo(p, p.qsl, p.seq_lens, b).nt : 0;
-    const int incl = wave_incl_scan_i32(v, lane);
-    const uint64_t hit = __builtin_amdgcn_ballot_w64(before + incl > g0);
-    if (hit != 0) {
-      const int l0 = __builtin_ctzll(hit);
-      b0 = base + l0;
-      f0 = before + __shfl(incl - v, l0, kWave);
-      break;
-    }
-    before += __shfl(incl, kWave - 1, kWave);
-  }
-  b0 = __builtin_amdgcn_readfirstlane(b0);
-  f0 = __builtin_amdgcn_readfirstlane(f0);
+  int total, b0 = 0, f0 = 0;
   Cursor start;
-  {
+  if (p.num_seqs <= kWave) {
+    // one pass: lane b holds sequence b's geometry; the share start is read from the lanes
+    const SeqGeo gl = lane < p.num_seqs ? seq_geo(p, p.qsl, p.seq_lens, lane) : SeqGeo{0, 0, 0, 0};
+    const int incl = wave_incl_scan_i32(gl.nt, lane);
+    total = __builtin_amdgcn_readlane(incl, kWave - 1);   // < 2^31 (host)
+    const int even = (total + p.nshares - 1) / p.nshares;
+    const int P = max(p.tiles_per_wave > 0 ? p.tiles_per_wave : kAttnMinTilesPerWave, even);
+    if ((int64_t)share * P >= total) return no_share();
+    const int g0 = share * P;
+    const uint64_t hit = __builtin_amdgcn_ballot_w64(incl > g0);
+    if (hit == 0) return no_share();
+    const int l0 = __builtin_ctzll(hit);
+    b0 = l0;
+    f0 = __builtin_amdgcn_readlane(incl - gl.nt, l0);
+    start.b = b0;
+    start.nt = __builtin_amdgcn_readlane(gl.nt, l0);
+    start.S = __builtin_amdgcn_readlane(gl.S, l0);
+    start.t = g0 - f0;
+  } else {
+    int per_lane = 0;
+    for (int base = 0; base < p.num_seqs; base += kWave)
+      if (base + lane < p.num_seqs) per_lane += seq_geo(p, p.qsl, p.seq_lens, base + lane).nt;
+    total = __builtin_amdgcn_readfirstlane(wave_sum_i32(per_lane));   // < 2^31 (host)
+    const int even = (total + p.nshares - 1) / p.nshares;
+    const int P = max(p.tiles_per_wave > 0 ? p.tiles_per_wave : kAttnMinTilesPerWave, even);
+    if ((int64_t)share * P >= total) return no_share();
+    const int g0 = share * P;
+    // the sequence holding tile g0, and the stream index of its first tile
+    int before = 0;
+    for (int base = 0; base < p.num_seqs; base += kWave) {
+      const int b = base + lane;
+      const int v = b < p.num_seqs ? seq_geo(p, p.qsl, p.seq_lens, b).nt : 0;
+      const int incl = wave_incl_scan_i32(v, lane);
+      const uint64_t hit = __builtin_amdgcn_ballot_w64(before + incl > g0);
+      if (hit != 0) {
+        const int l0 = __builtin_ctzll(hit);
+        b0 = base + l0;
+        f0 = before + __builtin_amdgcn_readlane(incl - v, l0);
+        break;
+      }
+      before += __builtin_amdgcn_readlane(incl, kWave - 1);
+    }
+    b0 = __builtin_amdgcn_readfirstlane(b0);
+    f0 = __builtin_amdgcn_readfirstlane(f0);
     const SeqGeo g = seq_geo(p, (sint32*)p.qsl, (sint32*)p.seq_lens, b0);
     if (g.nt == 0 || g0 < f0 || g0 - f0 >= g.nt) return no_share();   // inputs changed under us
     start.b = b0;
@@ -141,6 +159,10 @@ void verify_attn_kernel(AttnParams p) {
     start.S = g.S;
     start.t = g0 - f0;
   }
+  const int P = max(p.tiles_per_wave > 0 ? p.tiles_per_wave : kAttnMinTilesPerWave,
+                    (total + p.nshares - 1) / p.nshares);
+  const int g0 = share * P;
+  const int cnt = min(P, total - g0);
 
   const uint16_t* kc = reinterpret_cast<const uint16_t*>(p.k_cache);
   const uint16_t* vc = reinterpret_cast<const uint16_t*>(p.v_cache);
@@ -160,11 +182,10 @@ void verify_attn_kernel(AttnParams p) {
   // load side: the tile being issued (lc, its block ids) and the next one (nc), one step ahead
   Cursor lc = start, nc = start;
   int lidx = 0, la, lb, na = 0, nb = 0;
+  // both tiles' block ids fetched together (with one tile, the next cursor is the same one)
+  if (cnt > 1) advance(p, nc);
   tile_blocks(lc, la, lb);
-  if (cnt > 1) {
-    advance(p, nc);
-    tile_blocks(nc, na, nb);
-  }
+  tile_blocks(nc, na, nb);
 
   // Operand buffers; DEPTH rotate so that DEPTH-1 tiles are in flight while one is computed.
   // Loads are issued unconditionally -- past the share's end they re-read its last tile (an L2
