@@ -43,6 +43,7 @@ constexpr int kF4 = kWaveSub / (kWave * 4);      // float4 loads per lane (4)
 constexpr int kPerLane = 4 * kF4;                // vocab entries per lane (16)
 constexpr int kRoundGrid = 65536;                // workgroups of a later test round (256 per CU)
 constexpr int64_t kOneRoundBytes = 192ll << 20;  // target rows that one test round reads whole
+constexpr int64_t kRoundRowBytes = 256ll << 10;  // rows this long pay for the launches of a round
 
 enum Mode { kResidual = 1, kBonus = 2, kDone = 3 };
 
@@ -803,11 +804,13 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
   }
   if (p.kind == 1) {
     // Rounds of doubling width until position max_k is covered.  A round costs a few
-    // microseconds of launch and latency, a row 4V bytes: when all the target rows together
-    // stream in well under that many rounds' worth of time, one round reads every row;
-    // otherwise the first round is two positions wide ({0,1}, {2..5}, {6..13}, ...), since
-    // most sequences pass the first test at usual acceptance rates.
-    const bool one_round = (int64_t)p.B * (p.max_k + 1) * p.V * 4 <= kOneRoundBytes;
+    // microseconds of launch and latency, a row 4V bytes: with short rows (under 256 KB) that
+    // together stream in well under that many rounds' worth of time, one round reads every
+    // row; otherwise the first round is two positions wide ({0,1}, {2..5}, {6..13}, ...), since
+    // most sequences pass the first test at usual acceptance rates.  (Measured: rounds save
+    // 3.5 us at 64 sequences of 128256-entry rows, and cost 2.6 us at 128 of 32000.)
+    const bool one_round =
+        (int64_t)p.V * 4 < kRoundRowBytes && (int64_t)p.B * (p.max_k + 1) * p.V * 4 <= kOneRoundBytes;
     int width = one_round ? p.max_k + 1 : 2;
     for (int r = 0, lo = 0; lo <= p.max_k; ++r, lo += width, width *= 2) {
       const int hi = lo + width;
