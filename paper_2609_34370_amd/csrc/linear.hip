@@ -36,15 +36,22 @@ __global__ __launch_bounds__(kThreads) void linear_reduce_kernel(LinearParams p)
   if (e0 >= total) return;
   const int cnt = (int)min((int64_t)4, total - e0);
   float v[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < p.S; ++s) {
-    const float* src = p.part + (int64_t)s * total + e0;
-    if (cnt == 4 && ((e0 & 3) == 0)) {
-      const f32x4 x = *reinterpret_cast<const f32x4*>(src);
+  if (cnt == 4 && (total & 3) == 0) {   // 16-byte aligned in every partial
+    // the partials in groups of 8, every load of a group issued together, added in order
+    for (int s0 = 0; s0 < p.S; s0 += 8) {
+      f32x4 x[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] += x[i];
-    } else {
-      for (int i = 0; i < cnt; ++i) v[i] += src[i];
+      for (int u = 0; u < 8; ++u)
+        x[u] = *reinterpret_cast<const f32x4*>(p.part + (int64_t)min(s0 + u, p.S - 1) * total + e0);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (s0 + u < p.S)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[i] += x[u][i];
     }
+  } else {
+    for (int s = 0; s < p.S; ++s)
+      for (int i = 0; i < cnt; ++i) v[i] += p.part[(int64_t)s * total + e0 + i];
   }
   uint16_t* y = reinterpret_cast<uint16_t*>(p.y) + e0;
   const uint16_t* r = p.res ? reinterpret_cast<const uint16_t*>(p.res) + e0 : nullptr;
@@ -52,7 +59,7 @@ __global__ __launch_bounds__(kThreads) void linear_reduce_kernel(LinearParams p)
 }
 
 // K split for a problem (the same choice in the workspace query and the launch): the smallest
-// power of two that gives at least 256 workgroups, while K / S stays a multiple of 64 and the
+// power of two up to 8 that gives at least 256 workgroups, while K / S stays a multiple of 64 and the
 // partials (S M N fp32, written once and read once) stay within the weight's own traffic
 // (2 S M N 4 <= 2 N K 2, i.e. 2 S M <= K).
 int linear_split(int M, int N, int K) {
@@ -60,7 +67,7 @@ int linear_split(int M, int N, int K) {
   const int64_t mgroups = (M + rows_per_group - 1) / rows_per_group;
   const int64_t tiles = (N + kLmCols - 1) / kLmCols;
   int S = 1;
-  while (tiles * mgroups * S < 256 && K % (kLmK * 2 * S) == 0 && (int64_t)2 * (2 * S) * M <= K) S *= 2;
+  while (S < 8 && tiles * mgroups * S < 256 && K % (kLmK * 2 * S) == 0 && (int64_t)2 * (2 * S) * M <= K) S *= 2;
   return S;
 }
 
