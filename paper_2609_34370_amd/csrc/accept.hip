@@ -433,28 +433,39 @@ __global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p, 
   }
 }
 
-// Given per-tile statistics of `rows` rows reduced to one (max, sum) per row, in the order
-// row_stats uses (so a consumer of the reduced row gets the same M and 1/Z), one wave per row.
+// Given per-tile statistics of `rows` rows reduced to one (max, sum) per row, one wave per row:
+// M = max over the tiles, then Z = sum of z * 2^(m - M) (lane-strided partial sums, combined
+// across the wave in a fixed order; every consumer reads the reduced pair).  Each lane's tiles
+// are loaded 8 at a time, the loads of a group issued together.
 __global__ __launch_bounds__(kThreads) void accept_combine_kernel(const float* src, int parts, int rows,
                                                                   float* dst) {
+  constexpr int kG = 8;
   const int lane = threadIdx.x % kWave;
   const int row = blockIdx.x * kWaves + threadIdx.x / kWave;
   if (row >= rows) return;
-  const float* part = src + (int64_t)row * parts * 2;
-  const Part2 f = part_first(part, parts, lane, -INFINITY, 0.f);
-  float mm = f.a;
-  for (int x = lane + kWave; x < parts; x += kWave) mm = fmaxf(mm, part[2 * x]);
+  const f32x2* part = reinterpret_cast<const f32x2*>(src + (int64_t)row * parts * 2);
+  float mm = -INFINITY;
+  for (int x0 = lane; x0 < parts; x0 += kG * kWave) {
+    f32x2 v[kG];
+#pragma unroll
+    for (int u = 0; u < kG; ++u) v[u] = part[min(x0 + u * kWave, parts - 1)];
+#pragma unroll
+    for (int u = 0; u < kG; ++u)
+      if (x0 + u * kWave < parts) mm = fmaxf(mm, v[u][0]);
+  }
   mm = wave_max(mm);
   float zz = 0.f;
   int nan = 0;
-  if (lane < parts) {
-    nan |= f.b != f.b;
-    if (f.a != -INFINITY) zz += f.b * fast_exp2(f.a - mm);
-  }
-  for (int x = lane + kWave; x < parts; x += kWave) {
-    const float z = part[2 * x + 1];
-    nan |= z != z;
-    if (part[2 * x] != -INFINITY) zz += z * fast_exp2(part[2 * x] - mm);
+  for (int x0 = lane; x0 < parts; x0 += kG * kWave) {
+    f32x2 v[kG];
+#pragma unroll
+    for (int u = 0; u < kG; ++u) v[u] = part[min(x0 + u * kWave, parts - 1)];
+#pragma unroll
+    for (int u = 0; u < kG; ++u) {
+      if (x0 + u * kWave >= parts) continue;
+      nan |= v[u][1] != v[u][1];
+      if (v[u][0] != -INFINITY) zz += v[u][1] * fast_exp2(v[u][0] - mm);
+    }
   }
   zz = wave_sum(zz);
   nan = wave_or(nan);
