@@ -315,6 +315,9 @@ def bench_lm_head(args):
     print(json.dumps(line), flush=True)
 
 
+PIPE_STAGES = 4   # pipeline stages of the Eq. 3-4 model in the select component
+
+
 def bench_select(args):
     """Selective speculation at the workload's batch: latency of spexis_select_drafts, and the
     speculation accuracy of the drafts it keeps.  Confidences are the draft probabilities of the
@@ -324,6 +327,7 @@ def bench_select(args):
     drafts: Theta_alpha = sum_b min(a_b, kept_k_b) / sum_b kept_k_b against Theta = sum a_b / sum k_b."""
     import torch
 
+    from paper_2609_34370_amd import schedule
     from paper_2609_34370_amd import spexis as sx
     from paper_2609_34370_amd import workloads as wl
     from paper_2609_34370_amd.step import VerifyStep
@@ -361,11 +365,18 @@ def bench_select(args):
         us = timed(lambda: sx.spexis_select_drafts(step.qsl, conf, alpha, kept_k, kept_qsl, keep[:N]))
         kk = kept_k.cpu().numpy().astype(np.int64)
         theta_a = float(np.minimum(a, kk).sum() / max(kk.sum(), 1))
+        # Eq. 3-4 with the measured accuracies, for a 4-stage pipeline and this batch
+        b_eff0 = schedule.effective_batch(B, 0.0, PIPE_STAGES, theta)
+        b_eff = schedule.effective_batch(B, alpha, PIPE_STAGES, theta_a)
         rows.append({"alpha": alpha, "us": round(us, 2), "kept_drafts": int(kk.sum()), "drafts": int(N),
                      "theta": round(theta, 4), "theta_alpha": round(theta_a, 4),
-                     "accepted_kept": int(np.minimum(a, kk).sum()), "accepted_all": int(np.minimum(a, k).sum())})
+                     "accepted_kept": int(np.minimum(a, kk).sum()), "accepted_all": int(np.minimum(a, k).sum()),
+                     "pipeline_stages": PIPE_STAGES,
+                     "steady_batch": round(schedule.steady_batch(B, alpha, PIPE_STAGES), 2),
+                     "effective_batch": round(b_eff, 2), "effective_batch_no_drop": round(b_eff0, 2)})
         log(f"[select] alpha={alpha}: {us:.1f} us; kept {kk.sum()}/{N} drafts; theta {theta:.4f} -> "
-            f"theta_alpha {theta_a:.4f}; accepted {np.minimum(a, kk).sum()}/{np.minimum(a, k).sum()}")
+            f"theta_alpha {theta_a:.4f}; accepted {np.minimum(a, kk).sum()}/{np.minimum(a, k).sum()}; "
+            f"Eq. 4 effective batch {b_eff0:.1f} -> {b_eff:.1f} (N={PIPE_STAGES})")
     # the largest supported batch: 1024 sequences x 16 drafts
     qsl_max = torch.arange(0, 17 * 1025, 17, dtype=torch.int32, device="cuda")
     conf_max = torch.rand(16384, generator=torch.Generator(device="cuda").manual_seed(1), device="cuda")

@@ -221,6 +221,17 @@ def draft_step(h, w_in, w_q, w_k, w_v, w_o, w_lm, k_pool, v_pool, num_blocks, nu
     return dict(x=x, q=q, k=k, v=v, o=o, y=y, logits=logits, probs=p, tokens=tok, conf=conf, status=status)
 
 
+def batch_recurrence(B: float, alpha: float, N: int, steps: int = 20000) -> float:
+    """B_t of the selective-speculation recurrence B_{t+1} = alpha B_{t+1-N} + (1 - alpha) B_t
+    (Sec. 5, Eq. 3) iterated from B_0 = B with no earlier history (B_t = 0 for t < 0)."""
+    hist = [0.0] * (N - 1) + [float(B)]   # B_{t-N+1} .. B_t
+    for _ in range(steps):
+        nxt = alpha * hist[-N] + (1.0 - alpha) * hist[-1] if N > 1 else hist[-1]
+        hist.append(nxt)
+        hist.pop(0)
+    return hist[-1]
+
+
 def lookahead(cur_len, remaining, precision, pp: int, theta: float, iters: int = 64):
     """Algorithm 1: (mem, e_gen, e_nfin, e_lfin), each fp64 [iters], for the running requests'
     current lengths, predicted remaining lengths and prediction precisions."""
