@@ -75,7 +75,7 @@ extern "C" {
 
 /* row_status codes written by spexis_accept */
 #define SPEXIS_ROW_OK 0
-#define SPEXIS_ROW_EMPTY 1      /* the sampled row had no positive weight, even after fallback */
+#define SPEXIS_ROW_EMPTY 1      /* the sampled target row had no positive entry */
 #define SPEXIS_ROW_BAD_VALUE 2  /* the sampled row held a NaN, an infinity or a negative value */
 #define SPEXIS_ROW_BAD_TOKEN 3  /* a draft token id outside [0, vocab) */
 
@@ -186,13 +186,14 @@ size_t spexis_accept_workspace_size(int32_t num_seqs, int32_t vocab, int32_t max
  *   2. draft i is accepted iff (double)u_accept[qsl[b]-b+i] * (double)q_i(x_i)
  *      < (double)p_i(x_i), an exact comparison equal to u < min(1, p/q) for u in [0,1);
  *      a_b = number of leading accepts.
- *   3. a_b < k_b: weights w = max(0, fp32(p_a - q_a)), falling back to w = p_a if all are
- *      zero; a_b = k_b: w = p_k (bonus).  Rows read here must be finite and >= 0, else
- *      row_status = BAD_VALUE and the token at position a_b is -1.
+ *   3. a_b < k_b: weights w = max(0, fp32(p_a - q_a)); a_b = k_b: w = p_k (bonus).  Rows
+ *      read here must be finite and >= 0, else row_status = BAD_VALUE and the token at
+ *      position a_b is -1.
  *   4. the token at position a_b is the inverse-CDF sample of w with u_sample[b], taken in
- *      exact fixed point: M = max w in [2^e, 2^(e+1)), W_v = floor(w_v * 2^(40-e)),
- *      S = sum W_v, t = floor(u_sample[b] * S) (exact), token = smallest m with
- *      W_0 + ... + W_m > t.  No positive weight: row_status = EMPTY, token -1.
+ *      exact fixed point at the scale of the target row: M = max p_a in [2^e, 2^(e+1)),
+ *      W_v = floor(w_v * 2^(40-e)), S = sum W_v (if S = 0 for a residual, the weights are
+ *      p_a's instead), t = floor(u_sample[b] * S) (exact), token = smallest m with
+ *      W_0 + ... + W_m > t.  p_a without a positive entry: row_status = EMPTY, token -1.
  * Outputs: accepted_len[b] = a_b; out_tokens[b][0..a_b) = x_0..x_{a_b-1};
  *   out_tokens[b][a_b] = the sampled token; out_tokens[b][i > a_b] = -1 (out_tokens is
  *   [B][max_k+1] int32); row_status[b]; if seq_lens_inout != NULL,

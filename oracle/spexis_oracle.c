@@ -338,29 +338,37 @@ static uint64_t exact_threshold(float u, uint64_t S) {
 }
 
 /*
- * Inverse-CDF sample of the fp32 weight row w[0..V) with the uniform u, in fixed point:
- *   M = max w; e such that M in [2^e, 2^(e+1)); s = 40 - e;
+ * Inverse-CDF sample in fixed point.  The scale is that of the target row p: M = max p, and
+ * e such that M in [2^e, 2^(e+1)); s = 40 - e.  For the weight row w (w <= p entrywise):
  *   W_v = floor(w_v * 2^s)  (exact: a power-of-two scaling of an fp32 value, then floor);
- *   S = sum W_v;  t = floor(u * S) exactly;
+ *   S = sum W_v; if S == 0 and a fallback row is given, the weights become the fallback's;
+ *   t = floor(u * S) exactly;
  *   token = the smallest m with W_0 + ... + W_m > t.
- * Returns -1 if M == 0.
+ * Returns -1 if M == 0 (then every weight is 0).
  */
-static int32_t sample_fixed_point(const float* w, int32_t V, float u) {
-  float M = 0.0f;
-  for (int32_t v = 0; v < V; ++v) if (w[v] > M) M = w[v];
+static uint64_t fixed_sum(const float* w, int32_t V, int s) {
+  uint64_t S = 0;
+  for (int32_t v = 0; v < V; ++v) S += (uint64_t)floor(ldexp((double)w[v], s));
+  return S;
+}
+
+static int32_t sample_fixed_point(const float* w, const float* fallback, int32_t V, float M, float u) {
   if (M == 0.0f) return -1;
   int E;
   frexp((double)M, &E); /* M = f * 2^E, f in [0.5,1)  =>  M in [2^(E-1), 2^E) */
   int s = 40 - (E - 1);
-  uint64_t S = 0;
-  for (int32_t v = 0; v < V; ++v) S += (uint64_t)floor(ldexp((double)w[v], s));
+  uint64_t S = fixed_sum(w, V, s);
+  if (S == 0 && fallback) {
+    w = fallback;
+    S = fixed_sum(w, V, s);
+  }
   uint64_t t = exact_threshold(u, S);
   uint64_t prefix = 0;
   for (int32_t v = 0; v < V; ++v) {
     prefix += (uint64_t)floor(ldexp((double)w[v], s));
     if (prefix > t) return v;
   }
-  return V - 1; /* unreachable: prefix reaches S > t */
+  return V - 1; /* unreachable: prefix reaches S > t (S >= 2^40 once the weights are p's) */
 }
 
 /*
@@ -373,10 +381,11 @@ static int32_t sample_fixed_point(const float* w, int32_t V, float u) {
  *   2. for i = 0..k_b-1: accept iff (double)u_i * (double)q_i(x_i) < (double)p_i(x_i)
  *      (exact: a product of two fp32 values is exact in fp64, so this is u < p/q, i.e. the
  *      test u < min(1, p/q) for u in [0,1)); a_b = the number of leading accepts.
- *   3. a_b < k_b: weights w_v = max(0, fp32(p_a(v) - q_a(v))); if every w_v is 0, fall
- *      back to w = p_a.  a_b = k_b: w = p_k (bonus token).
+ *   3. a_b < k_b: weights w_v = max(0, fp32(p_a(v) - q_a(v))), with p_a as the fallback when
+ *      every fixed-point weight is 0.  a_b = k_b: w = p_k (bonus token).
  *      The row(s) read here must be finite and non-negative, else status 2.
- *   4. token = sample_fixed_point(w, u_sample[b]); if no weight is positive, status 1.
+ *   4. token = sample_fixed_point(w, fallback, max p_a, u_sample[b]) (the scale of the target
+ *      row); if p_a has no positive entry, status 1.
  *   Outputs: accepted_len[b] = a_b; out_tokens[b][0..a_b) = x_0..x_{a_b-1};
  *   out_tokens[b][a_b] = token (-1 on status 1/2); later positions -1.
  *   If seq_lens_inout is not NULL, seq_lens_inout[b] = S_b - k_b + a_b (the rows of
@@ -423,18 +432,17 @@ void oracle_accept(int32_t B, int32_t V, int32_t max_k, const int32_t* qsl, cons
     if (bad) { row_status[b] = ORACLE_BAD_ROW; continue; }
 
     float* w = (float*)malloc(sizeof(float) * (size_t)V);
-    int any = 0;
+    float M = 0.0f;
     for (int32_t v = 0; v < V; ++v) {
+      if (P[v] > M) M = P[v];
       if (Q) {
         float diff = P[v] - Q[v]; /* one IEEE fp32 subtraction, round to nearest */
         w[v] = diff > 0.0f ? diff : 0.0f;
       } else {
         w[v] = P[v];
       }
-      if (w[v] > 0.0f) any = 1;
     }
-    if (!any && Q) for (int32_t v = 0; v < V; ++v) w[v] = P[v];
-    int32_t token = sample_fixed_point(w, V, u_sample[b]);
+    int32_t token = sample_fixed_point(w, Q ? P : NULL, V, M, u_sample[b]);
     free(w);
     if (token < 0) row_status[b] = ORACLE_EMPTY_ROW;
     tok[a] = token;

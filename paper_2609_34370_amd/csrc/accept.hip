@@ -4,7 +4,8 @@
 //
 // Every decision is taken in exact arithmetic, so any reduction order gives the same integers:
 //   test      (double)u * (double)q(x) < (double)p(x)   (a product of two fp32 is exact)
-//   weights   W_v = floor(w_v * 2^(40-e)), e = floor(log2 max w)   (integer bit shifts)
+//   weights   W_v = floor(w_v * 2^(40-e)), e = floor(log2 max p)   (integer bit shifts; the scale
+//             is the target row's, so with logits it is known from the row statistics)
 //   threshold t = floor(u * sum W) from a 128-bit product
 //   token     the smallest m whose inclusive prefix of W exceeds t
 //
@@ -21,11 +22,12 @@
 //             independent of each other, so nothing here waits for a decision.
 //     decide  one work item per (sequence, sub-chunk): every item of a sequence runs the
 //             round's tests from those statistics (its waves split the positions) and reaches
-//             the same first failure a; then it computes the residual maxima of row a over
-//             its sub-chunk, or marks the bonus row, or puts the sequence on the next list.
+//             the same first failure a; then it computes the fixed-point sums of the residual
+//             of row a (or of the bonus row) over its sub-chunk, or puts the sequence on the
+//             next list.
 //   init      (probability inputs) one thread per sequence: geometry, draft-id check, tests.
-//   max pass  (probability inputs) per sub-chunk: max of the weights, max of p, bad flag.
-//   sum pass  per sub-chunk: sum of W_v.
+//   max pass  (probability inputs) per sub-chunk: max of p, bad flag.
+//   sum pass  (probability inputs) per sub-chunk: the sums of W_v.
 //   search    one workgroup per sequence: total, exact threshold, the sub-chunk holding it,
 //             the token inside that sub-chunk (its four waves split the entries), outputs.
 #include <math.h>
@@ -260,55 +262,107 @@ __device__ __forceinline__ T wg_combine(T v, int wave, int lane, F op) {
   return r;
 }
 
-// Residual / bonus maxima of sub-chunk `sub` by one workgroup, written to max_part / bad_part.
+// Probability inputs: the largest target probability over sub-chunk `sub` of the sampled row,
+// and whether the sampled row(s) hold a NaN, an infinity or a negative value there, written to
+// max_part / bad_part by one workgroup.
 __device__ void sub_maxima(const AcceptParams& p, const RowCtx& r, bool residual, int b, int sub, int wave, int lane) {
   const bool vec = (p.V & 3) == 0;
-  const float fill = r.logits ? -INFINITY : 0.f;
   float pv[kPerLane], qv[kPerLane];
-  load_sub(r.P, sub, wave, p.V, vec, fill, lane, pv);
-  if (residual) load_sub(r.Q, sub, wave, p.V, vec, fill, lane, qv);
-  float mw = 0.f, mp = 0.f;
+  load_sub(r.P, sub, wave, p.V, vec, 0.f, lane, pv);
+  if (residual) load_sub(r.Q, sub, wave, p.V, vec, 0.f, lane, qv);
+  float mp = 0.f;
   int bad = 0;
 #pragma unroll
   for (int e = 0; e < kPerLane; ++e) {
-    const float P = prob_of(r, pv[e], p.c, false);
-    const float Q = residual ? prob_of(r, qv[e], p.c, true) : 0.f;
-    bad |= bad_value(P) || (residual && bad_value(Q));
-    const float d = P - Q;
-    const float w = residual ? (d > 0.f ? d : 0.f) : P;
-    mw = w > mw ? w : mw;
-    mp = P > mp ? P : mp;
+    bad |= bad_value(pv[e]) || (residual && bad_value(qv[e]));
+    mp = pv[e] > mp ? pv[e] : mp;
   }
-  mw = wg_combine(wave_max(mw), wave, lane, [](float x, float y) { return fmaxf(x, y); });
   mp = wg_combine(wave_max(mp), wave, lane, [](float x, float y) { return fmaxf(x, y); });
   bad = wg_combine(wave_or(bad), wave, lane, [](int x, int y) { return x | y; });
   if (threadIdx.x == 0) {
-    *reinterpret_cast<f32x2*>(p.max_part + ((int64_t)b * p.nsub + sub) * 2) = f32x2{mw, mp};
+    p.max_part[(int64_t)b * p.nsub + sub] = mp;
     p.bad_part[(int64_t)b * p.nsub + sub] = bad;
   }
 }
 
-// Row maxima and bad flag of the sampled row (one wave; any reduction order gives the same).
-// Logit bonus rows have no max pass: their largest probability is 2^0 * (1/Z).
-__device__ __forceinline__ void sampled_maxima(const AcceptParams& p, const RowCtx& r, int b, bool residual, int lane,
-                                               float& MW, float& MP, int& bad) {
-  if (r.logits && !residual) {
-    MP = MW = r.Rp;   // 2^0 * (1/Z)
-    bad = !(MP > 0.f) || isinf(MP);
+// The scale of the sampled row, M = the largest probability of target row a (with logits
+// 2^0 * (1/Z), from its statistics), and whether a row the sampling reads holds a NaN, an
+// infinity or a negative value (with logits: a row whose statistics are not finite).  One
+// full wave; every consumer gets the same values.
+__device__ __forceinline__ void sampled_scale(const AcceptParams& p, const RowCtx& r, int b, bool residual, int lane,
+                                              float& M, int& bad) {
+  if (r.logits) {
+    M = r.Rp;
+    bad = !(r.Rp > 0.f) || isinf(r.Rp) || (residual && (!(r.Rq > 0.f) || isinf(r.Rq)));
     return;
   }
-  MW = 0.f;
-  MP = 0.f;
+  M = 0.f;
   bad = 0;
   for (int x = lane; x < p.nsub; x += kWave) {
-    const f32x2 v = *reinterpret_cast<const f32x2*>(p.max_part + ((int64_t)b * p.nsub + x) * 2);
-    MW = fmaxf(MW, v[0]);
-    MP = fmaxf(MP, v[1]);
+    M = fmaxf(M, p.max_part[(int64_t)b * p.nsub + x]);
     bad |= p.bad_part[(int64_t)b * p.nsub + x];
   }
-  MW = wave_max(MW);
-  MP = wave_max(MP);
+  M = wave_max(M);
   bad = wave_or(bad);
+}
+
+// Fixed-point weight of one entry: of p (use_p) or of the residual max(0, p - q).  The sums and
+// the search evaluate exactly this expression.
+__device__ __forceinline__ uint64_t entry_weight(const RowCtx& r, float c, float pv_raw, float qv_raw, bool use_p,
+                                                 int s) {
+  const float P = prob_of(r, pv_raw, c, false);
+  float w;
+  if (use_p) {
+    w = P;
+  } else {
+    const float d = P - prob_of(r, qv_raw, c, true);
+    w = d > 0.f ? d : 0.f;
+  }
+  return fixed_weight(w, s);
+}
+
+// Fixed-point sums over sub-chunk `sub` of the sampled row at shift s, by one workgroup: the
+// residual weights (0 for a bonus row) and the weights of p (the fallback of an empty
+// residual), written to sum_part[b][sub][0..1].  pv / qv hold the sub-chunk's entries.
+__device__ void sub_sums(const AcceptParams& p, const RowCtx& r, bool residual, int b, int sub, int s, int wave,
+                         int lane, const float (&pv)[kPerLane], const float (&qv)[kPerLane]) {
+  uint64_t sr = 0, sp = 0;
+#pragma unroll
+  for (int e = 0; e < kPerLane; ++e) {
+    sp += entry_weight(r, p.c, pv[e], 0.f, true, s);
+    if (residual) sr += entry_weight(r, p.c, pv[e], qv[e], false, s);
+  }
+  const auto add = [](uint64_t x, uint64_t y) { return x + y; };
+  sr = wg_combine(wave_sum_u64(sr), wave, lane, add);
+  sp = wg_combine(wave_sum_u64(sp), wave, lane, add);
+  if (threadIdx.x == 0) {
+    uint64_t* dst = p.sum_part + ((int64_t)b * p.nsub + sub) * 2;
+    dst[0] = sr;
+    dst[1] = sp;
+  }
+}
+
+// The sampled row(s) of sequence b at position a over sub-chunk `sub`: entries, statistics,
+// scale, then the fixed-point sums (a bad or empty row writes none; the search reports it).
+__device__ void sample_sums(const AcceptParams& p, int b, const Geom& g, int a, bool residual, int sub, int wave,
+                            int lane) {
+  const bool vec = (p.V & 3) == 0;
+  const float fill = p.kind == 1 ? -INFINITY : 0.f;
+  // the entries first: their loads overlap the reductions of the row statistics and maxima
+  float pv[kPerLane], qv[kPerLane];
+  load_sub(p.target + (int64_t)(g.t0 + a) * p.V, sub, wave, p.V, vec, fill, lane, pv);
+  if (residual) {
+    load_sub(p.draft + (int64_t)(g.d0 + a) * p.V, sub, wave, p.V, vec, fill, lane, qv);
+  } else {
+#pragma unroll
+    for (int e = 0; e < kPerLane; ++e) qv[e] = 0.f;
+  }
+  const RowCtx r = row_ctx(p, b, g, a, residual, lane);
+  float M;
+  int bad;
+  sampled_scale(p, r, b, residual, lane, M, bad);
+  if (bad || !(M > 0.f)) return;   // the same decision in every wave
+  sub_sums(p, r, residual, b, sub, 40 - floor_log2(M), wave, lane, pv, qv);
 }
 
 // ---------------------------------------------------------------------------------- init
@@ -493,8 +547,9 @@ __global__ __launch_bounds__(kThreads) void accept_gather_kernel(AcceptParams p)
 // Round r, positions [lo, hi): one work item per (sequence of the list, sub-chunk).  Every item
 // of a sequence runs the tests at those positions (its waves split them) and reaches the same
 // first failure.  A failure at a: the sequence is done testing (residual at a), and the item
-// computes the residual maxima of row a over its sub-chunk.  No failure: the bonus row if the
-// round reached position k, else the sequence joins round r+1's list.
+// computes the fixed-point sums of the residual of row a over its sub-chunk.  No failure: the
+// same for the bonus row if the round reached position k, else the sequence joins round r+1's
+// list.
 __global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p, int r, int lo, int hi) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int64_t total = (int64_t)round_count(p, r) * p.nsub;
@@ -534,21 +589,17 @@ __global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p,
     __syncthreads();
     const int a = min(min(sm_fail[0], sm_fail[1]), min(sm_fail[2], sm_fail[3]));
     __syncthreads();
-    if (a < g.k) {
+    if (a < g.k || hi > g.k) {
+      // a failure at a: the residual of row a; every test passed and the round reached k: the
+      // bonus row k.  Either way the scale is known from row a's statistics, so the sums follow.
+      const bool residual = a < g.k;
+      const int at = residual ? a : g.k;
       if (lead) {
         *reinterpret_cast<u32x4*>(p.geo + 4 * (int64_t)b) = u32x4{(uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k, 1u};
-        p.st_a[b] = a;
-        p.st_mode[b] = kResidual;
+        p.st_a[b] = at;
+        p.st_mode[b] = residual ? kResidual : kBonus;
       }
-      // the residual needs the maxima of w = max(0, p_a - q_a)
-      sub_maxima(p, row_ctx(p, b, g, a, true, lane), true, b, sub, wave, lane);
-    } else if (hi > g.k) {
-      // every test passed: the bonus row k, whose largest probability is known from its statistics
-      if (lead) {
-        *reinterpret_cast<u32x4*>(p.geo + 4 * (int64_t)b) = u32x4{(uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k, 1u};
-        p.st_a[b] = g.k;
-        p.st_mode[b] = kBonus;
-      }
+      sample_sums(p, b, g, at, residual, sub, wave, lane);
     } else if (lead) {
       const int at = __hip_atomic_fetch_add(p.counts + r + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       *reinterpret_cast<u32x4*>(p.lists + ((int64_t)r * p.B + at) * 4) =
@@ -570,20 +621,7 @@ __global__ __launch_bounds__(kThreads) void accept_max_kernel(AcceptParams p) {
   sub_maxima(p, row_ctx(p, b, g, a, residual, lane), residual, b, sub, wave, lane);
 }
 
-// ------------------------------------------------------------------------------ sum pass
-
-__device__ __forceinline__ uint64_t entry_weight(const RowCtx& r, float c, float pv_raw, float qv_raw, bool use_p,
-                                                 int s) {
-  const float P = prob_of(r, pv_raw, c, false);
-  float w;
-  if (use_p) {
-    w = P;
-  } else {
-    const float d = P - prob_of(r, qv_raw, c, true);
-    w = d > 0.f ? d : 0.f;
-  }
-  return fixed_weight(w, s);
-}
+// ------------------------------------------------------------------- probability sum pass
 
 __global__ __launch_bounds__(kThreads) void accept_sum_kernel(AcceptParams p) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -592,26 +630,7 @@ __global__ __launch_bounds__(kThreads) void accept_sum_kernel(AcceptParams p) {
   const int a = p.st_a[b];
   const Geom g = load_geom(p, b);
   if (mode != kResidual && mode != kBonus) return;
-  const bool residual = mode == kResidual;
-  const bool vec = (p.V & 3) == 0;
-  const float fill = p.kind == 1 ? -INFINITY : 0.f;
-  // the entries first: their loads overlap the reductions of the row statistics and maxima
-  float pv[kPerLane], qv[kPerLane];
-  load_sub(p.target + (int64_t)(g.t0 + a) * p.V, sub, wave, p.V, vec, fill, lane, pv);
-  if (residual) load_sub(p.draft + (int64_t)(g.d0 + a) * p.V, sub, wave, p.V, vec, fill, lane, qv);
-  const RowCtx r = row_ctx(p, b, g, a, residual, lane);
-  float MW, MP;
-  int bad;
-  sampled_maxima(p, r, b, residual, lane, MW, MP, bad);
-  const bool use_p = !residual || MW == 0.f;   // empty residual: fall back to p_a
-  const float M = use_p ? MP : MW;
-  if (bad || !(M > 0.f)) return;                // the search kernel writes these outputs
-  const int s = 40 - floor_log2(M);
-  uint64_t sum = 0;
-#pragma unroll
-  for (int e = 0; e < kPerLane; ++e) sum += entry_weight(r, p.c, pv[e], use_p ? 0.f : qv[e], use_p, s);
-  sum = wg_combine(wave_sum_u64(sum), wave, lane, [](uint64_t x, uint64_t y) { return x + y; });
-  if (threadIdx.x == 0) p.sum_part[(int64_t)b * p.nsub + sub] = sum;
+  sample_sums(p, b, g, a, mode == kResidual, sub, wave, lane);
 }
 
 // -------------------------------------------------------------------------------- search
@@ -626,22 +645,24 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
   const bool residual = mode == kResidual;
   // every wave takes the same decisions from the same partials
   const RowCtx r = row_ctx(p, b, g, a, residual, lane);
-  float MW, MP;
+  float M;
   int bad;
-  sampled_maxima(p, r, b, residual, lane, MW, MP, bad);
-  // the sub-chunk sums, prefetched while the maxima reduce (lanes own contiguous ranges)
-  const uint64_t* sums = p.sum_part + (int64_t)b * p.nsub;
+  sampled_scale(p, r, b, residual, lane, M, bad);
+  // the sub-chunk sums (residual, fallback), prefetched while the scale reduces (lanes own
+  // contiguous ranges)
+  const uint64_t* sums = p.sum_part + (int64_t)b * p.nsub * 2;
   const int per = (p.nsub + kWave - 1) / kWave;
   const int c_lo = min(p.nsub, lane * per), c_hi = min(p.nsub, c_lo + per);
-  uint64_t own = 0;
-  for (int x = c_lo; x < c_hi; ++x) own += sums[x];
+  uint64_t own_r = 0, own_p = 0;
+  for (int x = c_lo; x < c_hi; ++x) {
+    own_r += sums[2 * x];
+    own_p += sums[2 * x + 1];
+  }
   const bool lead = threadIdx.x == 0;
   if (bad) {
     if (lead) write_outputs(p, b, g, a, -1, SPEXIS_ROW_BAD_VALUE);
     return;
   }
-  const bool use_p = !residual || MW == 0.f;
-  const float M = use_p ? MP : MW;
   if (!(M > 0.f)) {
     if (lead) write_outputs(p, b, g, a, -1, SPEXIS_ROW_EMPTY);
     return;
@@ -649,6 +670,10 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
   const int s = 40 - floor_log2(M);
   const bool vec = (p.V & 3) == 0;
   const float fill = r.logits ? -INFINITY : 0.f;
+  // a residual whose fixed-point weights are all 0 falls back to p
+  const bool use_p = !residual || wave_sum_u64(own_r) == 0;
+  const int which = use_p ? 1 : 0;
+  const uint64_t own = use_p ? own_p : own_r;
 
   // total and exact threshold; the sub-chunk holding t
   const uint64_t incl = wave_incl_scan_u64(own);
@@ -659,19 +684,19 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
   uint64_t tt = 0;
   if (excl <= t && t < incl) {                        // exactly one lane holds t
     for (int x = c_lo; x < c_hi; ++x) {
-      if (t < excl + sums[x]) {
+      if (t < excl + sums[2 * x + which]) {
         cstar = x;
         tt = t - excl;
         break;
       }
-      excl += sums[x];
+      excl += sums[2 * x + which];
     }
   }
   const uint64_t found = __ballot(cstar >= 0);
   const int src = __builtin_amdgcn_readfirstlane(found ? __ffsll((unsigned long long)found) - 1 : 0);
   cstar = __builtin_amdgcn_readlane(cstar, src);
   tt = readlane_u64(tt, src);
-  if (cstar < 0) return;   // unreachable: S > 0 because M > 0 gives a weight >= 2^40
+  if (cstar < 0) return;   // unreachable: S > 0 (p's largest entry alone weighs >= 2^40)
   // wave w owns entries cstar*4096 + 1024 w .. + 1023 of the sub-chunk, lane l 16 of them, in order
   constexpr int kRun = kAcceptSub / (kWaves * kWave);   // 16
   const int base = cstar * kAcceptSub + kRun * (kWave * wave + lane);
@@ -771,12 +796,7 @@ hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V
   return hipGetLastError();
 }
 
-// The sampling passes every mode ends with: fixed-point sums, then the search.
-static hipError_t launch_sampling(const AcceptParams& p, hipStream_t s) {
-  const unsigned items = (unsigned)((int64_t)p.B * p.nsub);
-  hipLaunchKernelGGL(accept_sum_kernel, dim3(items), dim3(kThreads), 0, s, p);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+static hipError_t launch_search(const AcceptParams& p, hipStream_t s) {
   hipLaunchKernelGGL(accept_search_kernel, dim3(p.B), dim3(kThreads), 0, s, p);
   return hipGetLastError();
 }
@@ -811,7 +831,7 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
     }
     hipLaunchKernelGGL(accept_decide_kernel, dim3(items), dim3(kThreads), 0, s, q, 0, 0, q.max_k + 1);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    return launch_sampling(q, s);
+    return launch_search(q, s);
   }
   if (p.kind == 1) {
     // Rounds of doubling width until position max_k is covered.  A round costs a few
@@ -840,8 +860,10 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(accept_max_kernel, dim3(items), dim3(kThreads), 0, s, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(accept_sum_kernel, dim3(items), dim3(kThreads), 0, s, p);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  return launch_sampling(p, s);
+  return launch_search(p, s);
 }
 
 }  // namespace spexis

@@ -86,9 +86,9 @@ AcceptLayout accept_layout(int64_t B, int64_t V, int64_t max_k) {
   l.lists = take(spexis::kAcceptMaxRounds * B * 4 * 4);
   l.lse = take(B * (max_k + 1) * 2 * ns * 2 * 4);
   l.tin = take(B * (max_k > 0 ? max_k : 1) * 4 * 4);
-  l.max_part = take(B * ns * 2 * 4);
+  l.max_part = take(B * ns * 4);
   l.bad_part = take(B * ns * 4);
-  l.sum_part = take(B * ns * 8);
+  l.sum_part = take(B * ns * 2 * 8);
   l.total = off;
   return l;
 }

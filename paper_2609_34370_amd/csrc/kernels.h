@@ -127,9 +127,9 @@ struct AcceptParams {
   int ext_parts;             // 2^(y*c - max) per column tile); null / 0: computed here
   float* tin;            // [B][max_k][4] test inputs of position i: target and draft logit of x_i,
                          // u_i, and 1 if x_i is a valid id (logits mode; gathered by the stats pass)
-  float* max_part;       // [B][nsub][2] (max w, max p) of the sampled row(s)
-  int32_t* bad_part;     // [B][nsub]
-  uint64_t* sum_part;    // [B][nsub]
+  float* max_part;       // [B][nsub] max of the sampled target row (probability inputs)
+  int32_t* bad_part;     // [B][nsub] the sampled row(s) hold a bad value (probability inputs)
+  uint64_t* sum_part;    // [B][nsub][2] fixed-point sums of the residual and of p
 };
 
 constexpr int kAcceptMaxRounds = 8;  // test rounds: widths 2, 4, 8, ... cover max_k <= 509

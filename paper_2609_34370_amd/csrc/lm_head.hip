@@ -66,8 +66,8 @@ void lm_head_kernel(LmParams p) {
   const int mg = local % p.mgroups;
   const int nt = (local / p.mgroups) * 8 + xcd;
   if (nt >= p.ntiles) return;
-  const int m0 = mg * kLmRows, n0 = nt * kLmCols;
-  const int rows = min(kLmRows, p.M - m0);
+  const int m0 = mg * 32 * NRT, n0 = nt * kLmCols;
+  const int rows = min(32 * NRT, p.M - m0);
   // K split: workgroup row ks takes K values ks * klen .. +klen-1 (nsteps steps of 64)
   const int ks = blockIdx.y;
   const int klen = p.d / p.ksplit, nsteps = klen / kLmK;
@@ -270,8 +270,11 @@ void lm_head_kernel(LmParams p) {
 }
 
 template <int RT, int CT, int WR, int NA, int DEPTH, int WPE>
-static hipError_t launch_lm_nrt(const LmParams& p, hipStream_t s) {
-  // grid: tiles of 8 vocabulary tiles (one per XCD) x row groups, row groups innermost; y: K split
+static hipError_t launch_lm_nrt(const LmParams& q, hipStream_t s) {
+  // grid: tiles of 8 vocabulary tiles (one per XCD) x row groups of 32 WR RT rows, row groups
+  // innermost; y: K split
+  LmParams p = q;
+  p.mgroups = (p.M + 32 * WR * RT - 1) / (32 * WR * RT);
   const int64_t grid = (int64_t)((p.ntiles + 7) / 8) * 8 * p.mgroups;
   const dim3 g((unsigned)grid, (unsigned)p.ksplit);
   if (p.mgroups == 1)

@@ -10,7 +10,9 @@ al. 2023; the paper's [sd]) rather than against a restatement of the rule:
   position i, given that position i is reached, is distributed as the target p_i
   (k = 0, the bonus row, and positions 0 and 1 with k = 2 at V = 8);
 * the acceptance frequency of draft x equals min(1, p(x)/q(x)) on that grid (to 2^-23);
-* exact inverse-CDF agreement with a rational computation for plain sampling;
+* exact inverse-CDF agreement with a rational computation for plain sampling and for the
+  residual of a rejected draft, up to the fixed-point resolution of the target row's scale;
+  a residual below that resolution falls back to the target row;
 * invariants: an identical draft accepts every token; p(x) = 0 always rejects;
   q(x) = 0 < p(x) always accepts; NaN rejects; lowering a uniform never shortens the
   accepted prefix; status codes and the sequence-length rollback.
@@ -218,6 +220,46 @@ def test_extreme_uniforms_pick_first_and_last_positive_token():
                                  np.array([0.0, 1 - 2.0 ** -24], np.float32), max_k=0)
     # 1e-30 is far below 2^-40 of the max weight: its fixed-point weight is 0, never sampled
     assert tok[0, 0] == 500 and tok[1, 0] == 993
+
+
+def test_residual_sampling_matches_rational_inverse_cdf():
+    # a rejected draft: the token is the rational inverse CDF of w = max(0, fp32(p - q)), except
+    # within the fixed-point resolution: each weight is truncated to a multiple of 2^(e - 40),
+    # e the exponent of the target row's largest probability
+    rng = np.random.default_rng(11)
+    V, nseq = 64, 200
+    p = rng.random((2 * nseq, V)).astype(np.float32) ** 2
+    q = rng.random((nseq, V)).astype(np.float32) ** 2
+    ids = np.argmax(q - p[0::2], axis=1).astype(np.int32)   # q > p there: rejected at u near 1
+    qsl = np.arange(0, 2 * nseq + 1, 2, dtype=np.int32)
+    ua = np.full(nseq, 1 - 2.0 ** -24, np.float32)
+    us = rng.random(nseq, dtype=np.float32)
+    a, tok, st, _ = oracle.accept(qsl, p, q, ids, ua, us)
+    assert (a == 0).all() and (st == 0).all()
+    checked = 0
+    for b in range(nseq):
+        w = np.maximum(p[2 * b] - q[b], np.float32(0))
+        e = np.frexp(np.float64(p[2 * b].max()))[1] - 1
+        m, margin = exact_inverse_cdf(w, us[b])
+        if margin > 4 * V * 2.0 ** (e - 40) / w.astype(np.float64).sum():
+            assert tok[b, 0] == m, b
+            checked += 1
+        assert w[tok[b, 0]] > 0
+    assert checked > nseq * 0.9
+
+
+def test_sampling_scale_is_the_target_rows_largest_probability():
+    # a positive residual below 2^-40 of max p has fixed-point weight 0: the sample falls back
+    # to p (a scale taken from the residual itself would give token 3)
+    V = 4
+    p = np.array([[0.5, 0.25 - 2.0 ** -26, 0.25, 2.0 ** -45], [0.25] * V], np.float32)
+    q = np.array([[0.5, 0.25, 0.25, 0.0]], np.float32)
+    a, tok, st, _ = oracle.accept([0, 2], p, q, [1], [1 - 2.0 ** -24], [0.999])
+    assert a[0] == 0 and st[0] == oracle.OK and tok[0, 0] == 2
+    # a residual weight of 2^-40 = 2 units at that scale is sampled
+    p[0, 3] = 2.0 ** -40
+    a, tok, st, _ = oracle.accept([0, 2], p, q, [1], [1 - 2.0 ** -24], [0.999])
+    assert a[0] == 0 and st[0] == oracle.OK and tok[0, 0] == 3
 
 
 # --------------------------------------------------------------- invariants
