@@ -17,14 +17,16 @@
 //             {2..5}, {6..13}, ... (one round for small batches); a round takes only the
 //             sequences that passed every test before it (a device-side list), so rows past a
 //             rejection are rarely read.
-//     stats   the statistics (max, sum of 2^(y - max)) of the round's target and draft rows,
+//     stats   round 0: the statistics (max, sum of 2^(y - max)) of its target and draft rows,
 //             per (row, sub-chunk), and the inputs of its tests.  The tests of a round are
 //             independent of each other, so nothing here waits for a decision.
-//     decide  one work item per (sequence, sub-chunk): every item of a sequence runs the
-//             round's tests from those statistics (its waves split the positions) and reaches
-//             the same first failure a; then it computes the fixed-point sums of the residual
-//             of row a (or of the bonus row) over its sub-chunk, or puts the sequence on the
-//             next list.
+//     decide  round r, one work item per (sequence, sub-chunk): every item of a sequence runs
+//             the round's tests from those statistics (its waves split the positions) and
+//             reaches the same first failure a; then it computes the fixed-point sums of the
+//             residual of row a (or of the bonus row) over its sub-chunk, or, for a sequence
+//             that passed every test, the statistics of round r+1's rows over its sub-chunk
+//             (and puts the sequence on round r+1's list).  So the sampled rows of finished
+//             sequences stream together with the next round's rows, one launch per round.
 //   init      (probability inputs) one thread per sequence: geometry, draft-id check, tests.
 //   max pass  (probability inputs) per sub-chunk: max of p, bad flag.
 //   sum pass  (probability inputs) per sub-chunk: the sums of W_v.
@@ -429,61 +431,97 @@ __device__ __forceinline__ void round_seq(const AcceptParams& p, int r, int li, 
 
 __device__ __forceinline__ int round_count(const AcceptParams& p, int r) { return r == 0 ? p.B : p.counts[r]; }
 
-// Round r, positions [lo, hi): statistics of target rows lo..min(hi-1, k) and draft rows
-// lo..min(hi, k)-1 of every sequence in the round's list, per (row, sub-chunk), and the inputs
-// of the tests at those positions.  Work items are strided over a bounded grid (the host does
-// not know how many sequences reach the round).
-__global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p, int r, int lo, int hi) {
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  if (r == 0 && blockIdx.x == 0 && threadIdx.x <= kAcceptMaxRounds) p.counts[threadIdx.x] = 0;
-  const int rows = 2 * (hi - lo);
-  const int64_t total = (int64_t)round_count(p, r) * rows * p.nsub;
+// The inputs of test pos of sequence b: target and draft entries of draft x_pos, u_pos, and
+// whether x_pos is a valid id (called by one thread).
+__device__ __forceinline__ void gather_test(const AcceptParams& p, int b, const Geom& g, int pos) {
+  const int x = p.ids[g.d0 + pos];
+  const bool ok = x >= 0 && x < p.V;
+  f32x4 t;
+  t[0] = ok ? p.target[(int64_t)(g.t0 + pos) * p.V + x] : 0.f;
+  t[1] = ok ? p.draft[(int64_t)(g.d0 + pos) * p.V + x] : 0.f;
+  t[2] = p.u_accept[g.d0 + pos];
+  t[3] = ok ? 1.f : 0.f;
+  *reinterpret_cast<f32x4*>(p.tin + ((int64_t)b * p.max_k + pos) * 4) = t;
+}
+
+// Statistics of one row over sub-chunk `sub` from its entries v (overwritten): the four waves'
+// (max, sum) combined in wave order (common maximum, rescaled sums; NaN stays NaN), written by
+// thread 0 to the row's slot.  (All four waves must call it.)
+__device__ __forceinline__ void store_sub_stats(const AcceptParams& p, float (&v)[kPerLane], float* slot, int sub,
+                                                int wave, int lane) {
   __shared__ float sm_m[kWaves], sm_z[kWaves];
+  float m, z;
+  wave_stats(v, p.c, m, z);
+  if (lane == 0) {
+    sm_m[wave] = m;
+    sm_z[wave] = z;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float M = sm_m[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) M = fmaxf(M, sm_m[w]);
+    float Z = 0.f;
+    bool nan = false;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      nan |= sm_z[w] != sm_z[w];
+      if (sm_m[w] != -INFINITY) Z += sm_z[w] * fast_exp2(sm_m[w] - M);
+    }
+    *reinterpret_cast<f32x2*>(slot + 2 * sub) = f32x2{M, nan ? NAN : Z};
+  }
+  __syncthreads();
+}
+
+// Round 0, positions [0, hi): statistics of target rows 0..min(hi-1, k) and draft rows
+// 0..min(hi, k)-1 of every sequence, one work item per (row, sub-chunk), and the inputs of the
+// tests at those positions.
+__global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p, int hi) {
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  if (blockIdx.x == 0 && threadIdx.x <= kAcceptMaxRounds) p.counts[threadIdx.x] = 0;
+  const int rows = 2 * hi;
+  const int64_t total = (int64_t)p.B * rows * p.nsub;
   for (int64_t item = blockIdx.x; item < total; item += gridDim.x) {
     const int sub = (int)(item % p.nsub);
     const int64_t rest = item / p.nsub;
-    const int rr = (int)(rest % rows), li = (int)(rest / rows);
-    const int pos = lo + (rr >> 1), which = rr & 1;
-    int b, n;
-    Geom g;
-    round_seq(p, r, li, b, g, n);
+    const int rr = (int)(rest % rows), b = (int)(rest / rows);
+    const int pos = rr >> 1, which = rr & 1;
+    int n;
+    const Geom g = seq_geom(p, b, n);
     if (!g.valid || pos > g.k || (which == 1 && pos == g.k)) continue;
-    if (which == 0 && pos < g.k && sub == 0 && threadIdx.x == 0) {
-      // the inputs of test pos, gathered here so that the decision needs no dependent gather
-      const int x = p.ids[g.d0 + pos];
-      const bool ok = x >= 0 && x < p.V;
-      f32x4 t;
-      t[0] = ok ? p.target[(int64_t)(g.t0 + pos) * p.V + x] : 0.f;
-      t[1] = ok ? p.draft[(int64_t)(g.d0 + pos) * p.V + x] : 0.f;
-      t[2] = p.u_accept[g.d0 + pos];
-      t[3] = ok ? 1.f : 0.f;
-      *reinterpret_cast<f32x4*>(p.tin + ((int64_t)b * p.max_k + pos) * 4) = t;
-    }
+    // the inputs of test pos, gathered here so that the decision needs no dependent gather
+    if (which == 0 && pos < g.k && sub == 0 && threadIdx.x == 0) gather_test(p, b, g, pos);
     const float* row = which ? p.draft + (int64_t)(g.d0 + pos) * p.V : p.target + (int64_t)(g.t0 + pos) * p.V;
     float v[kPerLane];
     load_sub<true>(row, sub, wave, p.V, (p.V & 3) == 0, -INFINITY, lane, v);
-    float m, z;
-    wave_stats(v, p.c, m, z);
-    // the four waves in order: common maximum, rescaled sums; NaN stays NaN
-    if (lane == 0) {
-      sm_m[wave] = m;
-      sm_z[wave] = z;
+    store_sub_stats(p, v, lse_slot(p, b, pos, which), sub, wave, lane);
+  }
+}
+
+// Round r+1, positions [lo, hi), of sequence b over sub-chunk `sub`: statistics of target rows
+// lo..min(hi-1, k) and draft rows lo..min(hi, k)-1 (target rows first), each row's loads issued
+// before the previous row reduces; the item of sub-chunk 0 gathers the round's test inputs.
+__device__ void next_round_stats(const AcceptParams& p, int b, const Geom& g, int lo, int hi, int sub, int wave,
+                                 int lane) {
+  const int nt = min(hi - 1, g.k) - lo + 1;   // >= 1: lo <= k
+  const int nd = max(0, min(hi, g.k) - lo);
+  const int rows = nt + nd;
+  if (sub == 0 && threadIdx.x == 0)
+    for (int pos = lo; pos < min(hi, g.k); ++pos) gather_test(p, b, g, pos);
+  const bool vec = (p.V & 3) == 0;
+  auto row = [&](int j) {
+    return j < nt ? p.target + (int64_t)(g.t0 + lo + j) * p.V : p.draft + (int64_t)(g.d0 + lo + j - nt) * p.V;
+  };
+  auto slot = [&](int j) { return j < nt ? lse_slot(p, b, lo + j, 0) : lse_slot(p, b, lo + j - nt, 1); };
+  float va[kPerLane], vb[kPerLane];
+  load_sub<true>(row(0), sub, wave, p.V, vec, -INFINITY, lane, va);
+  for (int j = 0; j < rows; j += 2) {
+    if (j + 1 < rows) load_sub<true>(row(j + 1), sub, wave, p.V, vec, -INFINITY, lane, vb);
+    store_sub_stats(p, va, slot(j), sub, wave, lane);
+    if (j + 1 < rows) {
+      if (j + 2 < rows) load_sub<true>(row(j + 2), sub, wave, p.V, vec, -INFINITY, lane, va);
+      store_sub_stats(p, vb, slot(j + 1), sub, wave, lane);
     }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      float M = sm_m[0];
-#pragma unroll
-      for (int w = 1; w < kWaves; ++w) M = fmaxf(M, sm_m[w]);
-      float Z = 0.f;
-      bool nan = false;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        nan |= sm_z[w] != sm_z[w];
-        if (sm_m[w] != -INFINITY) Z += sm_z[w] * fast_exp2(sm_m[w] - M);
-      }
-      *reinterpret_cast<f32x2*>(lse_slot(p, b, pos, which) + 2 * sub) = f32x2{M, nan ? NAN : Z};
-    }
-    __syncthreads();
   }
 }
 
@@ -534,23 +572,16 @@ __global__ __launch_bounds__(kThreads) void accept_gather_kernel(AcceptParams p)
   int n;
   const Geom g = seq_geom(p, b, n);
   if (!g.valid || i >= g.k) return;
-  const int x = p.ids[g.d0 + i];
-  const bool ok = x >= 0 && x < p.V;
-  f32x4 t;
-  t[0] = ok ? p.target[(int64_t)(g.t0 + i) * p.V + x] : 0.f;
-  t[1] = ok ? p.draft[(int64_t)(g.d0 + i) * p.V + x] : 0.f;
-  t[2] = p.u_accept[g.d0 + i];
-  t[3] = ok ? 1.f : 0.f;
-  *reinterpret_cast<f32x4*>(p.tin + (idx) * 4) = t;
+  gather_test(p, b, g, i);
 }
 
 // Round r, positions [lo, hi): one work item per (sequence of the list, sub-chunk).  Every item
 // of a sequence runs the tests at those positions (its waves split them) and reaches the same
 // first failure.  A failure at a: the sequence is done testing (residual at a), and the item
 // computes the fixed-point sums of the residual of row a over its sub-chunk.  No failure: the
-// same for the bonus row if the round reached position k, else the sequence joins round r+1's
-// list.
-__global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p, int r, int lo, int hi) {
+// same for the bonus row if the round reached position k, else the sequence joins round r+1
+// (positions [hi, hi2)) and the item computes that round's statistics over its sub-chunk.
+__global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p, int r, int lo, int hi, int hi2) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int64_t total = (int64_t)round_count(p, r) * p.nsub;
   __shared__ int sm_fail[kWaves];
@@ -600,10 +631,14 @@ __global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p,
         p.st_mode[b] = residual ? kResidual : kBonus;
       }
       sample_sums(p, b, g, at, residual, sub, wave, lane);
-    } else if (lead) {
-      const int at = __hip_atomic_fetch_add(p.counts + r + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      *reinterpret_cast<u32x4*>(p.lists + ((int64_t)r * p.B + at) * 4) =
-          u32x4{(uint32_t)b, (uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k};
+    } else {
+      // hi <= k <= max_k: round r+1 exists (the host passes hi2 > hi)
+      if (lead) {
+        const int at = __hip_atomic_fetch_add(p.counts + r + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        *reinterpret_cast<u32x4*>(p.lists + ((int64_t)r * p.B + at) * 4) =
+            u32x4{(uint32_t)b, (uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k};
+      }
+      next_round_stats(p, b, g, hi, hi2, sub, wave, lane);
     }
   }
 }
@@ -829,7 +864,7 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
                          s, q);
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(accept_decide_kernel, dim3(items), dim3(kThreads), 0, s, q, 0, 0, q.max_k + 1);
+    hipLaunchKernelGGL(accept_decide_kernel, dim3(items), dim3(kThreads), 0, s, q, 0, 0, q.max_k + 1, 0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return launch_search(q, s);
   }
@@ -843,16 +878,20 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
     const bool one_round =
         (int64_t)p.V * 4 < kRoundRowBytes && (int64_t)p.B * (p.max_k + 1) * p.V * 4 <= kOneRoundBytes;
     int width = one_round ? p.max_k + 1 : 2;
-    for (int r = 0, lo = 0; lo <= p.max_k; ++r, lo += width, width *= 2) {
-      const int hi = lo + width;
+    {
       // one workgroup per work item (a workgroup's items run one after another, their latency
-      // exposed); later rounds, whose size the host does not know, are capped
-      const int64_t rows = (int64_t)p.B * 2 * (hi - lo) * p.nsub;
-      const unsigned gs = (unsigned)(r == 0 || rows < kRoundGrid ? rows : kRoundGrid);
-      const unsigned gd = r == 0 || items < (unsigned)kRoundGrid ? items : (unsigned)kRoundGrid;
-      hipLaunchKernelGGL(accept_stats_kernel, dim3(gs), dim3(kThreads), 0, s, p, r, lo, hi);
+      // exposed)
+      const unsigned gs = (unsigned)((int64_t)p.B * 2 * width * p.nsub);
+      hipLaunchKernelGGL(accept_stats_kernel, dim3(gs), dim3(kThreads), 0, s, p, width);
       if ((e = hipGetLastError()) != hipSuccess) return e;
-      hipLaunchKernelGGL(accept_decide_kernel, dim3(gd), dim3(kThreads), 0, s, p, r, lo, hi);
+    }
+    for (int r = 0, lo = 0; lo <= p.max_k; ++r, lo += width, width *= 2) {
+      // decide round r; a sequence passing all of it computes round r+1's statistics.  Later
+      // rounds, whose size the host does not know, have a capped grid.
+      const int hi = lo + width;
+      const int hi2 = hi <= p.max_k ? hi + 2 * width : 0;
+      const unsigned gd = r == 0 || items < (unsigned)kRoundGrid ? items : (unsigned)kRoundGrid;
+      hipLaunchKernelGGL(accept_decide_kernel, dim3(gd), dim3(kThreads), 0, s, p, r, lo, hi, hi2);
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
   } else {
