@@ -212,6 +212,7 @@ __device__ void write_invalid(const AcceptParams& p, int b, int n) {
   p.row_status[b] = n >= 1 ? SPEXIS_ROW_BAD_TOKEN : SPEXIS_ROW_BAD_VALUE;
   p.st_mode[b] = kDone;
   p.st_a[b] = 0;
+  reinterpret_cast<u32x4*>(p.srec)[3 * (int64_t)b + 1] = u32x4{(uint32_t)kDone, 0u, 0u, 0u};
 }
 
 // Row context of a tested or sampled position a: target row a (P) and, for a residual, draft
@@ -363,6 +364,13 @@ __device__ void sample_sums(const AcceptParams& p, int b, const Geom& g, int a, 
   float M;
   int bad;
   sampled_scale(p, r, b, residual, lane, M, bad);
+  if (sub == 0 && threadIdx.x == 0) {
+    // the search's record: geometry, position and mode, bad flag and scale, row statistics
+    u32x4* rec = reinterpret_cast<u32x4*>(p.srec) + 3 * (int64_t)b;
+    rec[0] = u32x4{(uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k, (uint32_t)a};
+    rec[1] = u32x4{(uint32_t)(residual ? kResidual : kBonus), (uint32_t)bad, __float_as_uint(M), 0u};
+    rec[2] = u32x4{__float_as_uint(r.Mp), __float_as_uint(r.Rp), __float_as_uint(r.Mq), __float_as_uint(r.Rq)};
+  }
   if (bad || !(M > 0.f)) return;   // the same decision in every wave
   sub_sums(p, r, residual, b, sub, 40 - floor_log2(M), wave, lane, pv, qv);
 }
@@ -473,32 +481,7 @@ __device__ __forceinline__ void store_sub_stats(const AcceptParams& p, float (&v
   __syncthreads();
 }
 
-// Round 0, positions [0, hi): statistics of target rows 0..min(hi-1, k) and draft rows
-// 0..min(hi, k)-1 of every sequence, one work item per (row, sub-chunk), and the inputs of the
-// tests at those positions.
-__global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p, int hi) {
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  if (blockIdx.x == 0 && threadIdx.x <= kAcceptMaxRounds) p.counts[threadIdx.x] = 0;
-  const int rows = 2 * hi;
-  const int64_t total = (int64_t)p.B * rows * p.nsub;
-  for (int64_t item = blockIdx.x; item < total; item += gridDim.x) {
-    const int sub = (int)(item % p.nsub);
-    const int64_t rest = item / p.nsub;
-    const int rr = (int)(rest % rows), b = (int)(rest / rows);
-    const int pos = rr >> 1, which = rr & 1;
-    int n;
-    const Geom g = seq_geom(p, b, n);
-    if (!g.valid || pos > g.k || (which == 1 && pos == g.k)) continue;
-    // the inputs of test pos, gathered here so that the decision needs no dependent gather
-    if (which == 0 && pos < g.k && sub == 0 && threadIdx.x == 0) gather_test(p, b, g, pos);
-    const float* row = which ? p.draft + (int64_t)(g.d0 + pos) * p.V : p.target + (int64_t)(g.t0 + pos) * p.V;
-    float v[kPerLane];
-    load_sub<true>(row, sub, wave, p.V, (p.V & 3) == 0, -INFINITY, lane, v);
-    store_sub_stats(p, v, lse_slot(p, b, pos, which), sub, wave, lane);
-  }
-}
-
-// Round r+1, positions [lo, hi), of sequence b over sub-chunk `sub`: statistics of target rows
+// A round's positions [lo, hi) of sequence b over sub-chunk `sub`: statistics of target rows
 // lo..min(hi-1, k) and draft rows lo..min(hi, k)-1 (target rows first), each row's loads issued
 // before the previous row reduces; the item of sub-chunk 0 gathers the round's test inputs.
 __device__ void next_round_stats(const AcceptParams& p, int b, const Geom& g, int lo, int hi, int sub, int wave,
@@ -522,6 +505,32 @@ __device__ void next_round_stats(const AcceptParams& p, int b, const Geom& g, in
       if (j + 2 < rows) load_sub<true>(row(j + 2), sub, wave, p.V, vec, -INFINITY, lane, va);
       store_sub_stats(p, vb, slot(j + 1), sub, wave, lane);
     }
+  }
+}
+
+// Round 0, positions [0, hi): statistics of target rows 0..min(hi-1, k) and draft rows
+// 0..min(hi, k)-1 of every sequence, one work item per (row, sub-chunk), and the inputs of the
+// tests at those positions.  (Items of one row each keep more loads in flight than items that
+// stream a sequence's rows one after another.)
+__global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p, int hi) {
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  if (blockIdx.x == 0 && threadIdx.x <= kAcceptMaxRounds) p.counts[threadIdx.x] = 0;
+  const int rows = 2 * hi;
+  const int64_t total = (int64_t)p.B * rows * p.nsub;
+  for (int64_t item = blockIdx.x; item < total; item += gridDim.x) {
+    const int sub = (int)(item % p.nsub);
+    const int64_t rest = item / p.nsub;
+    const int rr = (int)(rest % rows), b = (int)(rest / rows);
+    const int pos = rr >> 1, which = rr & 1;
+    int n;
+    const Geom g = seq_geom(p, b, n);
+    if (!g.valid || pos > g.k || (which == 1 && pos == g.k)) continue;
+    // the inputs of test pos, gathered here so that the decision needs no dependent gather
+    if (which == 0 && pos < g.k && sub == 0 && threadIdx.x == 0) gather_test(p, b, g, pos);
+    const float* row = which ? p.draft + (int64_t)(g.d0 + pos) * p.V : p.target + (int64_t)(g.t0 + pos) * p.V;
+    float v[kPerLane];
+    load_sub<true>(row, sub, wave, p.V, (p.V & 3) == 0, -INFINITY, lane, v);
+    store_sub_stats(p, v, lse_slot(p, b, pos, which), sub, wave, lane);
   }
 }
 
@@ -624,13 +633,7 @@ __global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p,
       // a failure at a: the residual of row a; every test passed and the round reached k: the
       // bonus row k.  Either way the scale is known from row a's statistics, so the sums follow.
       const bool residual = a < g.k;
-      const int at = residual ? a : g.k;
-      if (lead) {
-        *reinterpret_cast<u32x4*>(p.geo + 4 * (int64_t)b) = u32x4{(uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k, 1u};
-        p.st_a[b] = at;
-        p.st_mode[b] = residual ? kResidual : kBonus;
-      }
-      sample_sums(p, b, g, at, residual, sub, wave, lane);
+      sample_sums(p, b, g, residual ? a : g.k, residual, sub, wave, lane);
     } else {
       // hi <= k <= max_k: round r+1 exists (the host passes hi2 > hi)
       if (lead) {
@@ -673,18 +676,10 @@ __global__ __launch_bounds__(kThreads) void accept_sum_kernel(AcceptParams p) {
 __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int b = blockIdx.x;
-  const int mode = p.st_mode[b];
-  const int a = p.st_a[b];
-  const Geom g = load_geom(p, b);
-  if (mode != kResidual && mode != kBonus) return;
-  const bool residual = mode == kResidual;
-  // every wave takes the same decisions from the same partials
-  const RowCtx r = row_ctx(p, b, g, a, residual, lane);
-  float M;
-  int bad;
-  sampled_scale(p, r, b, residual, lane, M, bad);
-  // the sub-chunk sums (residual, fallback), prefetched while the scale reduces (lanes own
-  // contiguous ranges)
+  // the record the sums' first sub-chunk left (every wave reads the same), and the sub-chunk
+  // sums (residual, fallback; lanes own contiguous ranges), loaded together
+  const u32x4* rec = reinterpret_cast<const u32x4*>(p.srec) + 3 * (int64_t)b;
+  const u32x4 q0 = rec[0], q1 = rec[1], q2 = rec[2];
   const uint64_t* sums = p.sum_part + (int64_t)b * p.nsub * 2;
   const int per = (p.nsub + kWave - 1) / kWave;
   const int c_lo = min(p.nsub, lane * per), c_hi = min(p.nsub, c_lo + per);
@@ -693,6 +688,21 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
     own_r += sums[2 * x];
     own_p += sums[2 * x + 1];
   }
+  const int mode = (int)q1[0];
+  if (mode != kResidual && mode != kBonus) return;
+  const bool residual = mode == kResidual;
+  const Geom g{(int)q0[0], (int)q0[1], (int)q0[2], 1};
+  const int a = (int)q0[3];
+  const int bad = (int)q1[1];
+  const float M = __uint_as_float(q1[2]);
+  RowCtx r;
+  r.P = p.target + (int64_t)(g.t0 + a) * p.V;
+  r.Q = residual ? p.draft + (int64_t)(g.d0 + a) * p.V : nullptr;
+  r.logits = p.kind == 1;
+  r.Mp = __uint_as_float(q2[0]);
+  r.Rp = __uint_as_float(q2[1]);
+  r.Mq = __uint_as_float(q2[2]);
+  r.Rq = __uint_as_float(q2[3]);
   const bool lead = threadIdx.x == 0;
   if (bad) {
     if (lead) write_outputs(p, b, g, a, -1, SPEXIS_ROW_BAD_VALUE);
@@ -879,8 +889,6 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
         (int64_t)p.V * 4 < kRoundRowBytes && (int64_t)p.B * (p.max_k + 1) * p.V * 4 <= kOneRoundBytes;
     int width = one_round ? p.max_k + 1 : 2;
     {
-      // one workgroup per work item (a workgroup's items run one after another, their latency
-      // exposed)
       const unsigned gs = (unsigned)((int64_t)p.B * 2 * width * p.nsub);
       hipLaunchKernelGGL(accept_stats_kernel, dim3(gs), dim3(kThreads), 0, s, p, width);
       if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -130,6 +130,8 @@ struct AcceptParams {
   float* max_part;       // [B][nsub] max of the sampled target row (probability inputs)
   int32_t* bad_part;     // [B][nsub] the sampled row(s) hold a bad value (probability inputs)
   uint64_t* sum_part;    // [B][nsub][2] fixed-point sums of the residual and of p
+  int32_t* srec;         // [B][12] the search's record of b: t0, d0, k, a | mode, bad, scale, 0 |
+                         // Mp, Rp, Mq, Rq (written with the sums of sub-chunk 0, or by write_invalid)
 };
 
 constexpr int kAcceptMaxRounds = 8;  // test rounds: widths 2, 4, 8, ... cover max_k <= 509
