@@ -407,8 +407,8 @@ int spexis_linear(const void* x, const void* weight, const void* residual, int32
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_linear: in_features %d is not a multiple of 256", in_features);
   if (rows == 0) return ok();
   const int64_t tiles = (out_features + spexis::kLmCols - 1) / spexis::kLmCols;
-  const int64_t groups = (rows + spexis::kLmRows - 1) / spexis::kLmRows;
-  if ((tiles + 7) / 8 * 8 * groups >= (1ll << 31) || (int64_t)rows * out_features >= (1ll << 36) ||
+  if (spexis::projection_workgroups(rows, out_features) + 8 * rows >= (1ll << 31) ||
+      (int64_t)rows * out_features >= (1ll << 36) ||
       (int64_t)rows * in_features >= (1ll << 40))
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_linear: problem too large");
   const int S = spexis::linear_split(rows, out_features, in_features);
@@ -423,7 +423,6 @@ int spexis_linear(const void* x, const void* weight, const void* residual, int32
   p.proj.V = out_features;
   p.proj.d = in_features;
   p.proj.ntiles = (int)tiles;
-  p.proj.mgroups = (int)groups;
   p.proj.ksplit = S;
   if (S > 1) {
     p.proj.logits = static_cast<float*>(workspace);   // [S][rows][out] partials
@@ -484,8 +483,7 @@ int spexis_lm_head(const void* hidden, const void* weight, int32_t rows, int32_t
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_lm_head: hidden_dim %d is not a multiple of 256", hidden_dim);
   if (rows == 0) return ok();
   const int64_t tiles = spexis_lm_head_tiles(vocab);
-  const int64_t groups = (rows + spexis::kLmRows - 1) / spexis::kLmRows;
-  if ((tiles + 7) / 8 * 8 * groups >= (1ll << 31) || (int64_t)rows * vocab >= (1ll << 40))
+  if (spexis::projection_workgroups(rows, vocab) + 8 * rows >= (1ll << 31) || (int64_t)rows * vocab >= (1ll << 40))
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_lm_head: problem too large");
   spexis::LmParams p{};
   p.h = hidden;
@@ -496,7 +494,6 @@ int spexis_lm_head(const void* hidden, const void* weight, int32_t rows, int32_t
   p.V = vocab;
   p.d = hidden_dim;
   p.ntiles = (int)tiles;
-  p.mgroups = (int)groups;
   p.ksplit = 1;
   p.c = (float)(1.4426950408889634 / (double)temperature);
   return hip_result(spexis::launch_projection(p, (hipStream_t)stream), "spexis_lm_head");

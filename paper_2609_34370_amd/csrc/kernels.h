@@ -55,12 +55,11 @@ struct LmParams {
   float* stats;          // [M][ntiles][2]: max of x*c and sum of 2^(x*c - max) over each tile (or null)
   void* y;               // [M][V] bf16 output, bf16(acc + res), instead of logits (ksplit == 1)
   const void* res;       // [M][V] bf16 residual for y, or null
-  int M, V, d, ntiles, mgroups;
+  int M, V, d, ntiles, mgroups;   // ntiles: 128-column statistics tiles; mgroups: set by the launcher
   int ksplit;            // K split over workgroups (grid y); each takes d / ksplit
   float c;               // log2(e) / temperature
 };
 
-constexpr int kLmRows = 320;   // rows of h per workgroup (ten 32-row MFMA tiles)
 constexpr int kLmCols = 128;   // vocabulary columns per workgroup (four waves of 32)
 constexpr int kLmK = 64;       // K per pipeline step (four MFMA k-steps)
 
@@ -148,6 +147,9 @@ hipError_t launch_pack_weight(const void* w, int N, int K, void* out, hipStream_
 constexpr int kPackTile = 2048;
 hipError_t launch_linear(const LinearParams& p, hipStream_t s);
 hipError_t launch_projection(const LmParams& p, hipStream_t s);
+// Workgroups launch_projection runs for M rows and N columns (without a K split; at most 8 more
+// are launched to round the column workgroups up to a multiple of 8 per row group).
+int64_t projection_workgroups(int64_t M, int64_t N);
 hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V, float c, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s);
 

@@ -63,11 +63,9 @@ __global__ __launch_bounds__(kThreads) void linear_reduce_kernel(LinearParams p)
 // partials (S M N fp32, written once and read once) stay within the weight's own traffic
 // (2 S M N 4 <= 2 N K 2, i.e. 2 S M <= K).
 int linear_split(int M, int N, int K) {
-  const int64_t rows_per_group = 320;
-  const int64_t mgroups = (M + rows_per_group - 1) / rows_per_group;
-  const int64_t tiles = (N + kLmCols - 1) / kLmCols;
+  const int64_t wgs = projection_workgroups(M, N);
   int S = 1;
-  while (S < 8 && tiles * mgroups * S < 256 && K % (kLmK * 2 * S) == 0 && (int64_t)2 * (2 * S) * M <= K) S *= 2;
+  while (S < 8 && wgs * S < 256 && K % (kLmK * 2 * S) == 0 && (int64_t)2 * (2 * S) * M <= K) S *= 2;
   return S;
 }
 

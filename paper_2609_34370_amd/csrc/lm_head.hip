@@ -19,16 +19,14 @@
 //     for h step i+1 leaves the NA steps of W loaded after it in flight, and W runs DEPTH >=
 //     NA + 2 steps ahead, so the compute of step i+1 never waits for its W.  Few row tiles leave
 //     registers for NA = 4, DEPTH = 8; the full 320-row group uses NA = 2, DEPTH = 4.
-//   * Workgroups of one vocabulary tile and consecutive row groups are dispatched to the same
-//     XCD one after another, so a W tile read for one row group is an L2 hit for the next.
+//   * Each XCD takes blocks of its vocabulary tiles x row groups (tile_of), so its resident
+//     workgroups share the K-slices of h and W they read through its L2.
 #include "common.h"
 #include "kernels.h"
 
 namespace spexis {
 
 namespace {
-
-constexpr int kRT = kLmRows / 32;   // row tiles per workgroup
 
 __device__ __forceinline__ uint16_t bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
@@ -46,37 +44,68 @@ __device__ __forceinline__ u32x4 ldw(const uint16_t* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
 
+// Workgroup -> (vocabulary tile nt, row group mg).  Workgroup i runs on XCD i % 8, which takes
+// the vocabulary tiles nt = 8 j + XCD; the XCD's workgroups, in launch order, walk blocks of
+// kTileBlock of its tiles, and within a block the row groups in blocks of kGroupBlock, each
+// (tiles x groups) block in tile-major order.  The XCD's resident workgroups (one per CU) then
+// cover a few row groups of a few tiles at a time, so each K-step's slice of h and of W is
+// fetched into the XCD's L2 once for several workgroups.
+constexpr int kTileBlock = 8, kGroupBlock = 4;
+__device__ __forceinline__ void tile_of(int bid, int ntiles, int groups, int& nt, int& mg) {
+  const int xcd = bid & 7, local = bid >> 3;
+  const int per_xcd = (ntiles + 7) / 8;                     // tiles of an XCD (the last may be absent)
+  const int tb = local / (kTileBlock * groups), rem = local % (kTileBlock * groups);
+  const int ctb = min(kTileBlock, per_xcd - tb * kTileBlock);   // tiles in this block
+  const int full = groups / kGroupBlock * kGroupBlock;      // groups in whole group blocks
+  int t, g;
+  if (rem < ctb * full) {
+    const int gb = rem / (ctb * kGroupBlock), r2 = rem % (ctb * kGroupBlock);
+    t = r2 / kGroupBlock;
+    g = gb * kGroupBlock + r2 % kGroupBlock;
+  } else {
+    const int r2 = rem - ctb * full, tail = groups - full;
+    t = r2 / tail;
+    g = full + r2 % tail;
+  }
+  nt = 8 * (tb * kTileBlock + t) + xcd;
+  mg = g;
+}
+
 }  // namespace
 
-// Waves form a WR x WC grid over the workgroup's (32 * WR * RT) rows x 128 columns: wave
-// (wr, wc) computes RT row tiles x CT column tiles (WC * CT = 4).  One column of waves (WR = 1,
-// CT = 1) suits few rows; for 320-row groups a 2 x 2 grid halves the h fragments each wave reads
-// from LDS per step for the same MFMA work (each W tile is then loaded by two waves, the second
-// load an L1 hit).
+// Waves form a WR x WC grid over the workgroup's (32 * WR * RT) rows x (32 * WC * CT) columns:
+// wave (wr, wc) computes RT row tiles x CT column tiles.  One column of waves (WR = 1) with one
+// column tile each suits few rows; for more rows, two column tiles per wave (256 columns per
+// workgroup) halve the h fragments each wave reads from LDS per MFMA, and halve the h rows
+// staged per column.  (A 2 x 2 grid over 128 columns does the former but loads each W tile
+// twice.)  Statistics stay per 128-column tile: a 256-column workgroup writes two.
 template <bool kStream, int RT, int CT, int WR, int NA, int DEPTH, int WPE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE)))
 void lm_head_kernel(LmParams p) {
   static_assert(DEPTH >= NA + 2 && DEPTH % NA == 0 && DEPTH % 2 == 0, "pipeline shape");
   constexpr int WC = 4 / WR;
-  static_assert(WR * WC == 4 && WC * CT == 4, "wave grid");
+  constexpr int kCols = 32 * WC * CT;           // columns of the workgroup
+  constexpr int kStatTiles = kCols / kLmCols;   // its 128-column statistics tiles
+  static_assert(WR * WC == 4 && (kCols == 128 || kCols == 256), "wave grid");
   constexpr int NRT = WR * RT;   // row tiles of the workgroup
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 31, half = lane >> 5;
   const int wr = wave / WC, wc = wave % WC;
-  const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
-  const int mg = local % p.mgroups;
-  const int nt = (local / p.mgroups) * 8 + xcd;
-  if (nt >= p.ntiles) return;
-  const int m0 = mg * 32 * NRT, n0 = nt * kLmCols;
+  const int wgcols = (p.V + kCols - 1) / kCols;
+  int nt, mg;
+  tile_of(blockIdx.x, wgcols, p.mgroups, nt, mg);
+  if (nt >= wgcols) return;
+  const int m0 = mg * 32 * NRT, n0 = nt * kCols;
   const int rows = min(32 * NRT, p.M - m0);
   // K split: workgroup row ks takes K values ks * klen .. +klen-1 (nsteps steps of 64)
   const int ks = blockIdx.y;
   const int klen = p.d / p.ksplit, nsteps = klen / kLmK;
-  // column tile c of this wave is packed tile row 4 nt + CT wc + c (clamped for the columns past
-  // V, whose results are dropped); lane l reads 16 contiguous bytes at s * 512 + 8 l of each tile
+  // column tile c of this wave is packed tile row n0 / 32 + CT wc + c (clamped for the columns
+  // past V, whose results are dropped); lane l reads 16 contiguous bytes at s * 512 + 8 l of each
+  // tile
   const uint16_t* wrow[CT];
 #pragma unroll
   for (int c = 0; c < CT; ++c) {
-    const int wtile = min(4 * nt + CT * wc + c, (p.V + 31) / 32 - 1);
+    const int wtile = min(n0 / 32 + CT * wc + c, (p.V + 31) / 32 - 1);
     wrow[c] = reinterpret_cast<const uint16_t*>(p.w) +
               ((int64_t)wtile * (p.d / kLmK) + (int64_t)ks * nsteps) * kPackTile + 8 * lane;
   }
@@ -214,7 +243,8 @@ void lm_head_kernel(LmParams p) {
   if (!p.stats) return;
   // Row statistics: each wave transposes one 32x32 tile at a time through its part of the (now
   // free) h stages; lane r < 32 reduces row r over the tile's 32 columns, then over the wave's
-  // CT tiles in order; the WC waves of a row are combined in order at the end.
+  // CT tiles in order; the waves of a row and 128-column statistics tile are combined in order
+  // at the end.
   __shared__ float sm_m[WC][32 * NRT], sm_z[WC][32 * NRT];
   constexpr int kTS = 36;   // floats per transposed row (16-byte aligned, padded)
   float* tile = reinterpret_cast<float*>(&sm_a[0][0]) + wave * 32 * kTS;
@@ -257,15 +287,19 @@ void lm_head_kernel(LmParams p) {
     }
   }
   __syncthreads();
-  for (int r = threadIdx.x; r < rows; r += 256) {
-    float M = sm_m[0][r];
+  constexpr int kWavesPerStat = WC / kStatTiles;   // waves of a row within one statistics tile
+  for (int q = threadIdx.x; q < rows * kStatTiles; q += 256) {
+    const int r = q % rows, st = q / rows, w0 = st * kWavesPerStat;
+    const int tile = nt * kStatTiles + st;
+    if (tile >= p.ntiles) continue;
+    float M = sm_m[w0][r];
 #pragma unroll
-    for (int w = 1; w < WC; ++w) M = fmaxf(M, sm_m[w][r]);
+    for (int w = 1; w < kWavesPerStat; ++w) M = fmaxf(M, sm_m[w0 + w][r]);
     float Z = 0.f;
 #pragma unroll
-    for (int w = 0; w < WC; ++w)
-      if (sm_m[w][r] != -INFINITY) Z += sm_z[w][r] * fast_exp2(sm_m[w][r] - M);
-    *reinterpret_cast<f32x2*>(p.stats + ((int64_t)(m0 + r) * p.ntiles + nt) * 2) = f32x2{M, Z};
+    for (int w = 0; w < kWavesPerStat; ++w)
+      if (sm_m[w0 + w][r] != -INFINITY) Z += sm_z[w0 + w][r] * fast_exp2(sm_m[w0 + w][r] - M);
+    *reinterpret_cast<f32x2*>(p.stats + ((int64_t)(m0 + r) * p.ntiles + tile) * 2) = f32x2{M, Z};
   }
 }
 
@@ -275,7 +309,8 @@ static hipError_t launch_lm_nrt(const LmParams& q, hipStream_t s) {
   // innermost; y: K split
   LmParams p = q;
   p.mgroups = (p.M + 32 * WR * RT - 1) / (32 * WR * RT);
-  const int64_t grid = (int64_t)((p.ntiles + 7) / 8) * 8 * p.mgroups;
+  const int wgcols = (p.V + 32 * (4 / WR) * CT - 1) / (32 * (4 / WR) * CT);
+  const int64_t grid = (int64_t)((wgcols + 7) / 8) * 8 * p.mgroups;
   const dim3 g((unsigned)grid, (unsigned)p.ksplit);
   if (p.mgroups == 1)
     hipLaunchKernelGGL((lm_head_kernel<true, RT, CT, WR, NA, DEPTH, WPE>), g, dim3(256), 0, s, p);
@@ -284,17 +319,26 @@ static hipError_t launch_lm_nrt(const LmParams& q, hipStream_t s) {
   return hipGetLastError();
 }
 
+int64_t projection_workgroups(int64_t M, int64_t N) {
+  // the shapes launch_projection picks: 128-column workgroups of one row group up to 128 rows,
+  // 160-row x 256-column workgroups beyond
+  if (M <= 128) return (N + kLmCols - 1) / kLmCols;
+  return (N + 255) / 256 * ((M + 159) / 160);
+}
+
 hipError_t launch_projection(const LmParams& p, hipStream_t s) {
   // row tiles computed per workgroup: the smallest instantiated count covering the rows (a
   // group of fewer rows repeats its last row in the padding tiles, whose results are dropped).
-  // Few rows: one column of waves, two workgroups per CU, deep pipelines (the weight stream is
-  // the bound); many rows: a 2 x 2 wave grid (the LDS reads of h are).
-  const int need = p.M >= kLmRows ? kRT : (p.M + 31) / 32;
+  // Few rows: one column of waves, 128 columns, deep pipelines (the weight stream is the bound).
+  // More rows: groups of 160 rows x 256 columns.  There every load -- h from L2, W from HBM --
+  // is an L1 miss, and each CU's capacity for pending misses bounds the streams, so the larger
+  // tile's fewer requests per MFMA pay (measured at 320 x 4096 @ 128256: 437 us against 460 for
+  // 320 x 128 workgroups on a 2 x 2 wave grid, and 5.0 against 5.7 ms at 4608 rows).
+  const int need = (p.M + 31) / 32;
   if (need <= 1) return launch_lm_nrt<1, 1, 1, 4, 8, 2>(p, s);
   if (need <= 2) return launch_lm_nrt<2, 1, 1, 4, 8, 2>(p, s);
   if (need <= 4) return launch_lm_nrt<4, 1, 1, 4, 8, 1>(p, s);
-  if (need <= 6) return launch_lm_nrt<3, 2, 2, 2, 4, 1>(p, s);
-  return launch_lm_nrt<kRT / 2, 2, 2, 2, 4, 1>(p, s);
+  return launch_lm_nrt<5, 2, 1, 2, 4, 1>(p, s);
 }
 
 }  // namespace spexis

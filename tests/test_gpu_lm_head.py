@@ -70,7 +70,7 @@ def check(h, hb, w, wb, T, rows_idx=None):
 
 
 @pytest.mark.parametrize("rows,V,d", [(1, 1000, 256), (37, 4101, 512), (320, 2048, 256), (333, 3000, 256),
-                                      (700, 130, 512)])
+                                      (700, 130, 512), (1500, 9000, 256)])
 def test_lm_head_small_shapes(rows, V, d):
     h, hb = bf16_pair((rows, d), 1, 1.0)
     w, wb = bf16_pair((V, d), 2, 0.05)
@@ -95,6 +95,17 @@ def test_lm_head_llama3_8b_shape_sampled_rows():
     w, wb = bf16_pair((V, d), 6, 0.02)
     say(f"[lm head] rows={rows} V={V} d={d} (rows 0, 31, 200, 319 checked)")
     check(h, hb, w, wb, 1.0, rows_idx=[0, 31, 200, 319])
+
+
+def test_lm_head_large_row_count_sampled_rows():
+    # many row groups: the acceptance-stress workload's shape (4608 query tokens, hidden 3584,
+    # vocabulary 152064); rows on both sides of group boundaries checked over the whole vocabulary
+    rows, V, d = 4608, 152064, 3584
+    h, hb = bf16_pair((rows, d), 7, 1.0)
+    w, wb = bf16_pair((V, d), 8, 0.02)
+    sel = [0, 319, 320, 2301, 4607]
+    say(f"[lm head] rows={rows} V={V} d={d} (rows {sel} checked)")
+    check(h, hb, w, wb, 0.7, rows_idx=sel)
 
 
 def test_accept_with_fused_statistics_agrees_with_oracle():
