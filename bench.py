@@ -450,6 +450,16 @@ def bench_draft(args):
         step.run()
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    # the same step replayed from a HIP graph: no host work between its kernels
+    step.capture()
+    for _ in range(args.warmup):
+        step.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step.replay()
+    torch.cuda.synchronize()
+    ms_graph = (time.perf_counter() - t0) * 1e3 / args.steps
     phases = (("adapter_in", step.adapter_in), ("attention", step.attention), ("adapter_out", step.adapter_out),
               ("lm_head", step.lm_head), ("sample", step.sample))
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(phases) + 1)] for _ in range(args.steps)]
@@ -472,13 +482,16 @@ def bench_draft(args):
     at_gbs = kv_bytes / (us["attention"] * 1e-6) / 1e9
     tok = step.tokens.cpu().numpy()
     conf = step.conf.cpu().numpy()
-    log(f"[draft] {spec.name}: step {ms * 1e3:.1f} us; " + ", ".join(f"{k} {v:.1f} us" for k, v in us.items()))
+    log(f"[draft] {spec.name}: step {ms * 1e3:.1f} us ({ms_graph * 1e3:.1f} us replayed from a graph); "
+        + ", ".join(f"{k} {v:.1f} us" for k, v in us.items()))
     log(f"[draft] LM head {w_bytes['lm_head'] / 1e9:.3f} GB -> {lm_gbs:.0f} GB/s ({lm_gbs / HBM_PEAK_GBS:.1%}); "
         f"attention {kv_bytes / 1e9:.3f} GB -> {at_gbs:.0f} GB/s; whole step {total / 1e9:.3f} GB -> "
         f"{total / (ms * 1e-3) / 1e9:.0f} GB/s; confidence median {np.median(conf):.2e}")
     print(json.dumps({"component": "draft_step", "workload": spec.name, "batch": B, "hidden": d, "vocab": V,
-                      "us_per_step": round(ms * 1e3, 2), "phases_us": {k: round(v, 2) for k, v in us.items()},
+                      "us_per_step": round(ms * 1e3, 2), "us_per_step_graph": round(ms_graph * 1e3, 2),
+                      "phases_us": {k: round(v, 2) for k, v in us.items()},
                       "draft_tokens_per_s": round(B / (ms * 1e-3), 1),
+                      "draft_tokens_per_s_graph": round(B / (ms_graph * 1e-3), 1),
                       "lm_head": {"bytes": w_bytes["lm_head"], "achieved": round(lm_gbs, 1), "peak": HBM_PEAK_GBS,
                                   "unit": "GB/s", "frac": round(lm_gbs / HBM_PEAK_GBS, 4)},
                       "attention": {"bytes": kv_bytes, "achieved": round(at_gbs, 1), "unit": "GB/s"},

@@ -92,3 +92,23 @@ class DraftStep:
         self.adapter_out(stream)
         self.lm_head(stream)
         self.sample(stream)
+
+    def capture(self, warmup: int = 1):
+        """Records run() into a HIP graph (torch.cuda.CUDAGraph); replay() then launches the whole
+        step at once, with no host work between its kernels.  Every buffer the step touches is
+        allocated in __init__ and the library calls neither allocate nor set memory, so the graph
+        holds only the step's kernel launches.  Like run(), a replay reads the current contents of
+        the input buffers (h, the cache, the uniforms); the sizes are those of this batch."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for _ in range(warmup):
+                self.run()
+        torch.cuda.current_stream().wait_stream(side)
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            self.run()
+        return self.graph
+
+    def replay(self):
+        self.graph.replay()

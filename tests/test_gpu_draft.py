@@ -84,3 +84,31 @@ def test_draft_step_matches_oracle(wid, B):
         assert len(diff) <= B * spec.num_kv_heads * spec.head_dim
         a, b = oracle.bf16_value(g[diff]), oracle.bf16_value(ref_pool[diff])
         assert (np.abs(a - b) <= 2.0 ** -6 * np.abs(b) + 1e-3).all()
+
+
+def test_draft_step_graph_replays_equal_the_eager_step():
+    # the step captured into a HIP graph: every replay, with eager work and synchronisations
+    # between them, gives bit for bit the eager step's outputs
+    spec = wl.spec_with(2, batch=16)
+    base = wl.make_batch(spec)
+    batch = wl.make_batch(spec, ctx_lens=base.ctx_lens, k=np.zeros(16, np.int32))
+    cache = wl.make_attention_inputs(spec, batch, device="cuda")
+    ad = wl.make_adapter_inputs(spec, batch, device="cuda")
+    step = DraftStep(batch, cache, ad)
+    step.run()
+    torch.cuda.synchronize()
+    outs = lambda: [t.clone() for t in (step.x, step.o, step.logits, step.stats, step.tokens, step.conf, step.status)]
+    ref = outs()
+    step.capture()
+    for i in range(3):
+        for t in (step.x, step.o, step.logits, step.stats, step.conf):
+            t.zero_()
+        step.tokens.fill_(-7)
+        step.status.fill_(-7)
+        torch.cuda.synchronize()
+        step.replay()
+        torch.cuda.synchronize()
+        got = outs()
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b), i
+        say(f"[draft graph] replay {i}: equal to the eager step")
