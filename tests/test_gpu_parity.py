@@ -389,6 +389,43 @@ def test_accept_logits_edge_rows_across_rounds():
         assert borderline(p, q, ids, ua, us, qsl, b, ra[b], rt[b], a[b], t[b]), b
 
 
+def test_accept_logits_empty_residual_falls_back_to_target_row():
+    # Rejections whose residual is empty in fixed point, with logits.  Sequence 0: identical target
+    # and draft rows with the drafted entry at -inf (p(x) = q(x) = 0 rejects), so max(0, p - q)
+    # is exactly 0.  Sequence 1: the same, and the draft also drops an entry the target gives
+    # e^-35 of its largest probability, so the residual's only weight lies below 2^-40 of max p:
+    # at the target row's scale it is 0 and the token comes from p (never that entry).
+    V, B, K = 5000, 2, 1
+    rng = np.random.default_rng(21)
+    qsl = np.array([0, 2, 4], np.int32)
+    tl = (rng.standard_normal((4, V)) * 2).astype(np.float32)
+    ids = np.array([11, 22], np.int32)
+    j = 4321
+    for b in range(B):
+        tl[qsl[b], ids[b]] = -np.inf
+    tl[qsl[1], j] = tl[qsl[1]].max() - 35.0
+    dl = np.stack([tl[qsl[0]], tl[qsl[1]]]).copy()
+    dl[1, j] = -np.inf
+    ua = np.full(B, 0.5, np.float32)
+    us = rng.random(B, dtype=np.float32)
+    dev = lambda x: torch.as_tensor(x, device="cuda")
+    accepted = torch.empty(B, dtype=torch.int32, device="cuda")
+    toks = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+    stat = torch.empty(B, dtype=torch.int32, device="cuda")
+    ws = torch.empty(sx.spexis_accept_workspace_size(B, V, K), dtype=torch.uint8, device="cuda")
+    sx.spexis_accept(sx.SPEXIS_INPUT_LOGITS, dev(qsl), dev(tl), dev(dl), dev(ids), dev(ua), dev(us), K, accepted,
+                     toks, stat, ws, temperature=1.0)
+    torch.cuda.synchronize()
+    a, t, s = accepted.cpu().numpy(), toks.cpu().numpy(), stat.cpu().numpy()
+    p, q = oracle.softmax(tl, 1.0), oracle.softmax(dl, 1.0)
+    ra, rt, rs, _ = oracle.accept(qsl, p, q, ids, ua, us, max_k=K)
+    say(f"[accept empty residual] tokens {t[:, 0].tolist()} oracle {rt[:, 0].tolist()}")
+    assert list(a) == [0, 0] and list(ra) == [0, 0] and (s == 0).all() and (rs == 0).all()
+    assert t[1, 0] != j and rt[1, 0] != j
+    for b in range(B):
+        assert t[b, 0] == rt[b, 0] or borderline(p, q, ids, ua, us, qsl, b, ra[b], rt[b], a[b], t[b]), b
+
+
 # -------------------------------------------------------------------------- boundary
 
 def test_boundary_errors_on_gpu():
