@@ -30,6 +30,9 @@
  *     token ids) is trusted for correctness but clamped for memory safety: an inconsistent
  *     value gives an unspecified result, never an access outside the buffers described here.
  *   - Return codes: SPEXIS_OK, or a negative code with a message in spexis_last_error().
+ *   - A call with no work (no sequences, no query tokens, or no rows) validates its scalar
+ *     arguments and returns SPEXIS_OK without reading or writing any buffer; its buffer
+ *     pointers may then be NULL (as a zero-element tensor's are).
  *   - Calls on one stream run in order; calls that share a workspace or an output and run
  *     concurrently on different streams race.
  *

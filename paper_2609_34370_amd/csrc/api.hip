@@ -108,8 +108,6 @@ int spexis_append_kv(void* k_cache, void* v_cache, int32_t num_blocks, int32_t n
                      const int32_t* block_tables, int32_t max_blocks_per_seq,
                      int32_t total_tokens, int32_t max_query_len, const void* new_k,
                      const void* new_v, void* stream) {
-  if (!k_cache || !v_cache || !query_start_loc || !seq_lens || !block_tables || !new_k || !new_v)
-    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_append_kv: null pointer");
   if (num_blocks <= 0 || num_kv_heads <= 0 || num_seqs < 0 || max_blocks_per_seq <= 0 || total_tokens < 0 ||
       max_query_len <= 0)
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_append_kv: non-positive size");
@@ -117,6 +115,8 @@ int spexis_append_kv(void* k_cache, void* v_cache, int32_t num_blocks, int32_t n
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_append_kv: block_size %d / head_dim %d not in {16,32} x {64,128}",
                 block_size, head_dim);
   if (num_seqs == 0 || total_tokens == 0) return ok();
+  if (!k_cache || !v_cache || !query_start_loc || !seq_lens || !block_tables || !new_k || !new_v)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_append_kv: null pointer");
   spexis::AppendParams p{k_cache, v_cache, query_start_loc, seq_lens, block_tables, new_k, new_v,
                          num_blocks, num_kv_heads, block_size, head_dim, num_seqs, max_blocks_per_seq,
                          total_tokens};
@@ -143,8 +143,6 @@ int spexis_verify_attention(const void* k_cache, const void* v_cache, int32_t nu
                             int32_t num_q_heads, float scale, void* out,
                             int32_t kv_chunk_tokens, void* workspace, size_t workspace_bytes,
                             void* stream) {
-  if (!k_cache || !v_cache || !query_start_loc || !seq_lens || !block_tables || !q || !out)
-    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: null pointer");
   if (num_blocks <= 0 || num_kv_heads <= 0 || num_q_heads <= 0 || num_seqs < 0 || max_blocks_per_seq <= 0 ||
       total_tokens < 0 || max_query_len <= 0 || max_seq_len <= 0 || kv_chunk_tokens < 0)
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: non-positive size");
@@ -152,7 +150,6 @@ int spexis_verify_attention(const void* k_cache, const void* v_cache, int32_t nu
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: %d query heads not a multiple of %d KV heads",
                 num_q_heads, num_kv_heads);
   if (!std::isfinite(scale)) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: scale not finite");
-  if (q == out) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: out aliases q");
   if (bad_cache_shape(block_size, head_dim))
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_verify_attention: block_size %d / head_dim %d not in {16,32} x {64,128}",
                 block_size, head_dim);
@@ -166,6 +163,9 @@ int spexis_verify_attention(const void* k_cache, const void* v_cache, int32_t nu
   if ((int64_t)num_seqs * (((int64_t)max_blocks_per_seq * block_size + 31) / 32) >= (1ll << 31))
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_verify_attention: more than 2^31 key tiles");
   if (num_seqs == 0 || total_tokens == 0) return ok();
+  if (!k_cache || !v_cache || !query_start_loc || !seq_lens || !block_tables || !q || !out)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: null pointer");
+  if (q == out) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: out aliases q");
   int tpw, nshares, nwaves;
   if (!attn_waves(num_seqs, num_kv_heads, max_seq_len, kv_chunk_tokens, &tpw, &nshares, &nwaves))
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_verify_attention: kv_chunk_tokens %d asks for too many waves",
@@ -203,11 +203,12 @@ int spexis_verify_attention(const void* k_cache, const void* v_cache, int32_t nu
 
 int spexis_softmax_rows(const float* logits, float* probs, int64_t rows, int32_t vocab, float temperature,
                         void* stream) {
-  if (!logits || !probs) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_softmax_rows: null pointer");
   if (rows < 0 || vocab <= 0) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_softmax_rows: bad size");
   if (!(temperature > 0.f) || !std::isfinite(temperature))
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_softmax_rows: temperature must be finite and > 0");
   if (rows >= (1ll << 31)) return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_softmax_rows: too many rows");
+  if (rows == 0) return ok();
+  if (!logits || !probs) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_softmax_rows: null pointer");
   const float c = (float)(1.4426950408889634 / (double)temperature);
   return hip_result(spexis::launch_softmax(logits, probs, rows, vocab, c, (hipStream_t)stream),
                     "spexis_softmax_rows");
@@ -233,16 +234,16 @@ int accept_impl(const char* who, int32_t kind, int32_t num_seqs, int32_t vocab, 
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: kind %d is neither PROBS nor LOGITS", who, kind);
   if (num_seqs < 0 || vocab <= 0 || max_k < 0 || total_tokens < num_seqs)
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: bad size", who);
-  const bool has_drafts = total_tokens > num_seqs;
-  if ((!query_start_loc && total_tokens != num_seqs) || !target || !u_sample || !accepted_len || !out_tokens ||
-      !row_status ||
-      (has_drafts && (!draft || !draft_ids || !u_accept)))
-    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: null pointer", who);
   if (kind == SPEXIS_INPUT_LOGITS && (!(temperature > 0.f) || !std::isfinite(temperature)))
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: temperature must be finite and > 0 for logits", who);
   if (max_k > kMaxK) return fail(SPEXIS_ERR_UNSUPPORTED, "%s: max_k %d > %d", who, max_k, kMaxK);
   if (vocab > kMaxVocab) return fail(SPEXIS_ERR_UNSUPPORTED, "%s: vocab %d > %d", who, vocab, kMaxVocab);
   if (num_seqs == 0) return ok();
+  const bool has_drafts = total_tokens > num_seqs;
+  if ((!query_start_loc && total_tokens != num_seqs) || !target || !u_sample || !accepted_len || !out_tokens ||
+      !row_status ||
+      (has_drafts && (!draft || !draft_ids || !u_accept)))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: null pointer", who);
   const AcceptLayout lay = accept_layout(num_seqs, vocab, max_k);
   if (!workspace || workspace_bytes < lay.total)
     return fail(SPEXIS_ERR_WORKSPACE_TOO_SMALL, "%s: workspace %zu bytes < %zu needed", who, workspace_bytes,
@@ -311,7 +312,7 @@ int spexis_accept_with_stats(int32_t num_seqs, int32_t vocab, int32_t max_k, flo
                              int32_t* row_status, int32_t* seq_lens_inout, void* workspace, size_t workspace_bytes,
                              void* stream) {
   const bool has_drafts = total_tokens > num_seqs;
-  if (!target_stats || (has_drafts && !draft_stats))
+  if (num_seqs > 0 && (!target_stats || (has_drafts && !draft_stats)))
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept_with_stats: null statistics");
   if (stats_tiles <= 0) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept_with_stats: stats_tiles <= 0");
   // the per-row reductions of the statistics live in the workspace's statistics area
@@ -333,12 +334,12 @@ int spexis_sample_tokens(int32_t kind, int32_t rows, int32_t vocab, float temper
                          const float* stats, int32_t stats_tiles, const float* u, int32_t* tokens, float* token_prob,
                          int32_t* row_status, void* workspace, size_t workspace_bytes, void* stream) {
   if (rows < 0 || vocab <= 0) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_sample_tokens: bad size");
-  if (!input || !u || !tokens || !row_status)
-    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_sample_tokens: null pointer");
   if (stats && kind != SPEXIS_INPUT_LOGITS)
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_sample_tokens: statistics need logits");
   if (stats && stats_tiles <= 0) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_sample_tokens: stats_tiles <= 0");
   if (rows == 0) return ok();
+  if (!input || !u || !tokens || !row_status)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_sample_tokens: null pointer");
   const size_t need = spexis_sample_workspace_size(rows, vocab);
   if (!workspace || workspace_bytes < need)
     return fail(SPEXIS_ERR_WORKSPACE_TOO_SMALL, "spexis_sample_tokens: workspace %zu bytes < %zu needed",
@@ -353,8 +354,6 @@ int spexis_sample_tokens(int32_t kind, int32_t rows, int32_t vocab, float temper
 int spexis_select_drafts(int32_t num_seqs, int32_t total_tokens, const int32_t* query_start_loc,
                          const float* draft_conf, float alpha, int32_t* kept_k, int32_t* kept_query_start_loc,
                          int32_t* keep, void* stream) {
-  if (!query_start_loc || !kept_k || !kept_query_start_loc)
-    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_select_drafts: null pointer");
   if (num_seqs < 0 || total_tokens < num_seqs)
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_select_drafts: bad size");
   if (!(alpha >= 0.f) || !(alpha < 1.f))
@@ -362,8 +361,9 @@ int spexis_select_drafts(int32_t num_seqs, int32_t total_tokens, const int32_t* 
   const int32_t N = total_tokens - num_seqs;
   if (N > spexis::kSelectMaxDrafts)
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_select_drafts: %d drafts > %d", N, spexis::kSelectMaxDrafts);
-  if (N > 0 && (!draft_conf || !keep)) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_select_drafts: null pointer");
   if (num_seqs == 0) return ok();
+  if (!query_start_loc || !kept_k || !kept_query_start_loc || (N > 0 && (!draft_conf || !keep)))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_select_drafts: null pointer");
   spexis::SelectParams p{};
   p.qsl = query_start_loc;
   p.conf = draft_conf;
@@ -400,12 +400,12 @@ size_t spexis_linear_workspace_size(int32_t rows, int32_t out_features, int32_t 
 
 int spexis_linear(const void* x, const void* weight, const void* residual, int32_t rows, int32_t out_features,
                   int32_t in_features, void* y, void* workspace, size_t workspace_bytes, void* stream) {
-  if (!x || !weight || !y) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_linear: null pointer");
   if (rows < 0 || out_features <= 0 || in_features <= 0)
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_linear: bad size");
   if (in_features % 256 != 0)
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_linear: in_features %d is not a multiple of 256", in_features);
   if (rows == 0) return ok();
+  if (!x || !weight || !y) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_linear: null pointer");
   const int64_t tiles = (out_features + spexis::kLmCols - 1) / spexis::kLmCols;
   if (spexis::projection_workgroups(rows, out_features) + 8 * rows >= (1ll << 31) ||
       (int64_t)rows * out_features >= (1ll << 36) ||
@@ -474,7 +474,6 @@ size_t spexis_lm_head_stats_size(int32_t rows, int32_t vocab) {
 
 int spexis_lm_head(const void* hidden, const void* weight, int32_t rows, int32_t vocab, int32_t hidden_dim,
                    float temperature, float* logits, float* stats, void* stream) {
-  if (!hidden || !weight || !stats) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lm_head: null pointer");
   if (rows < 0 || vocab <= 0 || hidden_dim <= 0)
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lm_head: bad size");
   if (!(temperature > 0.f) || !std::isfinite(temperature))
@@ -482,6 +481,7 @@ int spexis_lm_head(const void* hidden, const void* weight, int32_t rows, int32_t
   if (hidden_dim % 256 != 0)
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_lm_head: hidden_dim %d is not a multiple of 256", hidden_dim);
   if (rows == 0) return ok();
+  if (!hidden || !weight || !stats) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lm_head: null pointer");
   const int64_t tiles = spexis_lm_head_tiles(vocab);
   if (spexis::projection_workgroups(rows, vocab) + 8 * rows >= (1ll << 31) || (int64_t)rows * vocab >= (1ll << 40))
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_lm_head: problem too large");

@@ -443,3 +443,38 @@ def test_boundary_errors_on_gpu():
                          acc.u_accept, acc.u_sample, batch.max_k, step.accepted_len, step.out_tokens,
                          step.row_status, step.acc_ws, temperature=0.0)
     assert e.value.code == sx.SPEXIS_ERR_INVALID_ARGUMENT
+
+
+def test_empty_batches_return_ok_and_touch_nothing():
+    # no sequences or no rows: every entry point returns OK without reading or writing a buffer
+    # (zero-element tensors pass NULL pointers); the outputs and pools keep their contents
+    dev = "cuda"
+    i32 = lambda *s: torch.full(s, 77, dtype=torch.int32, device=dev)
+    bf = lambda *s: torch.empty(s, dtype=torch.bfloat16, device=dev)
+    f32 = lambda *s: torch.full(s, 0.25, dtype=torch.float32, device=dev)
+    none8 = torch.empty(0, dtype=torch.uint8, device=dev)
+    k_pool = torch.full((4, 2, 16, 64), 1.5, dtype=torch.bfloat16, device=dev)
+    v_pool = k_pool.clone()
+    qsl0 = torch.zeros(1, dtype=torch.int32, device=dev)
+    sx.spexis_append_kv(k_pool, v_pool, 4, 2, 16, 64, qsl0, i32(0), i32(0, 4), 0, 1, bf(0, 2, 64), bf(0, 2, 64))
+    sx.spexis_verify_attention(k_pool, v_pool, 4, 2, 16, 64, qsl0, i32(0), i32(0, 4), 0, 1, 16, bf(0, 4, 64), 4,
+                               0.125, bf(0, 4, 64), workspace=None)
+    V = 100
+    for kind in (sx.SPEXIS_INPUT_PROBS, sx.SPEXIS_INPUT_LOGITS):
+        sx.spexis_accept(kind, qsl0, f32(0, V), f32(0, V), i32(0), f32(0), f32(0), 2, i32(0), i32(0, 3), i32(0),
+                         none8)
+    sx.spexis_accept_with_stats(qsl0, f32(0, V), f32(0, V), f32(0, 1, 2), f32(0, 1, 2), i32(0), f32(0), f32(0), 2,
+                                i32(0), i32(0, 3), i32(0), none8)
+    sx.spexis_softmax_rows(f32(0, V), f32(0, V))
+    sx.spexis_sample_tokens(sx.SPEXIS_INPUT_LOGITS, f32(0, V), f32(0), i32(0), i32(0), none8)
+    kept_qsl = i32(1)
+    sx.spexis_select_drafts(qsl0, f32(0), 0.3, i32(0), kept_qsl, i32(0))
+    g = torch.Generator().manual_seed(1)
+    w_lm = sx.spexis_pack_weight(torch.randn((V, 256), generator=g).to(torch.bfloat16).cuda())
+    w_lin = sx.spexis_pack_weight(torch.randn((64, 256), generator=g).to(torch.bfloat16).cuda())
+    sx.spexis_lm_head(bf(0, 256), w_lm, f32(0, 1, 2), logits=f32(0, V))
+    sx.spexis_linear(bf(0, 256), w_lin, bf(0, 64))
+    torch.cuda.synchronize()
+    assert (k_pool == 1.5).all() and (v_pool == 1.5).all()
+    assert kept_qsl.item() == 77
+    say("[empty] every entry point accepted an empty batch")
