@@ -6,14 +6,16 @@
 
 namespace spexis {
 
-// One workgroup per (sequence, KV head); its four waves take the sequence's tokens in turn.
-// K rows: D/8 lanes each move one 16-byte chunk (eight head-dim values) of a token.
-// V rows: 2-byte stores, head-dim index d at slot position swap23(slot).
+// One workgroup per (sequence, KV head).  Its threads take (token, 16-byte chunk) pairs of the
+// sequence's new K and V rows -- n * D/8 chunks of each -- so that the workgroup's loads are
+// issued together (five rows of D = 128: 160 chunks, one per thread), not one token per wave
+// in turn.  K chunks keep their 16 bytes together (the K layout holds 8 head-dim values of a
+// slot contiguously); V values go to slot position swap23(slot) of each head-dim row.
 template <int D, int BS>
 __global__ __launch_bounds__(256) void append_kv_kernel(AppendParams p) {
+  constexpr int kCh = D / 8;
   const int b = blockIdx.x / p.hkv;
   const int h = blockIdx.x % p.hkv;
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int q0 = clampi(p.qsl[b], 0, p.total_tokens);
   const int q1 = clampi(p.qsl[b + 1], q0, p.total_tokens);
   const int cap = p.max_blocks * BS;
@@ -24,19 +26,20 @@ __global__ __launch_bounds__(256) void append_kv_kernel(AppendParams p) {
   const uint16_t* nv = reinterpret_cast<const uint16_t*>(p.new_v);
   uint16_t* kc = reinterpret_cast<uint16_t*>(p.k_cache);
   uint16_t* vc = reinterpret_cast<uint16_t*>(p.v_cache);
-  for (int j = wave; j < n; j += 4) {
+  for (int c = threadIdx.x; c < 2 * n * kCh; c += 256) {
+    const int which = c / (n * kCh), rc = c % (n * kCh), j = rc / kCh, ch = rc % kCh;
     const int pos = L + j;
+    const u32x4 v = ld16((which ? nv : nk) + ((int64_t)(q0 + j) * p.hkv + h) * D + 8 * ch);
     const int blk = clampi(p.block_tables[(int64_t)b * p.max_blocks + pos / BS], 0, p.num_blocks - 1);
     const int slot = pos % BS;
-    const int64_t src = ((int64_t)(q0 + j) * p.hkv + h) * D;
     const int64_t head = (int64_t)blk * p.hkv + h;
-    if (lane < D / 8) {
-      u32x4 v = ld16(nk + src + lane * 8);
-      st16(kc + ((head * (D / 8) + lane) * BS + slot) * 8, v);
-    }
-    const int vslot = (slot & ~12) | (((slot >> 2) & 1) << 3) | (((slot >> 3) & 1) << 2);
+    if (which == 0) {
+      st16(kc + ((head * kCh + ch) * BS + slot) * 8, v);
+    } else {
+      const int vslot = (slot & ~12) | (((slot >> 2) & 1) << 3) | (((slot >> 3) & 1) << 2);
 #pragma unroll
-    for (int d = lane; d < D; d += kWave) vc[(head * D + d) * BS + vslot] = nv[src + d];
+      for (int e = 0; e < 8; ++e) vc[(head * D + 8 * ch + e) * BS + vslot] = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
+    }
   }
 }
 
