@@ -74,11 +74,11 @@ __device__ __forceinline__ void tile_of(int bid, int ntiles, int groups, int& nt
 }  // namespace
 
 // Waves form a WR x WC grid over the workgroup's (32 * WR * RT) rows x (32 * WC * CT) columns:
-// wave (wr, wc) computes RT row tiles x CT column tiles.  One column of waves (WR = 1) with one
-// column tile each suits few rows; for more rows, two column tiles per wave (256 columns per
-// workgroup) halve the h fragments each wave reads from LDS per MFMA, and halve the h rows
-// staged per column.  (A 2 x 2 grid over 128 columns does the former but loads each W tile
-// twice.)  Statistics stay per 128-column tile: a 256-column workgroup writes two.
+// wave (wr, wc) computes RT row tiles x CT column tiles.  The launched shapes put the four waves
+// side by side (WR = 1) with two column tiles each (256 columns per workgroup): against one tile
+// each, that halves the h fragments each wave reads from LDS per MFMA and the h rows staged per
+// column.  (A 2 x 2 grid over 128 columns does the former but loads each W tile twice.)
+// Statistics stay per 128-column tile: a 256-column workgroup writes two.
 template <bool kStream, int RT, int CT, int WR, int NA, int DEPTH, int WPE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE)))
 void lm_head_kernel(LmParams p) {
@@ -329,24 +329,26 @@ static int64_t group_rows(int64_t M) {
 }
 
 int64_t projection_workgroups(int64_t M, int64_t N) {
-  // the shapes launch_projection picks: 128-column workgroups of one row group up to 128 rows,
-  // groups of 160 or 192 rows x 256 columns beyond
-  if (M <= 128) return (N + kLmCols - 1) / kLmCols;
+  // the shapes launch_projection picks: 256-column workgroups throughout, one row group up to 128
+  // rows, groups of 160 or 192 rows beyond
+  if (M <= 128) return (N + 255) / 256;
   return (N + 255) / 256 * ((M + group_rows(M) - 1) / group_rows(M));
 }
 
 hipError_t launch_projection(const LmParams& p, hipStream_t s) {
   // row tiles computed per workgroup: the smallest instantiated count covering the rows (a
   // group of fewer rows repeats its last row in the padding tiles, whose results are dropped).
-  // Few rows: one column of waves, 128 columns, deep pipelines (the weight stream is the bound).
-  // More rows: groups of 160 or 192 rows x 256 columns (group_rows).  There every load -- h from
-  // L2, W from HBM -- is an L1 miss, and each CU's capacity for pending misses bounds the
-  // streams, so larger tiles' fewer requests per MFMA pay (measured at 320 x 4096 @ 128256:
-  // 437 us against 460 for 320 x 128 workgroups on a 2 x 2 wave grid).
+  // Every shape is 256 columns wide: four waves across, each two column tiles of 32.  Up to 64
+  // rows, a hint of two waves per SIMD; more rows take more accumulators and one.  Beyond 128
+  // rows, groups of 160 or 192 rows (group_rows).  Every load -- h from L2, W from HBM -- is an L1 miss, and each
+  // CU's capacity for pending misses bounds the streams, so wider tiles' fewer requests per MFMA
+  // pay: at 4096 @ 128256, 180 against 188 us for 128-column workgroups at 32 rows, 190 against
+  // 205 at 64, 215 against 265 at 128, and at 320 rows 437 against 460 us for 320 x 128
+  // workgroups on a 2 x 2 wave grid.
   const int need = (p.M + 31) / 32;
-  if (need <= 1) return launch_lm_nrt<1, 1, 1, 4, 8, 2>(p, s);
-  if (need <= 2) return launch_lm_nrt<2, 1, 1, 4, 8, 2>(p, s);
-  if (need <= 4) return launch_lm_nrt<4, 1, 1, 4, 8, 1>(p, s);
+  if (need <= 1) return launch_lm_nrt<1, 2, 1, 2, 4, 2>(p, s);
+  if (need <= 2) return launch_lm_nrt<2, 2, 1, 2, 4, 2>(p, s);
+  if (need <= 4) return launch_lm_nrt<4, 2, 1, 2, 4, 1>(p, s);
   if (group_rows(p.M) == 192) return launch_lm_nrt<6, 2, 1, 2, 4, 1>(p, s);
   return launch_lm_nrt<5, 2, 1, 2, 4, 1>(p, s);
 }
