@@ -328,24 +328,36 @@ static int64_t group_rows(int64_t M) {
   return p192 * 20 <= p160 * 21 ? 192 : 160;
 }
 
+// Up to 128 rows, 256-column workgroups when the columns alone give at least one workgroup per
+// CU (an LM head's vocabulary); narrower outputs (hidden-size projections) keep 128 columns, whose
+// twice as many workgroups the K split then fills the chip with.
+static bool wide_columns(int64_t M, int64_t N) { return M > 128 || (N + 255) / 256 >= 256; }
+
 int64_t projection_workgroups(int64_t M, int64_t N) {
-  // the shapes launch_projection picks: 256-column workgroups throughout, one row group up to 128
-  // rows, groups of 160 or 192 rows beyond
-  if (M <= 128) return (N + 255) / 256;
-  return (N + 255) / 256 * ((M + group_rows(M) - 1) / group_rows(M));
+  // the shapes launch_projection picks: one row group up to 128 rows, groups of 160 or 192 rows
+  // beyond
+  const int64_t cols = wide_columns(M, N) ? (N + 255) / 256 : (N + kLmCols - 1) / kLmCols;
+  if (M <= 128) return cols;
+  return cols * ((M + group_rows(M) - 1) / group_rows(M));
 }
 
 hipError_t launch_projection(const LmParams& p, hipStream_t s) {
   // row tiles computed per workgroup: the smallest instantiated count covering the rows (a
   // group of fewer rows repeats its last row in the padding tiles, whose results are dropped).
-  // Every shape is 256 columns wide: four waves across, each two column tiles of 32.  Up to 64
-  // rows, a hint of two waves per SIMD; more rows take more accumulators and one.  Beyond 128
-  // rows, groups of 160 or 192 rows (group_rows).  Every load -- h from L2, W from HBM -- is an L1 miss, and each
-  // CU's capacity for pending misses bounds the streams, so wider tiles' fewer requests per MFMA
-  // pay: at 4096 @ 128256, 180 against 188 us for 128-column workgroups at 32 rows, 190 against
-  // 205 at 64, 215 against 265 at 128, and at 320 rows 437 against 460 us for 320 x 128
-  // workgroups on a 2 x 2 wave grid.
+  // Wide shapes are 256 columns: four waves across, each two column tiles of 32 (wide_columns).
+  // Up to 64 rows, a hint of two waves per SIMD; more rows take more accumulators and one.
+  // Beyond 128 rows, groups of 160 or 192 rows (group_rows).  Every load -- h from L2, W from
+  // HBM -- is an L1 miss, and each CU's capacity for pending misses bounds the streams, so wider
+  // tiles' fewer requests per MFMA pay: at 4096 @ 128256, 180 against 188 us for 128-column
+  // workgroups at 32 rows, 190 against 205 at 64, 215 against 265 at 128, and at 320 rows 437
+  // against 460 us for 320 x 128 workgroups on a 2 x 2 wave grid.  Narrow outputs: 128 columns,
+  // one column tile per wave.
   const int need = (p.M + 31) / 32;
+  if (!wide_columns(p.M, p.V)) {
+    if (need <= 1) return launch_lm_nrt<1, 1, 1, 4, 8, 2>(p, s);
+    if (need <= 2) return launch_lm_nrt<2, 1, 1, 4, 8, 2>(p, s);
+    return launch_lm_nrt<4, 1, 1, 4, 8, 1>(p, s);
+  }
   if (need <= 1) return launch_lm_nrt<1, 2, 1, 2, 4, 2>(p, s);
   if (need <= 2) return launch_lm_nrt<2, 2, 1, 2, 4, 2>(p, s);
   if (need <= 4) return launch_lm_nrt<4, 2, 1, 2, 4, 1>(p, s);

@@ -78,6 +78,25 @@ def test_lm_head_small_shapes(rows, V, d):
     check(h, hb, w, wb, 0.8)
 
 
+@pytest.mark.parametrize("rows", [1, 40, 64, 100])
+def test_lm_head_few_rows_wide_vocabulary(rows):
+    # up to 128 rows, a vocabulary of at least 256 x 256 columns takes the 256-column
+    # workgroups (two column tiles per wave); 70001 leaves a ragged last tile
+    V, d = 70001, 256
+    h, hb = bf16_pair((rows, d), 11, 1.0)
+    w, wb = bf16_pair((V, d), 12, 0.05)
+    say(f"[lm head] rows={rows} V={V} d={d}")
+    check(h, hb, w, wb, 0.9)
+
+
+def test_lm_head_four_row_tiles_narrow_vocabulary():
+    rows, V, d = 100, 5000, 256
+    h, hb = bf16_pair((rows, d), 13, 1.0)
+    w, wb = bf16_pair((V, d), 14, 0.05)
+    say(f"[lm head] rows={rows} V={V} d={d}")
+    check(h, hb, w, wb, 1.1)
+
+
 def test_lm_head_statistics_only_and_extreme_logits():
     rows, V, d = 64, 5000, 256
     h, hb = bf16_pair((rows, d), 3, 4.0)        # large logits: the maximum dominates each tile
