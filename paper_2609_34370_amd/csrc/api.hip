@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <numeric>
 #include <string>
 
 #include "kernels.h"
@@ -46,18 +47,39 @@ constexpr int kMaxVocab = 1 << 22; // keeps sum W_v < 2^63 (W_v < 2^41)
 bool bad_cache_shape(int32_t bs, int32_t d) { return !((bs == 16 || bs == 32) && (d == 64 || d == 128)); }
 
 // Shares per KV head, grid waves and the 32-key tiles of a share.  kv_chunk_tokens = 0: about
-// kAttnMaxWaves waves split each head's tiles evenly (at least kAttnMinTilesPerWave each);
-// otherwise every share takes ceil(kv_chunk_tokens / 32) tiles and there are enough shares for
-// the most tiles that max_seq_len allows.  (The kernel widens the shares if the sequences hold
-// more.)
+// kAttnMaxWaves waves split each head's tiles evenly (at least kAttnMinTilesPerWave each), in
+// pairs of shares whose waves run on XCDs of opposite parity, the even one kAttnXcdSkew / 1024
+// longer (skew); otherwise every share takes ceil(kv_chunk_tokens / 32) tiles and there are
+// enough shares for the most tiles that max_seq_len allows.  (The kernel widens the shares if the
+// sequences hold more.)
 bool attn_waves(int32_t num_seqs, int32_t num_kv_heads, int32_t max_seq_len, int32_t req, int* tpw,
-                int* nshares, int* nwaves) {
+                int* nshares, int* nwaves, int* skew) {
   const int64_t max_tiles = (int64_t)num_seqs * ((max_seq_len + 31) / 32);   // per KV head
   const int64_t per = req > 0 ? ((int64_t)req + 31) / 32 : spexis::kAttnMinTilesPerWave;
-  int64_t sh = (max_tiles + per - 1) / per;
-  if (req == 0) sh = std::min<int64_t>(sh, std::max(1, spexis::kAttnMaxWaves / num_kv_heads));
-  sh = std::max<int64_t>(sh, 1);
-  const int64_t w = round_up(sh * num_kv_heads, 4);
+  int64_t sh = std::max<int64_t>((max_tiles + per - 1) / per, 1);
+  int64_t w;
+  *skew = 0;
+  if (req == 0) {
+    sh = std::min<int64_t>(sh, std::max(1, spexis::kAttnMaxWaves / num_kv_heads));
+    if (sh >= 2 && spexis::kAttnXcdSkew > 0) {
+      // paired shares: an even count per head, and a grid whose waves map one to one onto
+      // (share, head) (a multiple of 8 waves and of 2 hkv), kept within one wave per SIMD
+      const int64_t L = std::lcm<int64_t>(8, 2 * (int64_t)num_kv_heads);
+      int64_t s2 = sh & ~(int64_t)1;
+      while (s2 > 2 && round_up(s2 * num_kv_heads, L) > spexis::kAttnMaxWaves) s2 -= 2;
+      if (round_up(s2 * num_kv_heads, L) <= spexis::kAttnMaxWaves) {
+        sh = s2;
+        w = round_up(sh * num_kv_heads, L);
+        *skew = spexis::kAttnXcdSkew;
+      } else {
+        w = round_up(sh * num_kv_heads, 4);
+      }
+    } else {
+      w = round_up(sh * num_kv_heads, 4);
+    }
+  } else {
+    w = round_up(sh * num_kv_heads, 4);
+  }
   *tpw = req > 0 ? (int)per : 0;
   *nshares = (int)std::min<int64_t>(sh, 1 << 30);
   *nwaves = (int)std::min<int64_t>(w, 1 << 30);
@@ -128,8 +150,8 @@ size_t spexis_verify_attention_workspace_size(int32_t num_seqs, int32_t num_q_he
                                               int32_t kv_chunk_tokens) {
   if (num_seqs <= 0 || num_kv_heads <= 0 || num_q_heads <= 0 || max_query_len <= 0 || max_seq_len <= 0)
     return 0;
-  int tpw, nshares, nwaves;
-  if (!attn_waves(num_seqs, num_kv_heads, max_seq_len, kv_chunk_tokens, &tpw, &nshares, &nwaves)) return 0;
+  int tpw, nshares, nwaves, skew;
+  if (!attn_waves(num_seqs, num_kv_heads, max_seq_len, kv_chunk_tokens, &tpw, &nshares, &nwaves, &skew)) return 0;
   const int rmax = (num_q_heads / num_kv_heads) * max_query_len;
   return (size_t)spexis::attn_ws_bytes(nwaves, rmax, head_dim);
 }
@@ -166,8 +188,8 @@ int spexis_verify_attention(const void* k_cache, const void* v_cache, int32_t nu
   if (!k_cache || !v_cache || !query_start_loc || !seq_lens || !block_tables || !q || !out)
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: null pointer");
   if (q == out) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_attention: out aliases q");
-  int tpw, nshares, nwaves;
-  if (!attn_waves(num_seqs, num_kv_heads, max_seq_len, kv_chunk_tokens, &tpw, &nshares, &nwaves))
+  int tpw, nshares, nwaves, skew;
+  if (!attn_waves(num_seqs, num_kv_heads, max_seq_len, kv_chunk_tokens, &tpw, &nshares, &nwaves, &skew))
     return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_verify_attention: kv_chunk_tokens %d asks for too many waves",
                 kv_chunk_tokens);
   const size_t need = spexis_verify_attention_workspace_size(num_seqs, num_q_heads, num_kv_heads, head_dim,
@@ -197,6 +219,7 @@ int spexis_verify_attention(const void* k_cache, const void* v_cache, int32_t nu
   p.tiles_per_wave = tpw;
   p.nshares = nshares;
   p.nwaves = nwaves;
+  p.skew = skew;
   p.scale_log2e = (float)((double)scale * 1.4426950408889634);
   return hip_result(spexis::launch_attention(p, (hipStream_t)stream), "spexis_verify_attention");
 }

@@ -86,6 +86,19 @@ __device__ __forceinline__ void advance(const AttnParams& p, Cursor& c) {
   c.S = g.S;
 }
 
+// Share geometry of a head's tile stream: shares pair up, shares 2j and 2j+1 covering tiles
+// [2jP, 2(j+1)P), the first (the wave on an even XCD) P + dlt of them and the second P - dlt.
+// dlt = 0 gives equal shares of P.
+__device__ __forceinline__ int share_delta(int P, int skew) { return (int)(((int64_t)P * skew) >> 10); }
+__device__ __forceinline__ int64_t share_first(int s, int P, int dlt) {
+  return (int64_t)(s >> 1) * 2 * P + (s & 1) * (P + dlt);
+}
+__device__ __forceinline__ int share_size(int s, int P, int dlt) { return (s & 1) ? P - dlt : P + dlt; }
+__device__ __forceinline__ int share_of(int g, int P, int dlt) {
+  const int j = g / (2 * P);
+  return 2 * j + (g - 2 * P * j >= P + dlt ? 1 : 0);
+}
+
 template <int D, int BS, int NT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1)))
 void verify_attn_kernel(AttnParams p) {
@@ -94,7 +107,23 @@ void verify_attn_kernel(AttnParams p) {
   // Tiles in flight: the register file of one wave per SIMD holds DEPTH operand buffers.
   constexpr int DEPTH = NT == 1 ? 3 : 2;
   const int lane = threadIdx.x & 63, col = lane & 31, half = lane >> 5;
-  const int wid = __builtin_amdgcn_readfirstlane((int)blockIdx.x * 4 + (int)(threadIdx.x >> 6));
+  // Physical wave qw -> (share s, head h); wid = s * hkv + h names its partial slots and header.
+  // Paired shares (skew > 0): workgroups alternate between the XCDs of even and odd index, and
+  // wave qw = 8m + 4 par + r takes u = 4m + r: share 2 (u / hkv) + par of head u % hkv.  So the
+  // two shares of each pair run on XCDs of opposite parity, and the four waves of a workgroup
+  // take neighbouring heads of one share.  The host makes nwaves a multiple of 8 and of 2 hkv,
+  // which makes the map a bijection of [0, nwaves).
+  const int qw = __builtin_amdgcn_readfirstlane((int)blockIdx.x * 4 + (int)(threadIdx.x >> 6));
+  int s_, h_;
+  if (p.skew > 0) {
+    const int u = ((qw >> 3) << 2) | (qw & 3);
+    s_ = 2 * (u / p.hkv) + ((qw >> 2) & 1);
+    h_ = u % p.hkv;
+  } else {
+    s_ = qw / p.hkv;
+    h_ = qw % p.hkv;
+  }
+  const int wid = s_ * p.hkv + h_;
   const int64_t slot_f = attn_slot_floats(p.rmax, D);
   float* slots = p.ws + (int64_t)wid * 2 * slot_f;
   int32_t* hdr = reinterpret_cast<int32_t*>(p.ws + (int64_t)p.nwaves * 2 * slot_f) + (int64_t)wid * kAttnHdrInts;
@@ -102,7 +131,7 @@ void verify_attn_kernel(AttnParams p) {
   auto no_share = [&]() {
     if (lane == 0) *reinterpret_cast<u32x4*>(hdr) = u32x4{0u, 0u, 0u, 0u};
   };
-  const int h = wid % p.hkv, share = wid / p.hkv;
+  const int h = h_, share = s_;
   if (share >= p.nshares) return no_share();
 
   // ---- this wave's share [g0, g0 + cnt) of head h's tile stream
@@ -115,8 +144,8 @@ void verify_attn_kernel(AttnParams p) {
     total = __builtin_amdgcn_readlane(incl, kWave - 1);   // < 2^31 (host)
     const int even = (total + p.nshares - 1) / p.nshares;
     const int P = max(p.tiles_per_wave > 0 ? p.tiles_per_wave : kAttnMinTilesPerWave, even);
-    if ((int64_t)share * P >= total) return no_share();
-    const int g0 = share * P;
+    if (share_first(share, P, share_delta(P, p.skew)) >= total) return no_share();
+    const int g0 = (int)share_first(share, P, share_delta(P, p.skew));
     const uint64_t hit = __builtin_amdgcn_ballot_w64(incl > g0);
     if (hit == 0) return no_share();
     const int l0 = __builtin_ctzll(hit);
@@ -133,8 +162,8 @@ void verify_attn_kernel(AttnParams p) {
     total = __builtin_amdgcn_readfirstlane(wave_sum_i32(per_lane));   // < 2^31 (host)
     const int even = (total + p.nshares - 1) / p.nshares;
     const int P = max(p.tiles_per_wave > 0 ? p.tiles_per_wave : kAttnMinTilesPerWave, even);
-    if ((int64_t)share * P >= total) return no_share();
-    const int g0 = share * P;
+    if (share_first(share, P, share_delta(P, p.skew)) >= total) return no_share();
+    const int g0 = (int)share_first(share, P, share_delta(P, p.skew));
     // the sequence holding tile g0, and the stream index of its first tile
     int before = 0;
     for (int base = 0; base < p.num_seqs; base += kWave) {
@@ -161,8 +190,9 @@ void verify_attn_kernel(AttnParams p) {
   }
   const int P = max(p.tiles_per_wave > 0 ? p.tiles_per_wave : kAttnMinTilesPerWave,
                     (total + p.nshares - 1) / p.nshares);
-  const int g0 = share * P;
-  const int cnt = min(P, total - g0);
+  const int dlt = share_delta(P, p.skew);
+  const int g0 = (int)share_first(share, P, dlt);
+  const int cnt = min(share_size(share, P, dlt), total - g0);
 
   const uint16_t* kc = reinterpret_cast<const uint16_t*>(p.k_cache);
   const uint16_t* vc = reinterpret_cast<const uint16_t*>(p.v_cache);
@@ -421,7 +451,7 @@ void verify_attn_kernel(AttnParams p) {
   // header of the slot-1 partial: the item this wave starts and a later share finishes
   if (lane == 0) {
     *reinterpret_cast<u32x4*>(hdr) = u32x4{(uint32_t)head_flag, (uint32_t)head_b, (uint32_t)head_f, (uint32_t)head_nt};
-    *reinterpret_cast<u32x4*>(hdr + 4) = u32x4{(uint32_t)P, (uint32_t)head_q0, (uint32_t)head_n, 0u};
+    *reinterpret_cast<u32x4*>(hdr + 4) = u32x4{(uint32_t)P, (uint32_t)head_q0, (uint32_t)head_n, (uint32_t)dlt};
   }
 }
 
@@ -439,9 +469,9 @@ __global__ __launch_bounds__(512) void attn_merge_kernel(AttnParams p) {
   const u32x4 h0 = *reinterpret_cast<const u32x4*>(hdr);
   const u32x4 h1 = *reinterpret_cast<const u32x4*>(hdr + 4);   // loaded with h0: one round trip
   if (h0[0] != 1u) return;
-  const int f = (int)h0[2], nt = (int)h0[3], P = (int)h1[0], q0 = (int)h1[1], n = (int)h1[2];
+  const int f = (int)h0[2], nt = (int)h0[3], P = (int)h1[0], q0 = (int)h1[1], n = (int)h1[2], dlt = (int)h1[3];
   const int h = w % p.hkv, s0 = w / p.hkv;
-  const int C = min((f + nt - 1) / P, p.nshares - 1) - s0 + 1;   // contributing shares
+  const int C = min(share_of(f + nt - 1, P, dlt), p.nshares - 1) - s0 + 1;   // contributing shares
   const int R = p.group * n;
   const int64_t mo = (int64_t)p.rmax * D, lo = mo + p.rmax;
   auto slot = [&](int c) -> const float* {

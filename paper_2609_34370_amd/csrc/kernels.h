@@ -32,12 +32,16 @@ struct AttnParams {
   int tiles_per_wave;    // 32-key tiles per share; 0: the even split of each head's tiles
   int nshares;           // shares per KV head; wave s*hkv + h takes share s of head h
   int nwaves;            // waves of the attention grid (4 per workgroup, >= nshares * hkv)
+  int skew;              // 0: equal shares; else paired shares, the even-XCD one skew/1024 longer
   float scale_log2e;     // scale * log2(e): scores live in the base-2 domain
 };
 
 constexpr int kAttnHdrInts = 8;           // per-wave header of the partial an item's first wave leaves
 constexpr int kAttnMinTilesPerWave = 2;   // floor of the even split (short batches)
 constexpr int kAttnMaxWaves = 1024;       // waves of the even split: one per SIMD of 256 CUs
+// Tiles moved, per 1024, from the share of each pair on an odd XCD to the one on an even XCD:
+// waves on odd XCDs stream the cache a few per cent slower.
+constexpr int kAttnXcdSkew = 28;
 
 // One partial slot: [rmax][D] unnormalised output, then rmax reference maxima and rmax sums.
 // Rounded up to 16 floats so that every slot starts 64-byte aligned.

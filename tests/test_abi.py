@@ -2,6 +2,7 @@
 bad scalar arguments on the host with the documented codes (no GPU needed: validation
 returns before any device call)."""
 import ctypes
+import math
 import os
 import subprocess
 
@@ -63,20 +64,29 @@ def test_attention_validation():
 
 def test_workspace_queries():
     # attention: one header and two partial slots per wave; each KV head's tiles are cut into
-    # shares (the even split: about 1024 waves in all, at least 2 tiles a share; a fixed share
-    # size: enough shares for the largest possible stream), one wave per (share, head)
+    # shares (the even split: about 1024 waves in all, at least 2 tiles a share, shares in pairs
+    # and a grid of a multiple of 8 and of 2 hkv waves within 1024; a fixed share size: enough
+    # shares for the largest possible stream), one wave per (share, head)
     def expect(B, hq, hkv, D, mq, max_s, chunk):
         rows = (hq // hkv) * mq
         slot = -(-rows * (D + 2) // 16) * 16
         tiles = B * -(-max_s // 32)
         per = -(-chunk // 32) if chunk else 2
-        shares = -(-tiles // per)
+        shares = max(-(-tiles // per), 1)
+        step = 4
         if not chunk:
             shares = min(shares, max(1, 1024 // hkv))
-        waves = -(-(shares * hkv) // 4) * 4
+            L = math.lcm(8, 2 * hkv)
+            s2 = shares - shares % 2
+            while s2 > 2 and -(-(s2 * hkv) // L) * L > 1024:
+                s2 -= 2
+            if shares >= 2 and -(-(s2 * hkv) // L) * L <= 1024:
+                shares, step = s2, L
+        waves = -(-(shares * hkv) // step) * step
         return waves * (2 * slot * 4 + 8 * 4)
     for args in [(4, 8, 2, 64, 5, 256, 0), (64, 32, 8, 128, 5, 4100, 0), (64, 32, 8, 128, 5, 4100, 100),
-                 (1, 8, 8, 128, 1, 1, 0), (3, 64, 8, 128, 8, 16384, 4096)]:
+                 (1, 8, 8, 128, 1, 1, 0), (3, 64, 8, 128, 8, 16384, 4096), (5, 24, 3, 128, 4, 3000, 0),
+                 (7, 12, 12, 64, 2, 700, 0), (2, 40, 5, 128, 3, 33, 0), (64, 300, 300, 64, 1, 4100, 0)]:
         n = sx.spexis_verify_attention_workspace_size(*args)
         assert n == expect(*args) and n % 64 == 0, args
     assert sx.spexis_verify_attention_workspace_size(64, 32, 8, 128, 5, 1 << 20, 0) <= 1024 * (2 * 2608 * 4 + 32)

@@ -118,6 +118,21 @@ def test_attention_head_dim_64_block_32_and_wide_groups():
     check_attention(1, 6, seed=8, batch=6, block_size=32, num_q_heads=16, num_kv_heads=2, k=("fixed", 7))
 
 
+@pytest.mark.parametrize("hq,hkv,D", [(4, 1, 128), (12, 3, 128), (20, 5, 64), (24, 12, 64)])
+def test_attention_kv_head_counts(hq, hkv, D):
+    # KV head counts whose grids round up to a multiple of 8 and of 2 Hkv waves (the map of
+    # waves onto (share, head) for paired shares), padding waves included
+    check_attention(1, 6, seed=30 + hkv, batch=12, num_q_heads=hq, num_kv_heads=hkv, head_dim=D,
+                    ctx=("uniform", 100, 2000), k=("uniform", 0, 5))
+
+
+def test_attention_skewed_share_pairs_odd_head_count():
+    # 3 KV heads: 336 shares per head in 1008 waves; about 12500 tiles per head make shares of
+    # 38 tiles, paired as 39 + 37, so every cut point moves off the equal split
+    check_attention(1, 8, seed=41, batch=40, num_q_heads=12, num_kv_heads=3, head_dim=128,
+                    ctx=("uniform", 9000, 11000), k=("fixed", 4))
+
+
 def test_attention_block_permutation_invariance():
     spec, batch, attn, _ = case(1, seed=9, accept=False, batch=5, ctx=("uniform", 40, 200))
     step = VerifyStep(batch, attn, None)
