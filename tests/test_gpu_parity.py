@@ -404,6 +404,98 @@ def test_accept_logits_edge_rows_across_rounds():
         assert borderline(p, q, ids, ua, us, qsl, b, ra[b], rt[b], a[b], t[b]), b
 
 
+def test_accept_most_drafts_every_round_odd_vocab():
+    # max_k = 32 (the largest the boundary takes): logits-mode rounds {0,1}, {2..5}, {6..13},
+    # {14..29}, {30..61}.  Sequence b has k_b drafts and a draft row equal to the target row at
+    # positions below m_b (those tests always pass), a noisy one after; the m_b sit on both sides
+    # of every round boundary.  V = 70001: rows of 280 KB (rounds), not a multiple of 4 entries.
+    V, K = 70001, 32
+    km = [(32, 32), (32, 31), (32, 30), (31, 31), (30, 29), (29, 14), (14, 13), (13, 6), (6, 5), (5, 2),
+          (2, 1), (1, 0), (0, 0), (32, 0), (20, 20), (7, 7)]
+    B = len(km)
+    k = np.array([x for x, _ in km])
+    rng = np.random.default_rng(23)
+    qsl = np.concatenate([[0], np.cumsum(k + 1)]).astype(np.int32)
+    T = int(qsl[-1])
+    tl = (rng.standard_normal((T, V)) * 2.5).astype(np.float32)
+    dl = np.empty((T - B, V), np.float32)
+    ids = np.empty(T - B, np.int32)
+    for b, (kb, m) in enumerate(km):
+        for i in range(kb):
+            r = qsl[b] - b + i
+            dl[r] = tl[qsl[b] + i] if i < m else tl[qsl[b] + i] + (rng.standard_normal(V) * 2).astype(np.float32)
+            g = dl[r].astype(np.float64) - np.log(-np.log(rng.random(V)))
+            ids[r] = int(np.argmax(g))
+    ua = rng.random(T - B, dtype=np.float32)
+    us = rng.random(B, dtype=np.float32)
+    dev = lambda x: torch.as_tensor(x, device="cuda")
+    p, q = oracle.softmax(tl, 1.0), oracle.softmax(dl, 1.0)
+    ra, rt, rs, _ = oracle.accept(qsl, p, q, ids, ua, us, max_k=K)
+    ws = torch.empty(sx.spexis_accept_workspace_size(B, V, K), dtype=torch.uint8, device="cuda")
+    for kind, tg, dr in ((sx.SPEXIS_INPUT_PROBS, p, q), (sx.SPEXIS_INPUT_LOGITS, tl, dl)):
+        accepted = torch.empty(B, dtype=torch.int32, device="cuda")
+        toks = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+        stat = torch.empty(B, dtype=torch.int32, device="cuda")
+        sx.spexis_accept(kind, dev(qsl), dev(tg), dev(dr), dev(ids), dev(ua), dev(us), K, accepted, toks, stat, ws,
+                         temperature=1.0)
+        torch.cuda.synchronize()
+        a, t, s = accepted.cpu().numpy(), toks.cpu().numpy(), stat.cpu().numpy()
+        say(f"[accept max_k] kind={kind} a={a.tolist()} oracle={ra.tolist()}")
+        assert (rs == 0).all()
+        np.testing.assert_array_equal(s, rs)
+        assert all(a[b] >= m for b, (_, m) in enumerate(km)), "an identical draft row must pass"
+        if kind == sx.SPEXIS_INPUT_PROBS:
+            np.testing.assert_array_equal(a, ra)
+            np.testing.assert_array_equal(t, rt)
+        else:
+            diff = [b for b in range(B) if a[b] != ra[b] or not np.array_equal(t[b], rt[b])]
+            assert len(diff) <= 1
+            for b in diff:
+                assert borderline(p, q, ids, ua, us, qsl, b, ra[b], rt[b], a[b], t[b]), b
+    assert (ra >= 30).sum() >= 3 and ra[0] == 32
+
+
+def test_accept_largest_vocabulary():
+    # V = 2^22, the largest vocabulary the boundary takes: fixed-point sums up to 2^22 weights of
+    # under 2^41 each; 3 sequences with k = 2, 0, 1, both input kinds.  Sequence 0's draft rows
+    # equal its target rows (both tests pass, the bonus row is sampled); sequence 2's are noisy.
+    V, K = 1 << 22, 2
+    k = np.array([2, 0, 1])
+    B = len(k)
+    rng = np.random.default_rng(29)
+    qsl = np.concatenate([[0], np.cumsum(k + 1)]).astype(np.int32)
+    T = int(qsl[-1])
+    tl = (rng.standard_normal((T, V)) * 1.5).astype(np.float32)
+    dl = (tl[[qsl[b] + i for b in range(B) for i in range(k[b])]] +
+          rng.standard_normal((T - B, V)).astype(np.float32) * 0.3)
+    dl[:2] = tl[:2]
+    ids = np.array([int(np.argmax(r)) for r in dl], np.int32)
+    ua = rng.random(T - B, dtype=np.float32)
+    us = rng.random(B, dtype=np.float32)
+    p, q = oracle.softmax(tl, 1.0), oracle.softmax(dl, 1.0)
+    ra, rt, rs, _ = oracle.accept(qsl, p, q, ids, ua, us, max_k=K)
+    dev = lambda x: torch.as_tensor(x, device="cuda")
+    ws = torch.empty(sx.spexis_accept_workspace_size(B, V, K), dtype=torch.uint8, device="cuda")
+    for kind, tg, dr in ((sx.SPEXIS_INPUT_PROBS, p, q), (sx.SPEXIS_INPUT_LOGITS, tl, dl)):
+        accepted = torch.empty(B, dtype=torch.int32, device="cuda")
+        toks = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+        stat = torch.empty(B, dtype=torch.int32, device="cuda")
+        sx.spexis_accept(kind, dev(qsl), dev(tg), dev(dr), dev(ids), dev(ua), dev(us), K, accepted, toks, stat, ws,
+                         temperature=1.0)
+        torch.cuda.synchronize()
+        a, t, s = accepted.cpu().numpy(), toks.cpu().numpy(), stat.cpu().numpy()
+        say(f"[accept V=2^22] kind={kind} a={a.tolist()} tokens={t.tolist()} oracle a={ra.tolist()} {rt.tolist()}")
+        np.testing.assert_array_equal(s, rs)
+        assert a[0] == 2
+        if kind == sx.SPEXIS_INPUT_PROBS:
+            np.testing.assert_array_equal(a, ra)
+            np.testing.assert_array_equal(t, rt)
+        else:
+            for b in range(B):
+                if a[b] != ra[b] or not np.array_equal(t[b], rt[b]):
+                    assert borderline(p, q, ids, ua, us, qsl, b, ra[b], rt[b], a[b], t[b]), b
+
+
 def test_accept_logits_empty_residual_falls_back_to_target_row():
     # Rejections whose residual is empty in fixed point, with logits.  Sequence 0: identical target
     # and draft rows with the drafted entry at -inf (p(x) = q(x) = 0 rejects), so max(0, p - q)
