@@ -424,17 +424,32 @@ __device__ __forceinline__ void wave_stats(float (&v)[kPerLane], float c, float&
   if (bad) z = NAN;
 }
 
-// Sequence li of round r's list: all sequences in round 0, the ones still accepting after.
-__device__ __forceinline__ void round_seq(const AcceptParams& p, int r, int li, int& b, Geom& g, int& n) {
+// Sequence b's rows and state for the decide launches (valid: 1 valid, 0 no query token, -1 a
+// draft id outside [0, V)), written once per sequence by the pass before the first decide launch
+// (the statistics or the gather pass).  That launch then reads one record per item instead of
+// query_start_loc and every draft id: a dependent round trip less for each of its items.
+__device__ __forceinline__ void store_geom_state(const AcceptParams& p, int b, const Geom& g, int bad_id) {
+  const int state = !g.valid ? 0 : bad_id ? -1 : 1;
+  *reinterpret_cast<u32x4*>(p.geo + 4 * (int64_t)b) = u32x4{(uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k, (uint32_t)state};
+}
+
+// Sequence li of round r's list: all sequences in round 0 (their stored record; with no drafts
+// at all there are no ids to check, and no pass before writes one), the ones still accepting
+// after.
+__device__ __forceinline__ void round_seq(const AcceptParams& p, int r, int li, int& b, Geom& g) {
   if (r == 0) {
     b = li;
-    g = seq_geom(p, b, n);
+    if (p.max_k == 0) {
+      int n;
+      g = seq_geom(p, b, n);
+    } else {
+      g = load_geom(p, b);
+    }
     return;
   }
   const u32x4 e = *reinterpret_cast<const u32x4*>(p.lists + ((int64_t)(r - 1) * p.B + li) * 4);
   b = (int)e[0];
   g = Geom{(int)e[1], (int)e[2], (int)e[3], 1};
-  n = g.k + 1;
 }
 
 __device__ __forceinline__ int round_count(const AcceptParams& p, int r) { return r == 0 ? p.B : p.counts[r]; }
@@ -524,12 +539,26 @@ __global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p, 
     const int pos = rr >> 1, which = rr & 1;
     int n;
     const Geom g = seq_geom(p, b, n);
-    if (!g.valid || pos > g.k || (which == 1 && pos == g.k)) continue;
+    const bool skip = !g.valid || pos > g.k || (which == 1 && pos == g.k);
+    float v[kPerLane];
+    if (!skip) {
+      const float* row = which ? p.draft + (int64_t)(g.d0 + pos) * p.V : p.target + (int64_t)(g.t0 + pos) * p.V;
+      load_sub<true>(row, sub, wave, p.V, (p.V & 3) == 0, -INFINITY, lane, v);
+    }
+    // the first item of each sequence records it for the decide launches (its id loads follow the
+    // row's, so they add no round trip)
+    if (rr == 0 && sub == 0 && wave == 0) {
+      int bad = 0;
+      for (int i = lane; i < g.k; i += kWave) {
+        const int x = p.ids[g.d0 + i];
+        bad |= x < 0 || x >= p.V;
+      }
+      bad = wave_or(bad);
+      if (lane == 0) store_geom_state(p, b, g, bad);
+    }
+    if (skip) continue;
     // the inputs of test pos, gathered here so that the decision needs no dependent gather
     if (which == 0 && pos < g.k && sub == 0 && threadIdx.x == 0) gather_test(p, b, g, pos);
-    const float* row = which ? p.draft + (int64_t)(g.d0 + pos) * p.V : p.target + (int64_t)(g.t0 + pos) * p.V;
-    float v[kPerLane];
-    load_sub<true>(row, sub, wave, p.V, (p.V & 3) == 0, -INFINITY, lane, v);
     store_sub_stats(p, v, lse_slot(p, b, pos, which), sub, wave, lane);
   }
 }
@@ -575,11 +604,21 @@ __global__ __launch_bounds__(kThreads) void accept_combine_kernel(const float* s
 
 // The inputs of every test, when the statistics are given and no stats pass gathers them.
 __global__ __launch_bounds__(kThreads) void accept_gather_kernel(AcceptParams p) {
+  // one thread per (sequence, draft position); max_k >= 1 (with no drafts there is nothing to
+  // gather or check)
   const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (idx >= (int64_t)p.B * p.max_k) return;
   const int b = (int)(idx / p.max_k), i = (int)(idx % p.max_k);
   int n;
   const Geom g = seq_geom(p, b, n);
+  if (i == 0) {
+    int bad = 0;
+    for (int j = 0; j < g.k; ++j) {
+      const int x = p.ids[g.d0 + j];
+      bad |= x < 0 || x >= p.V;
+    }
+    store_geom_state(p, b, g, bad);
+  }
   if (!g.valid || i >= g.k) return;
   gather_test(p, b, g, i);
 }
@@ -597,19 +636,12 @@ __global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p,
   for (int64_t item = blockIdx.x; item < total; item += gridDim.x) {
     const int sub = (int)(item % p.nsub), li = (int)(item / p.nsub);
     const bool lead = sub == 0 && threadIdx.x == 0;
-    int b, n;
+    int b;
     Geom g;
-    round_seq(p, r, li, b, g, n);
-    if (r == 0) {
-      int bad = !g.valid;
-      for (int i = lane; i < g.k; i += kWave) {
-        const int x = p.ids[g.d0 + i];
-        bad |= x < 0 || x >= p.V;
-      }
-      if (wave_or(bad)) {
-        if (lead) write_invalid(p, b, n);
-        continue;
-      }
+    round_seq(p, r, li, b, g);
+    if (r == 0 && g.valid != 1) {   // no query token, or a draft id out of range
+      if (lead) write_invalid(p, b, g.valid == 0 ? 0 : 1);
+      continue;
     }
     // position i fails when !(u_i q_i(x_i) < p_i(x_i)) (NaN statistics fail)
     const f32x4* tin = reinterpret_cast<const f32x4*>(p.tin) + (int64_t)b * p.max_k;

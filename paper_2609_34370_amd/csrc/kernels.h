@@ -119,7 +119,8 @@ struct AcceptParams {
   int32_t* seq_lens_inout;
   float* tok_prob;       // [B] or null: probability of the emitted token under p at its position
   // workspace views
-  int32_t* geo;          // [B][4] first target row, first draft row, k, valid
+  int32_t* geo;          // [B][4] first target row, first draft row, k, state (1 valid; logits
+                         // mode: 0 no query token, -1 a draft id out of range; probabilities: 0 invalid)
   int32_t* st_a;         // [B] final a_b
   int32_t* st_mode;      // [B] 1 residual, 2 bonus, 3 done (outputs written)
   float* lse_part;       // [B][max_k+1][2 target/draft][nsub][2] (max, sum of 2^(y-max)) (logits mode)

@@ -185,3 +185,60 @@ def test_accept_with_fused_statistics_agrees_with_oracle():
             assert abs(float(ua[d0 + i]) * float(q[d0 + i, x]) - float(p[t0 + i, x])) <= 1e-4
     diff2 = [b for b in range(B) if a[b] != acc2.cpu().numpy()[b]]
     assert len(diff2) <= 1
+
+
+def test_accept_with_fused_statistics_flags_bad_draft_ids():
+    # a draft id past the vocabulary or negative marks its sequence (status 3, nothing accepted,
+    # tokens -1) on both acceptance paths; the other sequences decide as they would without it
+    rng = np.random.default_rng(31)
+    B, K, V, d, T = 6, 3, 3000, 256, 1.0
+    k = np.array([3, 0, 2, 3, 1, 3])
+    qsl = np.concatenate([[0], np.cumsum(k + 1)]).astype(np.int32)
+    Tt, Td = int(qsl[-1]), int(qsl[-1]) - B
+    w, _ = bf16_pair((V, d), 15, 0.08)
+    ht, _ = bf16_pair((Tt, d), 16, 1.0)
+    hd, _ = bf16_pair((Td, d), 17, 1.0)
+    tiles = sx.spexis_lm_head_tiles(V)
+    tl = torch.empty((Tt, V), dtype=torch.float32, device="cuda")
+    dl = torch.empty((Td, V), dtype=torch.float32, device="cuda")
+    ts = torch.empty((Tt, tiles, 2), dtype=torch.float32, device="cuda")
+    ds = torch.empty((Td, tiles, 2), dtype=torch.float32, device="cuda")
+    wp = sx.spexis_pack_weight(w.cuda())
+    sx.spexis_lm_head(ht.cuda(), wp, ts, logits=tl, temperature=T)
+    sx.spexis_lm_head(hd.cuda(), wp, ds, logits=dl, temperature=T)
+    ids = rng.integers(0, V, Td).astype(np.int32)
+    ua = rng.random(Td, dtype=np.float32)
+    us = rng.random(B, dtype=np.float32)
+    dev = lambda x: torch.as_tensor(x, device="cuda")
+    ws = torch.empty(sx.spexis_accept_workspace_size(B, V, K), dtype=torch.uint8, device="cuda")
+
+    def both(ids_h):
+        out = []
+        for fused in (True, False):
+            acc = torch.empty(B, dtype=torch.int32, device="cuda")
+            tok = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+            st = torch.empty(B, dtype=torch.int32, device="cuda")
+            if fused:
+                sx.spexis_accept_with_stats(dev(qsl), tl, dl, ts, ds, dev(ids_h), dev(ua), dev(us), K, acc, tok, st,
+                                            ws, temperature=T)
+            else:
+                sx.spexis_accept(sx.SPEXIS_INPUT_LOGITS, dev(qsl), tl, dl, dev(ids_h), dev(ua), dev(us), K, acc, tok,
+                                 st, ws, temperature=T)
+            torch.cuda.synchronize()
+            out.append((acc.cpu().numpy(), tok.cpu().numpy(), st.cpu().numpy()))
+        return out
+
+    clean = both(ids)
+    bad = ids.copy()
+    bad[qsl[0] - 0 + 2] = V + 5      # sequence 0, last draft
+    bad[qsl[3] - 3 + 0] = -2         # sequence 3, first draft
+    marked = both(bad)
+    for (a0, t0, s0), (a1, t1, s1) in zip(clean, marked):
+        assert (s0 == 0).all()
+        assert s1[0] == sx.SPEXIS_ROW_BAD_TOKEN and s1[3] == sx.SPEXIS_ROW_BAD_TOKEN
+        assert a1[0] == 0 and a1[3] == 0 and (t1[[0, 3]] == -1).all()
+        keep = [1, 2, 4, 5]
+        np.testing.assert_array_equal(a1[keep], a0[keep])
+        np.testing.assert_array_equal(t1[keep], t0[keep])
+        np.testing.assert_array_equal(s1[keep], 0)
+
