@@ -64,7 +64,7 @@ struct LmParams {
   float c;               // log2(e) / temperature
 };
 
-constexpr int kLmCols = 128;   // vocabulary columns per workgroup (four waves of 32)
+constexpr int kLmCols = 128;   // columns of a statistics tile, and of a narrow projection's workgroup
 constexpr int kLmK = 64;       // K per pipeline step (four MFMA k-steps)
 
 // Selective speculation over a batch of B sequences, T query tokens, N = T - B drafts.

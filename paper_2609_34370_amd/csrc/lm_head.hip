@@ -6,9 +6,10 @@
 //   stats = (max_v x*c, sum_v 2^(x*c - max))   over the tile's columns v < V.
 // Acceptance combines the tiles of a row into its normaliser without reading the row again.
 //
-// Work decomposition: one workgroup per (vocabulary tile of 128 columns, group of up to 320
-// rows of h); its four waves split the tile in a grid of waves (below), each holding 32x32
-// accumulator tiles of v_mfma_f32_32x32x16_bf16 (A operand: h rows, B operand: W rows).
+// Work decomposition: one workgroup per (vocabulary tile of 256 columns, or 128 for narrow
+// outputs; group of up to 192 rows of h, or all of up to 128 rows); its four waves split the
+// tile in a grid of waves (below), each holding 32x32 accumulator tiles of
+// v_mfma_f32_32x32x16_bf16 (A operand: h rows, B operand: W rows).
 //   * W, the stream that matters (V*d*2 bytes, read once), goes straight from HBM into each
 //     wave's registers, DEPTH K-steps of 64 ahead.  It is packed (pack.hip) so that each operand
 //     load of a wave reads 1 KB of contiguous memory; lane half h takes K = 32h + 8s .. +7 of
@@ -18,7 +19,8 @@
 //     registers NA steps ahead (NA register sets).  Wait counts retire in issue order: the wait
 //     for h step i+1 leaves the NA steps of W loaded after it in flight, and W runs DEPTH >=
 //     NA + 2 steps ahead, so the compute of step i+1 never waits for its W.  Few row tiles leave
-//     registers for NA = 4, DEPTH = 8; the full 320-row group uses NA = 2, DEPTH = 4.
+//     registers for NA = 4, DEPTH = 8 (one column tile per wave); two column tiles per wave and
+//     the larger row groups use NA = 2, DEPTH = 4.
 //   * Each XCD takes blocks of its vocabulary tiles x row groups (tile_of), so its resident
 //     workgroups share the K-slices of h and W they read through its L2.
 #include "common.h"
@@ -201,8 +203,8 @@ void lm_head_kernel(LmParams p) {
     }
   }
 
-  // ---- epilogue: logits (or partials, or bf16 outputs), and each row's statistics over this
-  // workgroup's 128 columns.  Accumulator value i of lane l in tile (t, c): row
+  // ---- epilogue: logits (or partials, or bf16 outputs), and each row's statistics over each
+  // of this workgroup's 128-column statistics tiles.  Accumulator value i of lane l in tile (t, c): row
   // 32 (wr RT + t) + 8 (i / 4) + 4 (l / 32) + i % 4, column 32 (CT wc + c) + l % 32.
   auto out_row = [&](int t, int i) { return 32 * (wr * RT + t) + 8 * (i >> 2) + 4 * half + (i & 3); };
   auto out_col = [&](int c) { return n0 + 32 * (CT * wc + c) + col; };
