@@ -16,7 +16,8 @@
  *   spexis_select_drafts     selective speculation: drop the least confident drafts first
  *   spexis_lookahead_memory  look-ahead KV-memory estimate of the running requests (Algorithm 1)
  *   spexis_linear            a linear layer of the drafting adapter (bf16, fp32 accumulation)
- *   spexis_pack_weight       weight layout of the two projections above (done once per weight)
+ *   spexis_linear_split      several linear layers of one input (q, k, v) in one projection
+ *   spexis_pack_weight       weight layout of the projections above (done once per weight)
  *   spexis_sample_tokens     one token per row of logits or probabilities, with its probability
  *   spexis_softmax_rows      temperature softmax of logit rows (probability inputs)
  *
@@ -317,6 +318,32 @@ int spexis_linear(const void* x, const void* weight, const void* residual, int32
 
 /* Bytes of workspace spexis_linear needs for this problem (0 if none). */
 size_t spexis_linear_workspace_size(int32_t rows, int32_t out_features, int32_t in_features);
+
+/*
+ * spexis_linear_split -- several linear layers of one input in one call: the drafting adapter's
+ * attention-layer q, k and v projections of x (Implementation).  weight is the packed stack of
+ * the layers' weights, W = [W_0; W_1; ...] with W_i [out_features[i]][in_features] in output
+ * order (spexis_pack_weight of the stacked rows), and output i receives its columns of x W^T:
+ *   y_i[r][o] = bf16( sum_j x[r][j] * W[c_i + o][j] ),   c_i = out_features[0] + ... + [i-1]
+ * with fp32 accumulation (the order over j is the library's) and one round to nearest even; no
+ * residual.  One projection launch and one launch that adds the K-split partials and routes each
+ * layer's columns: at few rows, where each launch is latency-bound, fewer launches than one
+ * spexis_linear per layer.
+ *   x            [rows][in_features] bf16
+ *   num_outputs  1 .. 4;  out_features: host [num_outputs], each > 0 and a multiple of 4
+ *   outputs      host [num_outputs] of device pointers: output i is [rows][out_features[i]]
+ *                bf16 (may not alias x, weight or one another)
+ *   workspace    >= spexis_linear_split_workspace_size(rows, sum of out_features, in_features)
+ *                bytes (the fp32 products pass through it: never 0 when rows > 0)
+ * Supported: in_features % 256 == 0.  Errors: INVALID_ARGUMENT (bad sizes or count, NULL
+ * pointers), UNSUPPORTED (widths, in_features, size), WORKSPACE_TOO_SMALL, HIP.
+ */
+int spexis_linear_split(const void* x, const void* weight, int32_t rows, int32_t in_features, int32_t num_outputs,
+                        const int32_t* out_features, void* const* outputs, void* workspace, size_t workspace_bytes,
+                        void* stream);
+
+/* Bytes of workspace spexis_linear_split needs (0 for an empty or unsupported problem). */
+size_t spexis_linear_split_workspace_size(int32_t rows, int32_t total_out_features, int32_t in_features);
 
 /*
  * spexis_sample_tokens -- draws one token per row from softmax(logits / T) (kind LOGITS) or from

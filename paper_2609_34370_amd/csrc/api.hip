@@ -462,6 +462,64 @@ int spexis_linear(const void* x, const void* weight, const void* residual, int32
   return hip_result(spexis::launch_linear(p, (hipStream_t)stream), "spexis_linear");
 }
 
+size_t spexis_linear_split_workspace_size(int32_t rows, int32_t total_out_features, int32_t in_features) {
+  if (rows <= 0 || total_out_features <= 0 || in_features <= 0 || in_features % 256 != 0) return 0;
+  const int S = spexis::linear_split(rows, total_out_features, in_features);
+  return (size_t)S * rows * total_out_features * sizeof(float);
+}
+
+int spexis_linear_split(const void* x, const void* weight, int32_t rows, int32_t in_features, int32_t num_outputs,
+                        const int32_t* out_features, void* const* outputs, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+  if (rows < 0 || in_features <= 0 || num_outputs < 1 || num_outputs > spexis::kLinearMaxOutputs || !out_features)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_linear_split: bad size or output count");
+  int64_t N = 0;
+  for (int i = 0; i < num_outputs; ++i) {
+    if (out_features[i] <= 0) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_linear_split: bad output width");
+    if (out_features[i] % 4 != 0)
+      return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_linear_split: output width %d is not a multiple of 4",
+                  out_features[i]);
+    N += out_features[i];
+  }
+  if (in_features % 256 != 0)
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_linear_split: in_features %d is not a multiple of 256",
+                in_features);
+  if (N >= (1ll << 30)) return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_linear_split: problem too large");
+  if (rows == 0) return ok();
+  if (!x || !weight || !outputs) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_linear_split: null pointer");
+  for (int i = 0; i < num_outputs; ++i)
+    if (!outputs[i]) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_linear_split: null output %d", i);
+  if (spexis::projection_workgroups(rows, N) + 8 * rows >= (1ll << 31) || (int64_t)rows * N >= (1ll << 36) ||
+      (int64_t)rows * in_features >= (1ll << 40))
+    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_linear_split: problem too large");
+  const int S = spexis::linear_split(rows, (int)N, in_features);
+  const size_t need = spexis_linear_split_workspace_size(rows, (int)N, in_features);
+  if (!workspace || workspace_bytes < need)
+    return fail(SPEXIS_ERR_WORKSPACE_TOO_SMALL, "spexis_linear_split: workspace %zu bytes < %zu needed",
+                workspace_bytes, need);
+  spexis::LinearParams p{};
+  p.proj.h = x;
+  p.proj.w = weight;
+  p.proj.M = rows;
+  p.proj.V = (int)N;
+  p.proj.d = in_features;
+  p.proj.ntiles = (int)((N + spexis::kLmCols - 1) / spexis::kLmCols);
+  p.proj.ksplit = S;
+  p.proj.logits = static_cast<float*>(workspace);   // [S][rows][N] fp32 products, S >= 1
+  p.part = static_cast<float*>(workspace);
+  p.M = rows;
+  p.N = (int)N;
+  p.S = S;
+  p.nout = num_outputs;
+  p.off[0] = 0;
+  for (int i = 0; i < num_outputs; ++i) {
+    p.off[i + 1] = p.off[i] + out_features[i];
+    p.ys[i] = outputs[i];
+  }
+  for (int i = num_outputs + 1; i <= spexis::kLinearMaxOutputs; ++i) p.off[i] = (int)N;
+  return hip_result(spexis::launch_linear(p, (hipStream_t)stream), "spexis_linear_split");
+}
+
 int spexis_lookahead_memory(int32_t num_requests, const int64_t* cur_len, const int32_t* remaining,
                             const double* precision, int32_t pp, double theta, int32_t iters, double* mem,
                             double* e_gen, double* e_nfin, double* e_lfin, void* stream) {

@@ -80,12 +80,17 @@ struct SelectParams {
 constexpr int kSelectMaxDrafts = 16384;
 
 // spexis_linear: the projection kernel, then (K split) the reduce of its partials.
+constexpr int kLinearMaxOutputs = 4;   // outputs of one split linear call
+
 struct LinearParams {
   LmParams proj;
-  float* part;       // fp32 [S][M][N] when S > 1
+  float* part;       // fp32 [S][M][N] when S > 1 or nout > 0
   const void* res;   // bf16 [M][N] or null
-  void* y;           // bf16 [M][N]
+  void* y;           // bf16 [M][N] (nout == 0)
   int M, N, S;
+  int nout;                          // 0: y alone; else outputs 0 .. nout-1 take columns
+  int off[kLinearMaxOutputs + 1];    // off[i] .. off[i+1]-1 (multiples of 4, off[nout] = N)
+  void* ys[kLinearMaxOutputs];       // bf16 [M][off[i+1] - off[i]]
 };
 
 struct LookaheadParams {

@@ -8,7 +8,9 @@
 // from its packed layout).  An adapter matrix has few column tiles, so the K range is split over
 // workgroups until the chip is covered -- as long as the fp32 partials cost no more traffic than
 // the weight; then a second kernel adds the partials in order, adds the residual and rounds
-// to bf16.  Without a split the projection writes bf16 (with the residual) itself.
+// to bf16.  Without a split the projection writes bf16 (with the residual) itself.  Several
+// layers of one input (the attention layer's q, k, v) run as one projection of their stacked
+// weights, the second kernel routing each layer's columns to its own output.
 #include "common.h"
 #include "kernels.h"
 
@@ -29,7 +31,8 @@ __device__ __forceinline__ float from_bf16(uint16_t b) { return __uint_as_float(
 
 }  // namespace
 
-// y = bf16(sum_s part[s] (in order) + R): 4 consecutive outputs per thread.
+// y = bf16(sum_s part[s] (in order) + R): 4 consecutive outputs per thread; with split outputs,
+// each group of four goes to the output that owns its columns.
 __global__ __launch_bounds__(kThreads) void linear_reduce_kernel(LinearParams p) {
   const int64_t total = (int64_t)p.M * p.N;
   const int64_t e0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * 4;
@@ -54,6 +57,21 @@ __global__ __launch_bounds__(kThreads) void linear_reduce_kernel(LinearParams p)
       for (int i = 0; i < cnt; ++i) v[i] += p.part[(int64_t)s * total + e0 + i];
   }
   uint16_t* y = reinterpret_cast<uint16_t*>(p.y) + e0;
+  if (p.nout > 0) {
+    // split outputs: the four columns lie in one output (its bounds are multiples of 4)
+    const int64_t row = e0 / p.N;
+    const int c = (int)(e0 - row * p.N);
+    void* base = p.ys[0];
+    int lo = 0, hi = p.off[1];
+#pragma unroll
+    for (int j = 1; j < kLinearMaxOutputs; ++j)
+      if (j < p.nout && c >= p.off[j]) {
+        base = p.ys[j];
+        lo = p.off[j];
+        hi = p.off[j + 1];
+      }
+    y = reinterpret_cast<uint16_t*>(base) + row * (hi - lo) + (c - lo);
+  }
   const uint16_t* r = p.res ? reinterpret_cast<const uint16_t*>(p.res) + e0 : nullptr;
   for (int i = 0; i < cnt; ++i) y[i] = to_bf16(r ? v[i] + from_bf16(r[i]) : v[i]);
 }
@@ -71,7 +89,7 @@ int linear_split(int M, int N, int K) {
 
 hipError_t launch_linear(const LinearParams& p, hipStream_t s) {
   hipError_t e = launch_projection(p.proj, s);
-  if (e != hipSuccess || p.S == 1) return e;
+  if (e != hipSuccess || (p.S == 1 && p.nout == 0)) return e;
   const int64_t quads = ((int64_t)p.M * p.N + 3) / 4;
   hipLaunchKernelGGL(linear_reduce_kernel, dim3((unsigned)((quads + kThreads - 1) / kThreads)), dim3(kThreads), 0, s,
                      p);

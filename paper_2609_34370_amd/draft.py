@@ -8,8 +8,8 @@ layer, followed by the LM head, after Kangaroo): from the exit hidden states h o
     y = o W_o^T + x
     logits = y W_lm^T                           (with the fused softmax statistics)
     draft token ~ softmax(logits / T), with its probability q(x) as the confidence
-Every step is one libspexis call on one stream; the adapter's KV cache uses the library's paged
-layout and the sequences' block tables.
+Every step is one libspexis call on one stream (q, k and v together: one call over their stacked
+weights); the adapter's KV cache uses the library's paged layout and the sequences' block tables.
 """
 from __future__ import annotations
 
@@ -27,8 +27,8 @@ class DraftStep:
         assert int(batch.k.max()) == 0, "a drafting step has one query token per sequence"
         self.batch, self.spec, self.cache, self.ad = batch, spec, cache, ad
         # the projections read packed weights (laid out once, as at model load)
-        self.w_in, self.w_q, self.w_k, self.w_v, self.w_o, self.w_lm = (
-            sx.spexis_pack_weight(w) for w in (ad.w_in, ad.w_q, ad.w_k, ad.w_v, ad.w_o, ad.w_lm))
+        self.w_in, self.w_o, self.w_lm = (sx.spexis_pack_weight(w) for w in (ad.w_in, ad.w_o, ad.w_lm))
+        self.w_qkv = sx.spexis_pack_weight(torch.cat([ad.w_q, ad.w_k, ad.w_v], dim=0))
         dev = torch.device(device)
         B, d = ad.h.shape
         hq, hkv, D = spec.num_q_heads, spec.num_kv_heads, spec.head_dim
@@ -49,8 +49,8 @@ class DraftStep:
         self.tokens = torch.empty(B, dtype=torch.int32, device=dev)
         self.conf = torch.empty(B, dtype=torch.float32, device=dev)
         self.status = torch.empty(B, dtype=torch.int32, device=dev)
-        lin = max(sx.spexis_linear_workspace_size(B, n, kk) for n, kk in ((d, d), (hq * D, d), (hkv * D, d),
-                                                                          (d, hq * D)))
+        lin = max([sx.spexis_linear_workspace_size(B, n, kk) for n, kk in ((d, d), (d, hq * D))] +
+                  [sx.spexis_linear_split_workspace_size(B, (hq + 2 * hkv) * D, d)])
         self.lin_ws = torch.empty(max(lin, 16), dtype=torch.uint8, device=dev)
         aw = sx.spexis_verify_attention_workspace_size(B, hq, hkv, D, 1, batch.max_seq_len, 0)
         self.attn_ws = torch.empty(max(aw, 16), dtype=torch.uint8, device=dev)
@@ -60,9 +60,8 @@ class DraftStep:
     def adapter_in(self, stream=None):
         a, B = self.ad, self.batch.B
         sx.spexis_linear(a.h, self.w_in, self.x, workspace=self.lin_ws, stream=stream)
-        sx.spexis_linear(self.x, self.w_q, self.q.view(B, -1), workspace=self.lin_ws, stream=stream)
-        sx.spexis_linear(self.x, self.w_k, self.k.view(B, -1), workspace=self.lin_ws, stream=stream)
-        sx.spexis_linear(self.x, self.w_v, self.v.view(B, -1), workspace=self.lin_ws, stream=stream)
+        sx.spexis_linear_split(self.x, self.w_qkv, [self.q.view(B, -1), self.k.view(B, -1), self.v.view(B, -1)],
+                               self.lin_ws, stream=stream)
 
     def attention(self, stream=None):
         s, b, c = self.spec, self.batch, self.cache

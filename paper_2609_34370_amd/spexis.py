@@ -89,6 +89,10 @@ def lib():
     L.spexis_linear.restype = ctypes.c_int
     L.spexis_linear_workspace_size.argtypes = [i32, i32, i32]
     L.spexis_linear_workspace_size.restype = sz
+    L.spexis_linear_split.argtypes = [P, P, i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(P), P, sz, P]
+    L.spexis_linear_split.restype = ctypes.c_int
+    L.spexis_linear_split_workspace_size.argtypes = [i32, i32, i32]
+    L.spexis_linear_split_workspace_size.restype = sz
     L.spexis_lookahead_memory.argtypes = [i32, P, P, P, i32, ctypes.c_double, i32, P, P, P, P, P]
     L.spexis_lookahead_memory.restype = ctypes.c_int
     _lib = L
@@ -248,6 +252,26 @@ def spexis_linear(x, weight, y, residual=None, workspace=None, stream=None) -> N
                                _ptr(residual, torch.bfloat16) if residual is not None else None, rows, n_out, n_in,
                                _ptr(y, torch.bfloat16), _ptr(workspace) if workspace is not None else None, ws_bytes,
                                _stream(stream)))
+
+
+def spexis_linear_split_workspace_size(rows: int, total_out_features: int, in_features: int) -> int:
+    return int(lib().spexis_linear_split_workspace_size(rows, total_out_features, in_features))
+
+
+def spexis_linear_split(x, weight, outputs, workspace, stream=None) -> None:
+    """outputs[i] = bf16(x W_i^T) for bf16 x [rows, in] and the packed stack of the weights W_i
+    (spexis_pack_weight of their rows stacked in output order); W_i's height is outputs[i]'s
+    width."""
+    rows, n_in = x.shape
+    widths = [int(o.shape[1]) for o in outputs]
+    assert all(int(o.shape[0]) == rows for o in outputs)
+    assert weight.numel() * 2 == spexis_packed_weight_size(sum(widths), n_in), "weight must be packed"
+    m = len(widths)
+    w_arr = (ctypes.c_int32 * m)(*widths)
+    o_arr = (ctypes.c_void_p * m)(*[_ptr(o, torch.bfloat16).value for o in outputs])
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().spexis_linear_split(_ptr(x, torch.bfloat16), _ptr(weight, torch.bfloat16), rows, n_in, m, w_arr,
+                                     o_arr, _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def spexis_sample_workspace_size(rows: int, vocab: int) -> int:

@@ -132,3 +132,36 @@ def test_append_validation():
         sx.SPEXIS_ERR_INVALID_ARGUMENT
     # nothing to do: no launch, success
     assert L.spexis_append_kv(FAKE, FAKE, 10, 2, 16, 64, 0, FAKE, FAKE, FAKE, 4, 0, 2, FAKE, FAKE, None) == sx.SPEXIS_OK
+
+
+def split(widths, rows=4, n_in=256, outs=None, ws=FAKE, wsb=1 << 30, x=FAKE, w=FAKE):
+    m = len(widths)
+    w_arr = (ctypes.c_int32 * max(m, 1))(*widths)
+    o_arr = (ctypes.c_void_p * max(m, 1))(*([256 * (i + 4) for i in range(m)] if outs is None else outs))
+    return sx.lib().spexis_linear_split(x, w, rows, n_in, m, w_arr, o_arr, ws, wsb, None)
+
+
+@no_gpu
+def test_linear_split_validation():
+    assert split([]) == sx.SPEXIS_ERR_INVALID_ARGUMENT                      # no outputs
+    assert split([8, 8, 8, 8, 8]) == sx.SPEXIS_ERR_INVALID_ARGUMENT         # more than four
+    assert split([8, 0]) == sx.SPEXIS_ERR_INVALID_ARGUMENT                  # empty output
+    assert split([8, 6]) == sx.SPEXIS_ERR_UNSUPPORTED                       # width not a multiple of 4
+    assert split([8], n_in=320) == sx.SPEXIS_ERR_UNSUPPORTED                # in_features % 256
+    assert split([8], rows=-1) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert split([8], rows=0, x=None, w=None, outs=[None], ws=None, wsb=0) == sx.SPEXIS_OK   # no work
+    assert split([8], x=None) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert split([8, 8], outs=[512, None]) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert split([4096, 1024, 1024], rows=64, n_in=4096, wsb=100) == sx.SPEXIS_ERR_WORKSPACE_TOO_SMALL
+    assert b"workspace" in sx.lib().spexis_last_error()
+
+
+def test_linear_split_workspace_query():
+    # the fp32 products of every K-split part pass through the workspace, also without a split
+    for rows, n, k in [(64, 6144, 4096), (5, 116, 256), (300, 320, 512), (1, 4, 256)]:
+        got = sx.spexis_linear_split_workspace_size(rows, n, k)
+        plain = sx.spexis_linear_workspace_size(rows, n, k)
+        assert got == (plain if plain > 0 else rows * n * 4), (rows, n, k)
+    assert sx.spexis_linear_split_workspace_size(0, 64, 256) == 0
+    assert sx.spexis_linear_split_workspace_size(4, 64, 300) == 0
+

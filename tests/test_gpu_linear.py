@@ -68,6 +68,51 @@ def test_linear_adapter_shapes_sampled_rows():
     check(512, 4096, 4096, True, 13, sample=[0, 255, 511])
 
 
+@pytest.mark.parametrize("rows,widths,n_in", [(64, [4096, 1024, 1024], 4096), (5, [12, 100, 4], 256),
+                                              (300, [256, 64], 512), (33, [8, 16, 32, 64], 768), (1, [4], 256)])
+def test_linear_split_matches_oracle(rows, widths, n_in):
+    # output i holds x W_i^T for W_i the i-th block of rows of one packed stacked weight; each is
+    # checked against the oracle's linear layer of its own block, to the bar above
+    seed = rows + sum(widths)
+    x, xb = bf16_pair((rows, n_in), seed, 1.0)
+    w, wb = bf16_pair((sum(widths), n_in), seed + 1, 0.03)
+    outs = [torch.empty((rows, n), dtype=torch.bfloat16, device="cuda") for n in widths]
+    ws = torch.empty(sx.spexis_linear_split_workspace_size(rows, sum(widths), n_in), dtype=torch.uint8,
+                     device="cuda")
+    sx.spexis_linear_split(x.cuda(), sx.spexis_pack_weight(w.cuda()), outs, ws)
+    torch.cuda.synchronize()
+    sel = np.arange(rows) if rows <= 40 else np.array([0, rows // 3, rows - 1])
+    c0 = 0
+    worst = 0.0
+    for n, o in zip(widths, outs):
+        got = o.float().cpu().double().numpy()[sel]
+        ref = oracle.linear(xb[sel], wb[c0:c0 + n])
+        mag = np.abs(x.double().numpy()[sel]) @ np.abs(w.double().numpy()[c0:c0 + n]).T
+        bound = 2.0 ** -8 * np.abs(ref) + 4 * n_in * 2.0 ** -24 * mag + 1e-30
+        err = np.abs(got - ref)
+        worst = max(worst, float((err / bound).max()))
+        assert (err <= bound).all(), (n, c0)
+        c0 += n
+    say(f"[linear split] {rows}x{n_in} @ {widths}: max err/bound {worst:.3f}")
+
+
+def test_linear_split_equals_one_stacked_layer():
+    # the same stacked weight through spexis_linear: the outputs are its column blocks, bit for bit
+    # whenever both take the same K split (they do here: one problem size)
+    rows, widths, n_in = 64, [4096, 1024, 1024], 4096
+    x, _ = bf16_pair((rows, n_in), 21, 1.0)
+    w, _ = bf16_pair((sum(widths), n_in), 22, 0.03)
+    wp = sx.spexis_pack_weight(w.cuda())
+    outs = [torch.empty((rows, n), dtype=torch.bfloat16, device="cuda") for n in widths]
+    ws = torch.empty(sx.spexis_linear_split_workspace_size(rows, sum(widths), n_in), dtype=torch.uint8,
+                     device="cuda")
+    sx.spexis_linear_split(x.cuda(), wp, outs, ws)
+    whole = torch.empty((rows, sum(widths)), dtype=torch.bfloat16, device="cuda")
+    sx.spexis_linear(x.cuda(), wp, whole, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat(outs, dim=1), whole)
+
+
 def test_linear_output_may_alias_residual():
     check(48, 256, 512, True, 14, alias=True)
     check(64, 4096, 1024, True, 15, alias=True)   # K split: the reduce pass reads the residual
