@@ -68,6 +68,26 @@ class VerifyStep:
         if self.acc is not None:
             self.accept(stream=stream)
 
+    def capture(self, warmup: int = 1):
+        """Records run() into a HIP graph (torch.cuda.CUDAGraph); replay() then launches the whole
+        step at once.  Every buffer is allocated in __init__ and the library calls neither
+        allocate nor set memory (the acceptance counters are cleared by its first kernel), so the
+        graph holds only the step's kernel launches.  A replay reads the current contents of the
+        input buffers; the sizes are those of this batch."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for _ in range(warmup):
+                self.run()
+        torch.cuda.current_stream().wait_stream(side)
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            self.run()
+        return self.graph
+
+    def replay(self):
+        self.graph.replay()
+
     def accept_outputs(self):
         return (self.accepted_len.cpu().numpy(), self.out_tokens.cpu().numpy(), self.row_status.cpu().numpy())
 

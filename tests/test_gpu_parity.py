@@ -535,6 +535,35 @@ def test_accept_logits_empty_residual_falls_back_to_target_row():
 
 # -------------------------------------------------------------------------- boundary
 
+@pytest.mark.parametrize("wid,B", [(2, 16), (1, None)])
+def test_verify_step_graph_replays_equal_the_eager_step(wid, B):
+    # append + attention + acceptance captured into a HIP graph: every replay, with eager work
+    # and synchronisations between them, gives bit for bit the eager step's outputs (workload 2:
+    # acceptance in test rounds; workload 1: one round)
+    over = {} if B is None else {"batch": B}
+    spec, batch, attn, acc = case(wid, seed=3, **over)
+    step = VerifyStep(batch, attn, acc)
+    step.run()
+    torch.cuda.synchronize()
+    outs = lambda: [t.clone() for t in (step.out, step.accepted_len, step.out_tokens, step.row_status,
+                                        attn.k_pool, attn.v_pool)]
+    ref = outs()
+    step.capture()
+    for i in range(3):
+        step.out.zero_()
+        step.accepted_len.fill_(-7)
+        step.out_tokens.fill_(-7)
+        step.row_status.fill_(-7)
+        step.attn_ws.fill_(0x5A)
+        step.acc_ws.fill_(0x5A)
+        torch.cuda.synchronize()
+        step.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(outs(), ref):
+            assert torch.equal(a, b), i
+        say(f"[verify graph] workload {wid} replay {i}: equal to the eager step")
+
+
 def test_boundary_errors_on_gpu():
     spec, batch, attn, acc = case(1)
     step = VerifyStep(batch, attn, acc, kv_chunk_tokens=32)
