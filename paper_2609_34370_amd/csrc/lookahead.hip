@@ -84,7 +84,7 @@ __global__ __launch_bounds__(kThreads) void lookahead_kernel(LookaheadParams p) 
   auto load = [&](int base) {   // indices clamped into [0, n): n > 0 here
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int r = min(base + threadIdx.x + kThreads * u, n - 1);
+      const int r = min(base + (int)threadIdx.x + kThreads * u, n - 1);
       len[u] = p.cur_len[r];
       tau[u] = p.remaining[r];
       prec[u] = p.prec[r];
@@ -120,7 +120,7 @@ __global__ __launch_bounds__(kThreads) void lookahead_kernel(LookaheadParams p) 
     if (base > 0) load(base);
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      if (base + threadIdx.x + kThreads * u >= n) continue;
+      if (base + (int)threadIdx.x + kThreads * u >= n) continue;
       ltot += (double)len[u];
       if (tau[u] > i) continue;   // k <= i for every w
       const int64_t ws = p.pp == 1 ? w_max : min((int64_t)w_max, ((int64_t)i - tau[u]) / (p.pp - 1));
