@@ -496,6 +496,45 @@ def test_accept_largest_vocabulary():
                     assert borderline(p, q, ids, ua, us, qsl, b, ra[b], rt[b], a[b], t[b]), b
 
 
+@pytest.mark.parametrize("V", [1, 2, 3])
+def test_accept_tiny_vocabularies(V):
+    # degenerate rows: with one entry every test passes and every token is 0; with two or three,
+    # both input kinds agree with the oracle (probabilities bit for bit)
+    rng = np.random.default_rng(40 + V)
+    k = np.array([0, 1, 2, 3, 2, 1, 0, 3])
+    B, K = len(k), 3
+    qsl = np.concatenate([[0], np.cumsum(k + 1)]).astype(np.int32)
+    T = int(qsl[-1])
+    tl = (rng.standard_normal((T, V)) * 2).astype(np.float32)
+    dl = (rng.standard_normal((T - B, V)) * 2).astype(np.float32)
+    ids = rng.integers(0, V, T - B).astype(np.int32)
+    ua = rng.random(T - B, dtype=np.float32)
+    us = rng.random(B, dtype=np.float32)
+    p, q = oracle.softmax(tl, 1.0), oracle.softmax(dl, 1.0)
+    ra, rt, rs, _ = oracle.accept(qsl, p, q, ids, ua, us, max_k=K)
+    dev = lambda x: torch.as_tensor(x, device="cuda")
+    ws = torch.empty(sx.spexis_accept_workspace_size(B, V, K), dtype=torch.uint8, device="cuda")
+    for kind, tg, dr in ((sx.SPEXIS_INPUT_PROBS, p, q), (sx.SPEXIS_INPUT_LOGITS, tl, dl)):
+        accepted = torch.empty(B, dtype=torch.int32, device="cuda")
+        toks = torch.empty((B, K + 1), dtype=torch.int32, device="cuda")
+        stat = torch.empty(B, dtype=torch.int32, device="cuda")
+        sx.spexis_accept(kind, dev(qsl), dev(tg), dev(dr), dev(ids), dev(ua), dev(us), K, accepted, toks, stat, ws,
+                         temperature=1.0)
+        torch.cuda.synchronize()
+        a, t, s = accepted.cpu().numpy(), toks.cpu().numpy(), stat.cpu().numpy()
+        np.testing.assert_array_equal(s, rs)
+        if V == 1:
+            np.testing.assert_array_equal(a, k)
+            assert all((t[b, :k[b] + 1] == 0).all() and (t[b, k[b] + 1:] == -1).all() for b in range(B))
+        if kind == sx.SPEXIS_INPUT_PROBS:
+            np.testing.assert_array_equal(a, ra)
+            np.testing.assert_array_equal(t, rt)
+        else:
+            for b in range(B):
+                if a[b] != ra[b] or not np.array_equal(t[b], rt[b]):
+                    assert borderline(p, q, ids, ua, us, qsl, b, ra[b], rt[b], a[b], t[b]), b
+
+
 def test_accept_logits_empty_residual_falls_back_to_target_row():
     # Rejections whose residual is empty in fixed point, with logits.  Sequence 0: identical target
     # and draft rows with the drafted entry at -inf (p(x) = q(x) = 0 rejects), so max(0, p - q)
