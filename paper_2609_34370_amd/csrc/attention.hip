@@ -460,7 +460,9 @@ void verify_attn_kernel(AttnParams p) {
 // hold the rest, in their slot 0, where s_last holds the item's last tile.
 //   o = sum_c acc_c 2^(m_c - M) / sum_c l_c 2^(m_c - M),   M = max_c m_c
 // Contributors are read four at a time, every load of a group issued together.
-template <int D>
+// U: output values per thread (4 or 8); the launcher takes 8 when one pass of the workgroup's
+// threads then covers an item's rows (up to 32), 4 for taller items.
+template <int D, int U>
 __global__ __launch_bounds__(512) void attn_merge_kernel(AttnParams p) {
   const int w = blockIdx.x;
   const int64_t slot_f = attn_slot_floats(p.rmax, D);
@@ -477,19 +479,23 @@ __global__ __launch_bounds__(512) void attn_merge_kernel(AttnParams p) {
   auto slot = [&](int c) -> const float* {
     return p.ws + ((int64_t)((s0 + c) * p.hkv + h) * 2 + (c == 0 ? 1 : 0)) * slot_f;
   };
-  for (int idx = threadIdx.x; idx < R * (D / 4); idx += blockDim.x) {
-    const int r = idx / (D / 4), d = (idx % (D / 4)) * 4;
+  constexpr int NQ = U / 4;   // f32x4 per contributor and thread
+  for (int idx = threadIdx.x; idx < R * (D / U); idx += blockDim.x) {
+    const int r = idx / (D / U), d = (idx % (D / U)) * U;
     float M = kNegBig, den = 0.f;
-    f32x4 o = {0.f, 0.f, 0.f, 0.f};
+    f32x4 o[NQ];
+#pragma unroll
+    for (int v = 0; v < NQ; ++v) o[v] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int c0 = 0; c0 < C; c0 += 4) {
       float mv[4], lv[4];
-      f32x4 av[4];
+      f32x4 av[4][NQ];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         const float* sp = slot(min(c0 + k, C - 1));
         mv[k] = sp[mo + r];
         lv[k] = sp[lo + r];
-        av[k] = *reinterpret_cast<const f32x4*>(sp + (int64_t)r * D + d);
+#pragma unroll
+        for (int v = 0; v < NQ; ++v) av[k][v] = *reinterpret_cast<const f32x4*>(sp + (int64_t)r * D + d + 4 * v);
       }
       float mc = M;
 #pragma unroll
@@ -497,23 +503,28 @@ __global__ __launch_bounds__(512) void attn_merge_kernel(AttnParams p) {
         if (c0 + k < C) mc = fmaxf(mc, mv[k]);
       const float a = fast_exp2(M - mc);
       den *= a;
-      o *= a;
+#pragma unroll
+      for (int v = 0; v < NQ; ++v) o[v] *= a;
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         if (c0 + k >= C) continue;
         const float e = fast_exp2(mv[k] - mc);
         den += e * lv[k];
-        o += av[k] * e;
+#pragma unroll
+        for (int v = 0; v < NQ; ++v) o[v] += av[k][v] * e;
       }
       M = mc;
     }
     const float inv = 1.0f / den;
     const int j = r / p.group, gq = r % p.group;
     uint16_t* orow = reinterpret_cast<uint16_t*>(p.out) + ((int64_t)(q0 + j) * p.hq + h * p.group + gq) * D;
-    u32x2 v2;
-    v2[0] = pack_bf16x2(o[0] * inv, o[1] * inv);
-    v2[1] = pack_bf16x2(o[2] * inv, o[3] * inv);
-    *reinterpret_cast<u32x2*>(orow + d) = v2;
+#pragma unroll
+    for (int v = 0; v < NQ; ++v) {
+      u32x2 v2;
+      v2[0] = pack_bf16x2(o[v][0] * inv, o[v][1] * inv);
+      v2[1] = pack_bf16x2(o[v][2] * inv, o[v][3] * inv);
+      *reinterpret_cast<u32x2*>(orow + d + 4 * v) = v2;
+    }
   }
 }
 
@@ -522,7 +533,11 @@ static hipError_t launch_attn_t(const AttnParams& p, hipStream_t s) {
   hipLaunchKernelGGL((verify_attn_kernel<D, BS, NT>), dim3((unsigned)(p.nwaves / 4)), dim3(256), 0, s, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_merge_kernel<D>), dim3((unsigned)p.nwaves), dim3(512), 0, s, p);   // 512: fewer items per thread
+  // 512 threads: fewer items per thread
+  if (p.rmax <= 32)
+    hipLaunchKernelGGL((attn_merge_kernel<D, 8>), dim3((unsigned)p.nwaves), dim3(512), 0, s, p);
+  else
+    hipLaunchKernelGGL((attn_merge_kernel<D, 4>), dim3((unsigned)p.nwaves), dim3(512), 0, s, p);
   return hipGetLastError();
 }
 
