@@ -708,10 +708,11 @@ __global__ __launch_bounds__(kThreads) void accept_sum_kernel(AcceptParams p) {
 __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int b = blockIdx.x;
-  // the record the sums' first sub-chunk left (every wave reads the same), and the sub-chunk
-  // sums (residual, fallback; lanes own contiguous ranges), loaded together
+  // the record the sums' first sub-chunk left (every wave reads the same), the sub-chunk sums
+  // (residual, fallback; lanes own contiguous ranges) and the uniform, loaded together
   const u32x4* rec = reinterpret_cast<const u32x4*>(p.srec) + 3 * (int64_t)b;
   const u32x4 q0 = rec[0], q1 = rec[1], q2 = rec[2];
+  const float u = p.u_sample[b];
   const uint64_t* sums = p.sum_part + (int64_t)b * p.nsub * 2;
   const int per = (p.nsub + kWave - 1) / kWave;
   const int c_lo = min(p.nsub, lane * per), c_hi = min(p.nsub, c_lo + per);
@@ -755,18 +756,23 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
   // total and exact threshold; the sub-chunk holding t
   const uint64_t incl = wave_incl_scan_u64(own);
   const uint64_t S = readlane_u64(incl, kWave - 1);
-  const uint64_t t = exact_threshold(p.u_sample[b], S);
+  const uint64_t t = exact_threshold(u, S);
   uint64_t excl = incl - own;
   int cstar = -1;
   uint64_t tt = 0;
   if (excl <= t && t < incl) {                        // exactly one lane holds t
-    for (int x = c_lo; x < c_hi; ++x) {
-      if (t < excl + sums[2 * x + which]) {
-        cstar = x;
-        tt = t - excl;
-        break;
+    if (c_hi - c_lo == 1) {                           // its one sub-chunk (up to 64 of them)
+      cstar = c_lo;
+      tt = t - excl;
+    } else {
+      for (int x = c_lo; x < c_hi; ++x) {
+        if (t < excl + sums[2 * x + which]) {
+          cstar = x;
+          tt = t - excl;
+          break;
+        }
+        excl += sums[2 * x + which];
       }
-      excl += sums[2 * x + which];
     }
   }
   const uint64_t found = __ballot(cstar >= 0);
@@ -774,6 +780,12 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
   cstar = __builtin_amdgcn_readlane(cstar, src);
   tt = readlane_u64(tt, src);
   if (cstar < 0) return;   // unreachable: S > 0 (p's largest entry alone weighs >= 2^40)
+  // the output row but its sampled entry: the accepted drafts, then -1 (wave 0; the id loads go
+  // out with the sub-chunk's, the stores follow them)
+  int32_t* orow = p.out_tokens + (int64_t)b * (p.max_k + 1);
+  static_assert(kAcceptMaxK < kWave, "one lane per accepted draft");
+  int idv = -1;
+  if (wave == 0 && lane < a) idv = p.ids[g.d0 + lane];   // a <= max_k <= kAcceptMaxK
   // wave w owns entries cstar*4096 + 1024 w .. + 1023 of the sub-chunk, lane l 16 of them, in order
   constexpr int kRun = kAcceptSub / (kWaves * kWave);   // 16
   const int base = cstar * kAcceptSub + kRun * (kWave * wave + lane);
@@ -788,6 +800,9 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
       qv[4 * j + i] = y[i];
     }
   }
+  if (wave == 0)
+    for (int i = lane; i <= p.max_k; i += kWave)
+      if (i != a) orow[i] = i < a ? idv : -1;
   uint64_t wv[kRun];
   uint64_t mine = 0;
 #pragma unroll
@@ -815,7 +830,10 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
       pre += wv[e];
     }
     if (p.tok_prob) p.tok_prob[b] = prob;
-    write_outputs(p, b, g, a, token, SPEXIS_ROW_OK);
+    orow[a] = token;
+    p.accepted_len[b] = a;
+    p.row_status[b] = SPEXIS_ROW_OK;
+    if (p.seq_lens_inout) p.seq_lens_inout[b] -= g.k - a;
   }
 }
 

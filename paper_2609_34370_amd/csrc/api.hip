@@ -41,7 +41,7 @@ int hip_result(hipError_t e, const char* what) {
 int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 constexpr int kMaxRows = 64;       // query rows per (sequence, KV head)
-constexpr int kMaxK = 32;
+constexpr int kMaxK = spexis::kAcceptMaxK;
 constexpr int kMaxVocab = 1 << 22; // keeps sum W_v < 2^63 (W_v < 2^41)
 
 bool bad_cache_shape(int32_t bs, int32_t d) { return !((bs == 16 || bs == 32) && (d == 64 || d == 128)); }

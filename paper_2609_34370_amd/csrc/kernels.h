@@ -143,6 +143,7 @@ struct AcceptParams {
                          // Mp, Rp, Mq, Rq (written with the sums of sub-chunk 0, or by write_invalid)
 };
 
+constexpr int kAcceptMaxK = 32;      // drafts per sequence the boundary takes (below one wave's lanes)
 constexpr int kAcceptMaxRounds = 8;  // test rounds: widths 2, 4, 8, ... cover max_k <= 509
 constexpr int kAcceptSub = 4096;     // vocab entries per partial result (one workgroup's share)
 
