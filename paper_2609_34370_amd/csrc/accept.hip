@@ -644,15 +644,18 @@ __global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p,
       continue;
     }
     // position i fails when !(u_i q_i(x_i) < p_i(x_i)) (NaN statistics fail)
-    const f32x4* tin = reinterpret_cast<const f32x4*>(p.tin) + (int64_t)b * p.max_k;
+    const float* tin = p.tin + (int64_t)b * p.max_k * 4;
     const int end = min(hi, g.k);
     int fail = g.k + 1;   // none
     for (int i = lo + wave; i < end; i += kWaves) {
-      const f32x4 t = tin[i];
+      // the three floats a test uses (loading the fourth, unused, would let its register be
+      // reused at once, which waits for the load before the statistics' loads are issued)
+      const f32x2 t = *reinterpret_cast<const f32x2*>(tin + 4 * i);
+      const float u = tin[4 * i + 2];
       const RowCtx rc = row_ctx(p, b, g, i, true, lane);
       const float pp = logit_prob(t[0], p.c, rc.Mp, rc.Rp);
       const float qq = logit_prob(t[1], p.c, rc.Mq, rc.Rq);
-      if (!((double)t[2] * (double)qq < (double)pp)) {
+      if (!((double)u * (double)qq < (double)pp)) {
         fail = i;
         break;
       }
