@@ -541,11 +541,12 @@ def ingest_traffic(fetch_csv: str, write_csv: str, workload: int, copy_bytes: in
 
 
 def _kernel_digest() -> str:
-    """Digest of the sources the attention kernels are built from: a stored traffic figure is
-    used only while they are unchanged."""
+    """Digest of the sources the attention kernels are built from (their code, the shared device
+    helpers, and the header with their parameters and launch constants): a stored traffic figure
+    is used only while they are unchanged."""
     import hashlib
     h = hashlib.sha256()
-    for name in ("attention.hip", "common.h"):
+    for name in ("attention.hip", "common.h", "kernels.h"):
         with open(os.path.join(ROOT, "paper_2609_34370_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
