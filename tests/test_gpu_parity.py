@@ -3,9 +3,10 @@
 Bars: append bit-exact; attention |gpu - oracle| <= 1e-2 + 1e-2 |oracle| per element (bf16
 inputs, fp32 accumulation, bf16 output); softmax within 1e-5 absolute; acceptance (accepted
 lengths, emitted tokens, row status) bit-exact when both sides get identical fp32
-probabilities and uniforms.  The oracle's inputs are the generator's host copies, never
-anything the GPU computed.  Full-size workloads are checked on sampled sequences, chosen to
-include the longest context and the shortest/ragged cases.
+probabilities and uniforms; with logits, every disagreement must sit within 1e-5 of a
+decision boundary.  The oracle's inputs are the generator's host copies, never anything the
+GPU computed.  The five workloads are checked at their full sizes, every sequence and every
+output element.
 """
 import math
 import sys
@@ -73,7 +74,7 @@ def test_append_bit_exact(wid):
 
 # ------------------------------------------------------------------------- attention
 
-def check_attention(wid, nseq, seed=None, kv_chunk_tokens=0, **over):
+def check_attention(wid, nseq=None, seed=None, kv_chunk_tokens=0, **over):
     spec, batch, attn, _ = case(wid, seed=seed, accept=False, **over)
     say(f"[attention] workload {wid} B={batch.B} T={batch.T} max_S={batch.max_seq_len} chunk={kv_chunk_tokens}")
     k0, v0 = bf16_to_u16(attn.k_pool), bf16_to_u16(attn.v_pool)
@@ -83,7 +84,7 @@ def check_attention(wid, nseq, seed=None, kv_chunk_tokens=0, **over):
     torch.cuda.synchronize()
     got = bf16_out_to_f64(step.out)
     kp, vp = oracle_pools_after_append(spec, batch, k0, v0, attn)
-    seqs = pick_seqs(batch, nseq, np.random.default_rng(wid))
+    seqs = np.arange(batch.B) if nseq is None else pick_seqs(batch, nseq, np.random.default_rng(wid))
     ref = oracle.attention(kp, vp, batch.num_blocks, spec.num_kv_heads, spec.block_size, spec.head_dim, batch.qsl,
                            batch.seq_lens, batch.block_tables, bf16_to_u16(attn.q), spec.num_q_heads,
                            float(np.float32(step.scale)), seqs=seqs)
@@ -97,9 +98,11 @@ def check_attention(wid, nseq, seed=None, kv_chunk_tokens=0, **over):
     return step, got
 
 
-@pytest.mark.parametrize("wid,nseq", [(1, 4), (2, 12), (3, 6), (4, 12), (5, 16)])
-def test_attention_matches_oracle(wid, nseq):
-    check_attention(wid, nseq)
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
+def test_attention_matches_oracle(wid):
+    # every sequence of the full-size workload, so every item cut between wave shares (and
+    # merged) is compared as well as the ones a wave covers whole
+    check_attention(wid)
 
 
 @pytest.mark.parametrize("chunk", [32, 96, 4096])
@@ -184,17 +187,19 @@ def test_attention_ignores_garbage_past_sequence_end():
 
 # --------------------------------------------------------------------------- softmax
 
-@pytest.mark.parametrize("wid", [1, 2, 4, 5])
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
 def test_softmax_matches_oracle(wid):
-    spec, batch, _, acc = case(wid, seed=None, batch=min(16, wl.WORKLOADS[wid].batch))
-    say(f"[softmax] workload {wid} rows={acc.target_logits.shape[0]} V={spec.vocab} T={acc.temperature}")
-    probs = torch.empty_like(acc.target_logits)
-    sx.spexis_softmax_rows(acc.target_logits, probs, acc.temperature)
-    torch.cuda.synchronize()
-    ref = oracle.softmax(acc.target_logits.cpu().numpy(), acc.temperature)
-    err = np.abs(probs.cpu().numpy() - ref).max()
-    say(f"  max|err|={err:.3e}")
-    assert err <= 1e-5
+    # every target and draft row of the full-size workload
+    spec, batch, _, acc = case(wid)
+    for name, rows in (("target", acc.target_logits), ("draft", acc.draft_logits)):
+        say(f"[softmax] workload {wid} {name} rows={rows.shape[0]} V={spec.vocab} T={acc.temperature}")
+        probs = torch.empty_like(rows)
+        sx.spexis_softmax_rows(rows, probs, acc.temperature)
+        torch.cuda.synchronize()
+        ref = oracle.softmax(rows.cpu().numpy(), acc.temperature)
+        err = np.abs(probs.cpu().numpy() - ref).max()
+        say(f"  max|err|={err:.3e}")
+        assert err <= 1e-5
 
 
 def test_softmax_odd_vocab_and_masked_logits():
@@ -226,10 +231,9 @@ def run_accept_probs(step, p_host, q_host, seq_lens=None):
     return a, t, s, (sl.cpu().numpy() if sl is not None else None)
 
 
-@pytest.mark.parametrize("wid,B", [(1, None), (2, None), (3, 64), (4, None), (5, 96)])
-def test_accept_probs_bit_exact(wid, B):
-    over = {} if B is None else {"batch": B}
-    spec, batch, attn, acc = case(wid, **over)
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
+def test_accept_probs_bit_exact(wid):
+    spec, batch, attn, acc = case(wid)
     say(f"[accept probs] workload {wid} B={batch.B} V={spec.vocab} max_k={batch.max_k}")
     p, q = oracle_probs(acc)
     step = VerifyStep(batch, attn, acc)
@@ -289,8 +293,11 @@ def test_accept_status_codes_and_edge_rows():
         np.testing.assert_array_equal(stat.cpu().numpy(), rs)
 
 
-def borderline(p, q, ids, ua, us, qsl, b, a_o, t_o, a_g, t_g, tol=1e-4):
-    """True if a logits-mode disagreement sits within fp32 rounding of a decision boundary."""
+def borderline(p, q, ids, ua, us, qsl, b, a_o, t_o, a_g, t_g, tol=1e-5):
+    """True if a logits-mode disagreement sits within fp32 rounding of a decision boundary: the
+    first test the two sides decide differently has |u q(x) - p(x)| <= tol, or the sampled
+    tokens differ and the uniform lies within tol of the normalised CDF between them (t within
+    tol * S of a prefix boundary)."""
     t0, d0 = qsl[b], qsl[b] - b
     if a_o != a_g:
         i = min(a_o, a_g)
@@ -304,10 +311,9 @@ def borderline(p, q, ids, ua, us, qsl, b, a_o, t_o, a_g, t_g, tol=1e-4):
     return abs(cdf[m] - float(us[b])) <= tol
 
 
-@pytest.mark.parametrize("wid,B", [(1, None), (2, None), (3, 64), (4, None), (5, 128)])
-def test_accept_logits_agrees_with_oracle(wid, B):
-    over = {} if B is None else {"batch": B}
-    spec, batch, attn, acc = case(wid, **over)
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
+def test_accept_logits_agrees_with_oracle(wid):
+    spec, batch, attn, acc = case(wid)
     say(f"[accept logits] workload {wid} B={batch.B} V={spec.vocab} T={acc.temperature}")
     step = VerifyStep(batch, attn, acc)
     step.accept()
@@ -319,7 +325,6 @@ def test_accept_logits_agrees_with_oracle(wid, B):
     assert (s == 0).all() and (rs == 0).all()
     diff = [b for b in range(batch.B) if a[b] != ra[b] or not np.array_equal(t[b], rt[b])]
     say(f"  mean accepted={a.mean():.3f} disagreements={len(diff)}")
-    assert len(diff) <= max(1, batch.B // 100)
     for b in diff:
         assert borderline(p, q, ids, ua, us, batch.qsl, b, ra[b], rt[b], a[b], t[b]), b
 
@@ -341,7 +346,6 @@ def test_accept_logits_rounds_with_ragged_drafts():
     assert (a >= 2).sum() > 0 and (a >= 6).sum() > 0, "some sequences must reach the later rounds"
     diff = [b for b in range(batch.B) if a[b] != ra[b] or not np.array_equal(t[b], rt[b])]
     say(f"  accepted histogram={np.bincount(a, minlength=9).tolist()} disagreements={len(diff)}")
-    assert len(diff) <= max(1, batch.B // 100)
     for b in diff:
         assert borderline(p, q, ids, ua, us, batch.qsl, b, ra[b], rt[b], a[b], t[b]), b
 
@@ -399,7 +403,6 @@ def test_accept_logits_edge_rows_across_rounds():
     np.testing.assert_array_equal(t[4], rt[4])
     np.testing.assert_array_equal(t[2, :K], rt[2, :K])
     diff = [b for b in range(2, B) if b != 4 and (a[b] != ra[b] or not np.array_equal(t[b], rt[b]))]
-    assert len(diff) <= 1
     for b in diff:
         assert borderline(p, q, ids, ua, us, qsl, b, ra[b], rt[b], a[b], t[b]), b
 
@@ -449,7 +452,6 @@ def test_accept_most_drafts_every_round_odd_vocab():
             np.testing.assert_array_equal(t, rt)
         else:
             diff = [b for b in range(B) if a[b] != ra[b] or not np.array_equal(t[b], rt[b])]
-            assert len(diff) <= 1
             for b in diff:
                 assert borderline(p, q, ids, ua, us, qsl, b, ra[b], rt[b], a[b], t[b]), b
     assert (ra >= 30).sum() >= 3 and ra[0] == 32
