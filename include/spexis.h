@@ -13,6 +13,7 @@
  *   spexis_accept            ratio tests, residual / bonus sampling, outputs
  *   spexis_lm_head           logits = h W^T with fused softmax statistics (next to accept)
  *   spexis_accept_with_stats acceptance from logits whose statistics are known
+ *   spexis_accept_noalloc    spexis_accept in a static scratch array (callers that cannot allocate)
  *   spexis_select_drafts     selective speculation: drop the least confident drafts first
  *   spexis_lookahead_memory  look-ahead KV-memory estimate of the running requests (Algorithm 1)
  *   spexis_linear            a linear layer of the drafting adapter (bf16, fp32 accumulation)
@@ -26,7 +27,8 @@
  *     asynchronous on `stream` (a hipStream_t passed as void*; NULL = the null stream);
  *     the library never synchronises and never reads device data on the host.
  *   - The caller owns all memory: cache pools, block tables, outputs and workspaces.  The
- *     library allocates nothing and holds no device state between calls.
+ *     library allocates nothing and holds no device state between calls, apart from the
+ *     static scratch array of spexis_accept_noalloc (whose contents no call depends on).
  *   - Scalars are validated on the host before any launch.  Device data (block ids, lengths,
  *     token ids) is trusted for correctness but clamped for memory safety: an inconsistent
  *     value gives an unspecified result, never an access outside the buffers described here.
@@ -217,6 +219,33 @@ int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k,
                   const float* u_accept, const float* u_sample, int32_t* accepted_len,
                   int32_t* out_tokens, int32_t* row_status, int32_t* seq_lens_inout,
                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of the static scratch array spexis_accept_noalloc works in (16 MiB per GPU). */
+#define SPEXIS_ACCEPT_NOALLOC_SCRATCH_BYTES (16 << 20)
+
+/*
+ * spexis_accept_noalloc -- spexis_accept without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Arguments, outputs and errors as spexis_accept; the kernels' scratch is a
+ * static device array of SPEXIS_ACCEPT_NOALLOC_SCRATCH_BYTES that every GPU the library runs on
+ * holds until the process ends.  Its address is looked up on the first call on each device (with
+ * that device current; `stream` must belong to it).  The call allocates nothing and calls no
+ * allocating routine.
+ *   - A problem whose workspace (spexis_accept_workspace_size) exceeds the array is rejected with
+ *     SPEXIS_ERR_UNSUPPORTED before any launch: 16 MiB holds e.g. 1024 sequences of 8 drafts over a
+ *     152064-entry vocabulary.
+ *   - Every call on one GPU shares that GPU's array, and the array keeps the last call's
+ *     contents.  No kernel reads scratch it has not written in the same call (the round
+ *     counters are cleared by the first kernel), so the contents left by an earlier call never
+ *     matter.  Calls that overlap on one GPU (different streams, or host threads) race on the
+ *     array and give undefined results; serialise them.
+ */
+int spexis_accept_noalloc(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k,
+                          float temperature, int32_t total_tokens, const int32_t* query_start_loc,
+                          const float* target, const float* draft, const int32_t* draft_ids,
+                          const float* u_accept, const float* u_sample, int32_t* accepted_len,
+                          int32_t* out_tokens, int32_t* row_status, int32_t* seq_lens_inout,
+                          void* stream);
 
 /*
  * spexis_lm_head -- the output projection in front of acceptance (the verifying stage owns an

@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <numeric>
 #include <string>
 
@@ -246,12 +247,38 @@ size_t spexis_accept_workspace_size(int32_t num_seqs, int32_t vocab, int32_t max
 
 namespace {
 
+// Scratch of spexis_accept_noalloc: one copy of this array per GPU, resident until the process
+// ends.  In host code its name stands for no device address; kernels get the address that
+// hipGetSymbolAddress returns for the current device, looked up once per device.
+static __device__ __align__(256) unsigned char scratch[SPEXIS_ACCEPT_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int static_scratch_of_current_device(const char* who, void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SPEXIS_ERR_HIP, "%s: hipGetDevice: %s", who, hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(SPEXIS_ERR_UNSUPPORTED, "%s: device %d >= %d", who, dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(SPEXIS_ERR_HIP, "%s: hipGetSymbolAddress of the scratch array: %s", who, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return SPEXIS_OK;
+}
+
 int accept_impl(const char* who, int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, float temperature,
                 int32_t total_tokens, const int32_t* query_start_loc, const float* target, const float* draft,
                 const float* target_stats, const float* draft_stats, int32_t stats_parts,
                 const int32_t* draft_ids, const float* u_accept, const float* u_sample, int32_t* accepted_len,
                 int32_t* out_tokens, int32_t* row_status, int32_t* seq_lens_inout, void* workspace,
-                size_t workspace_bytes, void* stream, float* tok_prob = nullptr) {
+                size_t workspace_bytes, void* stream, float* tok_prob = nullptr, bool static_scratch = false) {
   // query_start_loc == nullptr (internal callers only): every sequence is one row, no drafts
   if (kind != SPEXIS_INPUT_PROBS && kind != SPEXIS_INPUT_LOGITS)
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: kind %d is neither PROBS nor LOGITS", who, kind);
@@ -268,6 +295,14 @@ int accept_impl(const char* who, int32_t kind, int32_t num_seqs, int32_t vocab, 
       (has_drafts && (!draft || !draft_ids || !u_accept)))
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: null pointer", who);
   const AcceptLayout lay = accept_layout(num_seqs, vocab, max_k);
+  if (static_scratch) {
+    if (lay.total > (size_t)SPEXIS_ACCEPT_NOALLOC_SCRATCH_BYTES)
+      return fail(SPEXIS_ERR_UNSUPPORTED, "%s: needs %zu bytes of scratch, more than the %d of the static array", who,
+                  lay.total, SPEXIS_ACCEPT_NOALLOC_SCRATCH_BYTES);
+    const int rc = static_scratch_of_current_device(who, &workspace);
+    if (rc != SPEXIS_OK) return rc;
+    workspace_bytes = SPEXIS_ACCEPT_NOALLOC_SCRATCH_BYTES;
+  }
   if (!workspace || workspace_bytes < lay.total)
     return fail(SPEXIS_ERR_WORKSPACE_TOO_SMALL, "%s: workspace %zu bytes < %zu needed", who, workspace_bytes,
                 lay.total);
@@ -323,6 +358,16 @@ int spexis_accept(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, 
   return accept_impl("spexis_accept", kind, num_seqs, vocab, max_k, temperature, total_tokens, query_start_loc,
                      target, draft, nullptr, nullptr, 0, draft_ids, u_accept, u_sample, accepted_len, out_tokens,
                      row_status, seq_lens_inout, workspace, workspace_bytes, stream);
+}
+
+int spexis_accept_noalloc(int32_t kind, int32_t num_seqs, int32_t vocab, int32_t max_k, float temperature,
+                          int32_t total_tokens, const int32_t* query_start_loc, const float* target,
+                          const float* draft, const int32_t* draft_ids, const float* u_accept, const float* u_sample,
+                          int32_t* accepted_len, int32_t* out_tokens, int32_t* row_status, int32_t* seq_lens_inout,
+                          void* stream) {
+  return accept_impl("spexis_accept_noalloc", kind, num_seqs, vocab, max_k, temperature, total_tokens,
+                     query_start_loc, target, draft, nullptr, nullptr, 0, draft_ids, u_accept, u_sample, accepted_len,
+                     out_tokens, row_status, seq_lens_inout, nullptr, 0, stream, nullptr, true);
 }
 
 int32_t spexis_lm_head_tiles(int32_t vocab) { return vocab > 0 ? (vocab + spexis::kLmCols - 1) / spexis::kLmCols : 0; }

@@ -68,6 +68,8 @@ def lib():
     L.spexis_accept_workspace_size.restype = sz
     L.spexis_accept.argtypes = [i32, i32, i32, i32, f32, i32, P, P, P, P, P, P, P, P, P, P, P, sz, P]
     L.spexis_accept.restype = ctypes.c_int
+    L.spexis_accept_noalloc.argtypes = [i32, i32, i32, i32, f32, i32, P, P, P, P, P, P, P, P, P, P, P]
+    L.spexis_accept_noalloc.restype = ctypes.c_int
     L.spexis_lm_head.argtypes = [P, P, i32, i32, i32, f32, P, P, P]
     L.spexis_lm_head.restype = ctypes.c_int
     L.spexis_lm_head_tiles.argtypes, L.spexis_lm_head_tiles.restype = [i32], i32
@@ -175,6 +177,23 @@ def spexis_accept(kind, query_start_loc, target, draft, draft_ids, u_accept, u_s
         _ptr(u_sample, torch.float32), _ptr(accepted_len, torch.int32), _ptr(out_tokens, torch.int32),
         _ptr(row_status, torch.int32), _ptr(seq_lens_inout, torch.int32), _ptr(workspace), ws_bytes,
         _stream(stream)))
+
+
+SPEXIS_ACCEPT_NOALLOC_SCRATCH_BYTES = 16 << 20
+
+
+def spexis_accept_noalloc(kind, query_start_loc, target, draft, draft_ids, u_accept, u_sample, max_k, accepted_len,
+                          out_tokens, row_status, temperature=1.0, seq_lens_inout=None, stream=None) -> None:
+    """spexis_accept working in the library's static scratch array (no workspace argument)."""
+    num_seqs = query_start_loc.shape[0] - 1
+    total_tokens, vocab = target.shape
+    nd = total_tokens - num_seqs
+    _check(lib().spexis_accept_noalloc(
+        kind, num_seqs, vocab, max_k, ctypes.c_float(temperature), total_tokens, _ptr(query_start_loc, torch.int32),
+        _ptr(target, torch.float32), _ptr(draft, torch.float32) if nd > 0 else None,
+        _ptr(draft_ids, torch.int32) if nd > 0 else None, _ptr(u_accept, torch.float32) if nd > 0 else None,
+        _ptr(u_sample, torch.float32), _ptr(accepted_len, torch.int32), _ptr(out_tokens, torch.int32),
+        _ptr(row_status, torch.int32), _ptr(seq_lens_inout, torch.int32), _stream(stream)))
 
 
 def spexis_lm_head_tiles(vocab: int) -> int:

@@ -115,6 +115,31 @@ def test_accept_validation():
     assert acc(T=1) == sx.SPEXIS_ERR_INVALID_ARGUMENT            # fewer rows than sequences
 
 
+def acc_noalloc(**kw):
+    a = dict(kind=1, B=2, V=100, mk=2, t=1.0, T=6, qsl=FAKE, tg=FAKE, dr=FAKE, ids=FAKE, ua=FAKE, us=FAKE,
+             al=FAKE, ot=FAKE, rs=FAKE, sl=None)
+    a.update(kw)
+    return sx.lib().spexis_accept_noalloc(a["kind"], a["B"], a["V"], a["mk"], ctypes.c_float(a["t"]), a["T"],
+                                          a["qsl"], a["tg"], a["dr"], a["ids"], a["ua"], a["us"], a["al"], a["ot"],
+                                          a["rs"], a["sl"], None)
+
+
+@no_gpu
+def test_accept_noalloc_validation():
+    # the same host checks as spexis_accept, and a problem beyond the static scratch array is
+    # rejected before the array is ever looked up
+    assert acc_noalloc(kind=5) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert acc_noalloc(t=0.0) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert acc_noalloc(dr=None) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert acc_noalloc(mk=33) == sx.SPEXIS_ERR_UNSUPPORTED
+    B, V, K = 512, 1 << 18, 32
+    assert sx.spexis_accept_workspace_size(B, V, K) > sx.SPEXIS_ACCEPT_NOALLOC_SCRATCH_BYTES
+    assert acc_noalloc(B=B, V=V, mk=K, T=B * (K + 1)) == sx.SPEXIS_ERR_UNSUPPORTED
+    assert b"scratch" in sx.lib().spexis_last_error()
+    assert acc_noalloc(B=0, T=0, qsl=None, tg=None, dr=None, ids=None, ua=None, us=None, al=None, ot=None,
+                       rs=None) == sx.SPEXIS_OK
+
+
 @no_gpu
 def test_softmax_validation():
     L = sx.lib()
