@@ -453,55 +453,63 @@ void oracle_accept(int32_t B, int32_t V, int32_t max_k, const int32_t* qsl, cons
  * Look-ahead memory estimate (Sec. 5, Remaining-Length-Aware Scheduling; Algorithm 1): the
  * expected KV-cache tokens held by the running requests over the next `iters` decoding
  * iterations of a pipeline of depth pp whose speculation is accepted with probability theta.
- * Per request, a rejection costs pp iterations and an acceptance one; after i iterations with w
- * rejections, t = i - pp*w tokens were accepted and k = t + w generated, with probability
- *   p(i, w) = C(k, t) * theta^t * (1 - theta)^w,       w = 0 .. floor(i / pp).
- * For every i = 1 .. iters (all sums in fp64, in the order written):
- *   E_gen  = sum_w k * p(i, w)                                   generated tokens per request
- *   Pfin_r = prec[r] * sum_w [k >= remaining[r]] * p(i, w)       completion probability of r
- *   E_nfin = sum_r Pfin_r,  E_lfin = sum_r cur_len[r] * Pfin_r
- *   mem[i-1] = L_total + (n - E_nfin) * E_gen - E_lfin,          L_total = sum_r cur_len[r].
- * prec[r] is the precision of the length prediction for request r's predicted remaining length
- * (the paper's E(tau)).  e_gen, e_nfin and e_lfin may be NULL; otherwise they receive the
- * per-iteration intermediates.  Returns 0, or -1 on bad arguments.
+ *
+ * Derived here from the process the estimate models, not from the printed listing.  Each
+ * request runs a string of speculation outcomes: an accepted token advances it by one
+ * iteration, a rejection stalls it for pp iterations, and either way one token is generated.
+ * Let mass(c, w) be the probability weight of reaching exactly c iterations with w rejections.
+ * Its last outcome was an acceptance (from c-1, w) or a rejection (from c-pp, w-1):
+ *   mass(0, 0) = 1,  mass(c, w) = theta * mass(c-1, w) + (1 - theta) * mass(c-pp, w-1),
+ * i.e. the sum over every ordering of t = c - pp*w acceptances and w rejections of
+ * theta^t (1 - theta)^w (the paper's p(i, w); it does not sum to 1 over w when pp > 1, since
+ * a rejection can step over iteration i).  At iteration i such a string has generated
+ * k = t + w tokens.  The estimate then weighs the running requests by these masses:
+ *   E_gen(i)  = sum_w k mass(i, w)                      tokens a request is expected to add
+ *   Pfin_r(i) = prec[r] * (mass of the strings with k >= remaining[r])
+ *   mem(i)    = sum_r cur_len[r] + (n - sum_r Pfin_r) E_gen - sum_r cur_len[r] Pfin_r:
+ *     the current lengths, plus the expected growth of the requests still running, minus the
+ *     lengths that finished requests release.
+ * prec[r] is the precision of the prediction of request r's remaining length (the paper's
+ * E(tau)).  All arithmetic in fp64.  e_gen, e_nfin and e_lfin may be NULL; otherwise they
+ * receive E_gen, sum_r Pfin_r and sum_r cur_len[r] Pfin_r per iteration.  Returns 0, or -1 on
+ * bad arguments or a failed allocation.
  */
 int oracle_lookahead(int32_t n, const int64_t* cur_len, const int32_t* remaining, const double* prec,
                      int32_t pp, double theta, int32_t iters, double* mem, double* e_gen, double* e_nfin,
                      double* e_lfin) {
   if (n < 0 || pp < 1 || iters < 1 || !(theta >= 0.0 && theta <= 1.0) || !mem) return -1;
   if (n > 0 && (!cur_len || !remaining || !prec)) return -1;
-  double l_total = 0.0;
-  for (int32_t r = 0; r < n; ++r) l_total += (double)cur_len[r];
+  const int64_t W = iters / pp + 1;            /* rejections possible within the horizon */
+  double* m = calloc((size_t)(iters + 1) * (size_t)W, sizeof *m);   /* m[c*W + w] = mass(c, w) */
+  if (!m) return -1;
+  m[0] = 1.0;
+  for (int32_t c = 1; c <= iters; ++c)
+    for (int64_t w = 0; w < W; ++w) {
+      double v = theta * m[(int64_t)(c - 1) * W + w];
+      if (w > 0 && c >= pp) v += (1.0 - theta) * m[(int64_t)(c - pp) * W + (w - 1)];
+      m[(int64_t)c * W + w] = v;
+    }
+  double held = 0.0;                           /* tokens the requests hold now */
+  for (int32_t r = 0; r < n; ++r) held += (double)cur_len[r];
   for (int32_t i = 1; i <= iters; ++i) {
-    const int32_t w_max = i / pp;
-    double gen = 0.0;
-    for (int32_t w = 0; w <= w_max; ++w) {
-      const int32_t t = i - pp * w, k = t + w;
-      double binom = 1.0;                       /* C(t + w, t) = prod_{j=1..t} (w + j) / j */
-      for (int32_t j = 1; j <= t; ++j) binom = binom * (double)(w + j) / (double)j;
-      const double p = binom * pow(theta, t) * pow(1.0 - theta, w);
-      gen += (double)k * p;
-    }
-    double nfin = 0.0, lfin = 0.0;
+    const double* row = m + (int64_t)i * W;
+    double grow = 0.0;
+    for (int64_t w = 0; w * pp <= i; ++w) grow += (double)(i - pp * w + w) * row[w];
+    double fin = 0.0, released = 0.0;
     for (int32_t r = 0; r < n; ++r) {
-      double s = 0.0;
-      for (int32_t w = 0; w <= w_max; ++w) {
-        const int32_t t = i - pp * w, k = t + w;
-        if (k >= remaining[r]) {
-          double binom = 1.0;
-          for (int32_t j = 1; j <= t; ++j) binom = binom * (double)(w + j) / (double)j;
-          s += binom * pow(theta, t) * pow(1.0 - theta, w);
-        }
-      }
-      const double pfin = prec[r] * s;
-      nfin += pfin;
-      lfin += (double)cur_len[r] * pfin;
+      double tail = 0.0;                       /* mass of the strings that generated >= remaining[r] */
+      for (int64_t w = 0; w * pp <= i; ++w)
+        if (i - pp * w + w >= (int64_t)remaining[r]) tail += row[w];
+      const double pfin = prec[r] * tail;
+      fin += pfin;
+      released += (double)cur_len[r] * pfin;
     }
-    mem[i - 1] = l_total + ((double)n - nfin) * gen - lfin;
-    if (e_gen) e_gen[i - 1] = gen;
-    if (e_nfin) e_nfin[i - 1] = nfin;
-    if (e_lfin) e_lfin[i - 1] = lfin;
+    mem[i - 1] = held + ((double)n - fin) * grow - released;
+    if (e_gen) e_gen[i - 1] = grow;
+    if (e_nfin) e_nfin[i - 1] = fin;
+    if (e_lfin) e_lfin[i - 1] = released;
   }
+  free(m);
   return 0;
 }
 
