@@ -54,7 +54,9 @@ def attention_flops(batch, spec) -> int:
 
 def cpu_baseline(spec, batch, attn, acc, min_seconds=10.0, max_reps=40):
     """Time the oracle on the whole step (attention of every sequence, softmax of every target
-    and draft row, acceptance) on the host cores; returns the verified tokens/s it reaches."""
+    and draft row, acceptance) on the host cores; returns (the baseline record, the oracle's
+    accepted lengths and tokens).  For the two smallest workloads the oracle is also timed on
+    one thread."""
     import oracle
     from paper_2609_34370_amd.step import bf16_to_u16
 
@@ -64,23 +66,141 @@ def cpu_baseline(spec, batch, attn, acc, min_seconds=10.0, max_reps=40):
     tl, dl = acc.target_logits.cpu().numpy(), acc.draft_logits.cpu().numpy()
     ids, ua, us = acc.draft_ids.cpu().numpy(), acc.u_accept.cpu().numpy(), acc.u_sample.cpu().numpy()
     scale = float(np.float32(1.0 / math.sqrt(spec.head_dim)))
-    reps, emitted, t_total = 0, 0, 0.0
-    while reps < max_reps and (reps == 0 or t_total < min_seconds):
-        t0 = time.perf_counter()
+
+    def one_step():
         oracle.append_kv(kp, vp, batch.num_blocks, spec.num_kv_heads, spec.block_size, spec.head_dim, batch.qsl,
                          batch.seq_lens, batch.block_tables, nk, nv)
         oracle.attention(kp, vp, batch.num_blocks, spec.num_kv_heads, spec.block_size, spec.head_dim, batch.qsl,
                          batch.seq_lens, batch.block_tables, q, spec.num_q_heads, scale)
         p = oracle.softmax(tl, acc.temperature)
         qq = oracle.softmax(dl, acc.temperature)
-        a, _, _, _ = oracle.accept(batch.qsl, p, qq, ids, ua, us, max_k=batch.max_k)
-        t_total += time.perf_counter() - t0
-        emitted += int((a.astype(np.int64) + 1).sum())
-        reps += 1
-    return {"value": round(emitted / t_total, 2), "unit": "tokens/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": f"the full {spec.name} step ({batch.B} sequences: append, fp64 attention, fp64 softmax of "
-                      f"{batch.T}+{batch.T - batch.B} rows, exact acceptance) x{reps}, {t_total:.1f} s"}
+        return oracle.accept(batch.qsl, p, qq, ids, ua, us, max_k=batch.max_k)
+
+    def timed(min_s, max_r):
+        reps, emitted, t_total, out = 0, 0, 0.0, None
+        while reps < max_r and (reps == 0 or t_total < min_s):
+            t0 = time.perf_counter()
+            out = one_step()
+            t_total += time.perf_counter() - t0
+            emitted += int((out[0].astype(np.int64) + 1).sum())
+            reps += 1
+        return emitted / t_total, reps, t_total, out
+
+    threads = oracle.num_threads()
+    value, reps, t_total, out = timed(min_seconds, max_reps)
+    rec = {"value": round(value, 2), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+           "sample": f"the full {spec.name} step ({batch.B} sequences: append, fp64 attention, fp64 softmax of "
+                     f"{batch.T}+{batch.T - batch.B} rows, exact acceptance) x{reps}, {t_total:.1f} s",
+           "cpu_model": cpu_model()}
+    if spec.wid in (1, 2):
+        oracle.set_num_threads(1)
+        try:
+            v1, r1, t1, _ = timed(5.0, 3)
+        finally:
+            oracle.set_num_threads(threads)
+        rec["one_thread"] = {"value": round(v1, 2), "unit": "tokens/s", "reps": r1, "seconds": round(t1, 2)}
+    return rec, (out[0], out[1])
+
+
+def accept_bytes(batch, spec, accepted) -> int:
+    """Algorithmic bytes of one logits-mode acceptance: the normalisers of target and draft rows
+    0..a_b (test i needs both of row i's), 4V (a_b + 1) + 4V min(a_b + 1, k_b), plus the sampled
+    row(s) read again for the fixed-point sums: target and draft row a_b for a residual (8V),
+    target row k_b for the bonus token (4V)."""
+    V = spec.vocab
+    total = 0
+    for b in range(batch.B):
+        a, k = int(accepted[b]), int(batch.k[b])
+        total += 4 * V * (a + 1) + 4 * V * min(a + 1, k)
+        total += 8 * V if a < k else 4 * V
+    return total
+
+
+def pct(xs):
+    xs = np.asarray(xs, dtype=np.float64)
+    return {"mean": round(float(xs.mean()), 2), "median": round(float(np.median(xs)), 2),
+            "p10": round(float(np.percentile(xs, 10)), 2), "p90": round(float(np.percentile(xs, 90)), 2)}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def stream_peaks(torch, nbytes=4 << 30, reps=5):
+    """Measured HBM rates on this GPU: the read probe of libspexis_probe.so (plain coalesced
+    16-byte loads over a 4 GiB buffer, best grid and repetition) and torch's device copy (bytes
+    read plus bytes written per second)."""
+    import ctypes
+    from paper_2609_34370_amd import build as _b
+    probe = ctypes.CDLL(_b.PROBE_LIB_PATH)
+    probe.spexis_probe_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
+                                               ctypes.c_void_p]
+    probe.spexis_probe_stream_read.restype = ctypes.c_int
+    src = torch.zeros(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    sink = torch.empty(8192 * 256, dtype=torch.int32, device="cuda")
+    s = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+    def best(fn):
+        fn()
+        t = float("inf")
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            t = min(t, e0.elapsed_time(e1) * 1e-3)
+        return t
+
+    def read(grid):
+        rc = probe.spexis_probe_stream_read(ctypes.c_void_p(src.data_ptr()), nbytes, grid,
+                                            ctypes.c_void_p(sink.data_ptr()), s)
+        if rc != 0:
+            raise RuntimeError(f"stream probe failed: {rc}")
+
+    out = {"read": round(max(nbytes / best(lambda g=g: read(g)) / 1e9 for g in (1024, 2048, 4096, 8192)), 1),
+           "copy": round(2 * nbytes / best(lambda: dst.copy_(src)) / 1e9, 1)}
+    del src, dst, sink
+    torch.cuda.empty_cache()
+    return out
+
+
+def clone_step(step_cls, batch, attn, acc, kv_chunk, kind, wl):
+    """A VerifyStep over fresh copies of the inputs (same bytes, different HBM addresses)."""
+    a2 = wl.AttentionInputs(attn.k_pool.clone(), attn.v_pool.clone(), attn.q.clone(), attn.new_k.clone(),
+                            attn.new_v.clone())
+    c2 = wl.AcceptInputs(acc.target_logits.clone(), acc.draft_logits.clone(), acc.draft_ids.clone(),
+                         acc.u_accept.clone(), acc.u_sample.clone(), acc.temperature)
+    return step_cls(batch, a2, c2, kv_chunk_tokens=kv_chunk, kind=kind)
+
+
+def phase_pass(torch, steps, K, stream, flush=None):
+    """Per-phase HIP-event durations (us) of K steps, step i on steps[i % len(steps)]; with
+    `flush`, that function runs before every step, outside the events."""
+    names = ("append", "verify_attention", "accept")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    torch.cuda.synchronize()
+    for i in range(K):
+        st = steps[i % len(steps)]
+        if flush is not None:
+            flush()
+        ev[i][0].record(stream)
+        st.append()
+        ev[i][1].record(stream)
+        st.attention()
+        ev[i][2].record(stream)
+        st.accept()
+        ev[i][3].record(stream)
+    torch.cuda.synchronize()
+    return {n: [ev[i][j].elapsed_time(ev[i][j + 1]) * 1e3 for i in range(K)] for j, n in enumerate(names)}
 
 
 def main():
@@ -93,7 +213,8 @@ def main():
     ap.add_argument("--kv-chunk", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
-                    help="first copy BYTES device-to-device 3 times (a known-size kernel for counter calibration)")
+                    help="first copy BYTES device-to-device 3 times (a known-size kernel for counter calibration); "
+                         "skips the flushed pass and the stream-rate probe, whose copies would be confused with it")
     ap.add_argument("--ingest-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic.json from two rocprofv3 --pmc counter_collection.csv files "
                          "(FETCH_SIZE, WRITE_SIZE) of runs with --copy-probe N (pass the same N); needs no GPU")
@@ -141,7 +262,14 @@ def main():
     if not args.no_cpu_baseline:
         baseline_inputs = wl.AttentionInputs(attn.k_pool.cpu(), attn.v_pool.cpu(), attn.q.cpu(), attn.new_k.cpu(),
                                              attn.new_v.cpu())
-    step = VerifyStep(batch, attn, acc, kv_chunk_tokens=args.kv_chunk, kind=sx.SPEXIS_INPUT_LOGITS)
+    kind = sx.SPEXIS_INPUT_LOGITS
+    step = VerifyStep(batch, attn, acc, kv_chunk_tokens=args.kv_chunk, kind=kind)
+    # Cold steps: R copies of every input, used in turn, so that between two uses of one copy the
+    # other copies' steps stream at least 1 GiB through HBM; neither the 256 MB last-level cache
+    # nor the L2s can still hold a step's data.  Warm steps reuse one copy back to back.
+    abytes = attention_bytes(batch, spec)
+    R = 1 + min(7, max(1, -(-(1 << 30) // abytes)))   # tiny workloads: 8 copies, still far under 1 GiB
+    steps = [step] + [clone_step(VerifyStep, batch, attn, acc, args.kv_chunk, kind, wl) for _ in range(R - 1)]
     stream = torch.cuda.current_stream()
     if args.copy_probe > 0:
         src = torch.empty(args.copy_probe, dtype=torch.uint8, device="cuda")
@@ -151,64 +279,78 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    for _ in range(args.warmup):
-        step.run()
+    for i in range(args.warmup):
+        steps[i % R].run()
     torch.cuda.synchronize()
 
     K = args.steps
-    # Timed region: exactly K whole steps, nothing recorded between the calls.
+    # Timed region (the headline): exactly K whole cold steps, nothing recorded between calls.
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        steps[i % R].run()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    # The same K steps warm (one copy of the inputs, back to back), beside the headline.
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(K):
         step.run()
     torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
+    elapsed_warm = time.perf_counter() - t0
 
     # Per-phase durations: K more steps with HIP events on the launch stream around each call
-    # (an event record idles the stream for a few microseconds, so these steps are not the
-    # ones `value` is computed from).
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
-    torch.cuda.synchronize()
-    for i in range(K):
-        ev[i][0].record(stream)
-        step.append()
-        ev[i][1].record(stream)
-        step.attention()
-        ev[i][2].record(stream)
-        step.accept()
-        ev[i][3].record(stream)
-    torch.cuda.synchronize()
+    # (an event record idles the stream for a few microseconds, so these steps are not the ones
+    # `value` is computed from): cold as in the timed region, warm, and after a 1 GiB read
+    # (a reduction over a scratch buffer: it leaves no dirty lines to write back) before every step.
+    cold = phase_pass(torch, steps, K, stream)
+    warm = phase_pass(torch, [step], K, stream)
+    flushed = None
+    peaks = None
+    if args.copy_probe == 0:
+        fa = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        flushed = phase_pass(torch, [step], K, stream, flush=lambda: fa.sum())
+        del fa
+        torch.cuda.empty_cache()
+        peaks = stream_peaks(torch)
 
     a, toks, status = step.accept_outputs()
+    for other in steps[1:]:
+        a2, t2, s2 = other.accept_outputs()
+        assert np.array_equal(a, a2) and np.array_equal(toks, t2) and np.array_equal(status, s2)
     emitted = int((a.astype(np.int64) + 1).sum())
-    ms_append = float(np.mean([ev[i][0].elapsed_time(ev[i][1]) for i in range(K)]))
-    ms_attn = float(np.mean([ev[i][1].elapsed_time(ev[i][2]) for i in range(K)]))
-    ms_accept = float(np.mean([ev[i][2].elapsed_time(ev[i][3]) for i in range(K)]))
+    ms_append = float(np.mean(cold["append"])) * 1e-3
+    ms_attn = float(np.mean(cold["verify_attention"])) * 1e-3
+    ms_accept = float(np.mean(cold["accept"])) * 1e-3
     ms_step = elapsed * 1e3 / K
+    ms_step_warm = elapsed_warm * 1e3 / K
     value = emitted / (ms_step * 1e-3)
-    abytes = attention_bytes(batch, spec)
     achieved = abytes / (ms_attn * 1e-3) / 1e9
-    log(f"[bench] append {ms_append * 1e3:.1f} us  attention {ms_attn * 1e3:.1f} us  accept {ms_accept * 1e3:.1f} us"
-        f"  step {ms_step * 1e3:.1f} us  emitted {emitted}/step  accepted mean {a.mean():.3f}  status!=0 "
-        f"{int((status != 0).sum())}")
+    acc_bytes = accept_bytes(batch, spec, a)
+    acc_gbs = acc_bytes / (ms_accept * 1e-3) / 1e9
+    log(f"[bench] cold: append {ms_append * 1e3:.1f} us  attention {ms_attn * 1e3:.1f} us  accept "
+        f"{ms_accept * 1e3:.1f} us  step {ms_step * 1e3:.1f} us (warm {ms_step_warm * 1e3:.1f} us, {R} input copies)"
+        f"  emitted {emitted}/step  accepted mean {a.mean():.3f}  status!=0 {int((status != 0).sum())}")
     log(f"[bench] attention {abytes / 1e9:.3f} GB algorithmic -> {achieved:.0f} GB/s "
         f"({achieved / HBM_PEAK_GBS:.1%} of 8 TB/s); {attention_flops(batch, spec) / (ms_attn * 1e-3) / 1e12:.1f} "
-        f"TFLOP/s")
+        f"TFLOP/s; accept {acc_bytes / 1e9:.3f} GB algorithmic -> {acc_gbs:.0f} GB/s "
+        f"({acc_gbs / HBM_PEAK_GBS:.1%}); measured stream rates {peaks}")
 
     cpu = None
+    agreement = None
     if baseline_inputs is not None and int(os.environ.get("RANK", "0")) == 0:
         log("[bench] timing the CPU oracle on the host cores")
-        cpu = cpu_baseline(spec, batch, baseline_inputs, acc)
-        log(f"[bench] oracle: {cpu}")
+        cpu, ref = cpu_baseline(spec, batch, baseline_inputs, acc)
+        ra, rt = ref
+        same = int(sum(1 for b in range(batch.B) if a[b] == ra[b] and np.array_equal(toks[b], rt[b])))
+        agreement = {"sequences": batch.B, "agree": same, "rate": round(same / batch.B, 6),
+                     "what": "logits-mode accepted lengths and tokens against the oracle's exact rule on its "
+                             "fp64 softmax of the same logits"}
+        log(f"[bench] oracle: {cpu}; acceptance agreement {same}/{batch.B}")
 
-    traffic = None
-    prof = os.path.join(ROOT, "profiles", "traffic.json")
-    if os.path.exists(prof):
-        with open(prof) as f:
-            t = json.load(f).get(f"workload{spec.wid}")
-        if t and t.get("source_digest") == _kernel_digest():
-            traffic = t["bytes_per_launch"]
-
+    traffic = stored_traffic(spec.wid, "verify_attention")
+    acc_traffic = stored_traffic(spec.wid, "accept")
+    read_peak = peaks["read"] if peaks else None
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
@@ -217,12 +359,26 @@ def main():
                    "kv_heads": spec.num_kv_heads, "head_dim": spec.head_dim, "block_size": spec.block_size,
                    "context": list(spec.ctx), "draft_tokens": list(spec.k), "vocab": spec.vocab,
                    "temperature": spec.temperature, "accept_input": "logits", "parallelism": "none"},
+        "protocol": f"cold (headline): {R} copies of the inputs used in turn, {(R - 1) * abytes / 2**30:.2f} GiB "
+                    f"of other steps' attention reads between two uses of one copy; warm: one copy back to back; "
+                    f"flushed: one copy, a 1 GiB read before each step (phase times only)",
+        "warm": {"value": round(emitted / (ms_step_warm * 1e-3), 1), "ms_per_step": round(ms_step_warm, 4)},
         "phases_us": {"append": round(ms_append * 1e3, 2), "verify_attention": round(ms_attn * 1e3, 2),
                       "accept": round(ms_accept * 1e3, 2)},
+        "phase_stats_us": {"cold": {k: pct(v) for k, v in cold.items()},
+                           "warm": {k: pct(v) for k, v in warm.items()},
+                           "flushed": {k: pct(v) for k, v in flushed.items()} if flushed else None},
         "emitted_tokens_per_step": emitted,
         "roofline": {"bound": "hbm", "kernel": "spexis_verify_attention", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic, "algorithmic_bytes": abytes},
+                     "traffic": traffic, "algorithmic_bytes": abytes,
+                     "frac_of_measured_read": round(achieved / read_peak, 4) if read_peak else None},
+        "roofline_accept": {"bound": "hbm", "kernel": "spexis_accept", "achieved": round(acc_gbs, 1),
+                            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(acc_gbs / HBM_PEAK_GBS, 4),
+                            "traffic": acc_traffic, "algorithmic_bytes": acc_bytes,
+                            "frac_of_measured_read": round(acc_gbs / read_peak, 4) if read_peak else None},
+        "stream_peak_gbs": peaks,
+        "accept_agreement": agreement,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
@@ -499,54 +655,83 @@ def bench_draft(args):
           flush=True)
 
 
-ATTN_KERNELS = ("verify_attn_kernel", "attn_merge_kernel")   # the launches of spexis_verify_attention
 COPY_KERNEL = "copyBuffer"
+# per call: (kernel-name fragments of its launches, the launch that runs exactly once per call,
+# the sources its kernels are built from)
+TRAFFIC_CALLS = {
+    "verify_attention": (("verify_attn_kernel", "attn_merge_kernel"), "verify_attn_kernel", ("attention.hip",)),
+    "accept": (("accept_",), "accept_search_kernel", ("accept.hip",)),
+}
 
 
 def ingest_traffic(fetch_csv: str, write_csv: str, workload: int, copy_bytes: int) -> None:
-    """HBM bytes per spexis_verify_attention call from two counter runs of
-    `bench.py --copy-probe N`: each counter's KiB per dispatch, summed over the call's kernels,
-    averaged over the dispatches, and scaled by N / (the counter's reading for one copy of N
-    bytes), so that a plain copy reads and writes exactly N bytes."""
+    """HBM bytes per spexis_verify_attention and per spexis_accept call from two counter runs of
+    `bench.py --copy-probe N`: each counter's KiB per dispatch, summed over the call's launches
+    and divided by the number of calls, and scaled by N / (the counter's reading for one copy of
+    N bytes), so that a plain copy reads and writes exactly N bytes."""
     import csv
 
     def per_kernel(path, counter):
         rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
         out = {}
         for r in rows:
             out.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]) * 1024.0)
-        return out
+        # the probe: the last three copies before the library's first launch (bench.py makes
+        # them after generating and copying the inputs, before the first step)
+        first = next((i for i, r in enumerate(rows) if "spexis::" in r["Kernel_Name"]), len(rows))
+        copies = [float(r["Counter_Value"]) * 1024.0 for r in rows[:first] if COPY_KERNEL in r["Kernel_Name"]]
+        return out, copies[-3:]
 
-    result = {}
+    readings = {}
     for name, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
-        k = per_kernel(path, name)
-        copies = [v for n, vals in k.items() if COPY_KERNEL in n for v in vals]
-        if not copies:
-            raise SystemExit(f"{path}: no {COPY_KERNEL} dispatch; run the profile with --copy-probe N")
-        probe = max(copies)   # the 3 probe copies are the largest copies of the run
-        size = copy_bytes
-        factor = size / probe
-        attn = sum(float(np.mean(vals)) for n, vals in k.items() if any(a in n for a in ATTN_KERNELS))
-        result[name] = {"raw_bytes_per_call": attn, "copy_reading": probe, "copy_bytes": size,
-                        "factor": factor, "bytes_per_call": attn * factor}
-    total = result["FETCH_SIZE"]["bytes_per_call"] + result["WRITE_SIZE"]["bytes_per_call"]
+        k, probe = per_kernel(path, name)
+        if len(probe) < 3:
+            raise SystemExit(f"{path}: no {COPY_KERNEL} probe dispatches; run the profile with --copy-probe N")
+        readings[name] = (k, float(np.median(probe)))
     prof = os.path.join(ROOT, "profiles", "traffic.json")
     data = json.load(open(prof)) if os.path.exists(prof) else {}
-    data[f"workload{workload}"] = {"source_digest": _kernel_digest(), "bytes_per_launch": round(total),
-                                   "counters": result, "kernels": list(ATTN_KERNELS)}
+    for call, (frags, anchor, sources) in TRAFFIC_CALLS.items():
+        result = {}
+        for name, (k, probe) in readings.items():
+            calls = sum(len(vals) for n, vals in k.items() if anchor in n)
+            if calls == 0:
+                break
+            raw = sum(sum(vals) for n, vals in k.items() if any(f in n for f in frags)) / calls
+            factor = copy_bytes / probe
+            result[name] = {"raw_bytes_per_call": raw, "copy_reading": probe, "copy_bytes": copy_bytes,
+                            "factor": factor, "bytes_per_call": raw * factor, "calls": calls}
+        if len(result) < 2:
+            continue
+        total = result["FETCH_SIZE"]["bytes_per_call"] + result["WRITE_SIZE"]["bytes_per_call"]
+        data[f"workload{workload}:{call}"] = {"source_digest": _kernel_digest(sources),
+                                              "bytes_per_launch": round(total), "counters": result,
+                                              "kernels": list(frags)}
     with open(prof, "w") as f:
-        json.dump(data, f, indent=1)
+        json.dump(data, f, indent=1, sort_keys=True)
         f.write("\n")
-    print(json.dumps(data[f"workload{workload}"], indent=1))
+    print(json.dumps({k: v for k, v in data.items() if k.startswith(f"workload{workload}:")}, indent=1))
 
 
-def _kernel_digest() -> str:
-    """Digest of the sources the attention kernels are built from (their code, the shared device
+def stored_traffic(workload: int, call: str):
+    """Calibrated counter bytes per call from profiles/traffic.json, if taken on the current sources."""
+    prof = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(prof):
+        return None
+    with open(prof) as f:
+        t = json.load(f).get(f"workload{workload}:{call}")
+    if t and t.get("source_digest") == _kernel_digest(TRAFFIC_CALLS[call][2]):
+        return t["bytes_per_launch"]
+    return None
+
+
+def _kernel_digest(sources=("attention.hip",)) -> str:
+    """Digest of the sources a call's kernels are built from (their code, the shared device
     helpers, and the header with their parameters and launch constants): a stored traffic figure
     is used only while they are unchanged."""
     import hashlib
     h = hashlib.sha256()
-    for name in ("attention.hip", "common.h", "kernels.h"):
+    for name in tuple(sources) + ("common.h", "kernels.h"):
         with open(os.path.join(ROOT, "paper_2609_34370_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]

@@ -84,6 +84,8 @@ extern "C" {
 #define SPEXIS_ROW_EMPTY 1      /* the sampled target row had no positive entry */
 #define SPEXIS_ROW_BAD_VALUE 2  /* the sampled row held a NaN, an infinity or a negative value */
 #define SPEXIS_ROW_BAD_TOKEN 3  /* a draft token id outside [0, vocab) */
+#define SPEXIS_ROW_INTERNAL 4   /* the sampling search found no token (a library fault, never
+                                   expected): token -1, seq_lens_inout unchanged */
 
 /* input kinds of spexis_accept */
 #define SPEXIS_INPUT_PROBS 0
@@ -166,9 +168,13 @@ int spexis_verify_attention(const void* k_cache, const void* v_cache, int32_t nu
                             void* stream);
 
 /*
- * spexis_softmax_rows -- probs[r][v] = exp((logits[r][v] - max_u logits[r][u]) / T) /
- * sum_u exp(...), fp32, for rows r < rows (the temperature divides the logits of target and
- * draft rows alike).  logits and probs are [rows][vocab] fp32 and may alias.
+ * spexis_softmax_rows -- the probabilities p = softmax(logits / T) and q that the acceptance
+ * rule of [sd] (Related Work) compares, for callers that pass probabilities to spexis_accept
+ * (Sec. 4: the verifying model's outputs are turned into per-token probabilities):
+ * probs[r][v] = exp((logits[r][v] - max_u logits[r][u]) / T) / sum_u exp(...), fp32, for rows
+ * r < rows (the temperature divides the logits of target and draft rows alike).  Computed as
+ * 2^(x c - M) / Z with c = log2(e) / T, the expression spexis_accept uses with logits.  logits
+ * and probs are [rows][vocab] fp32 and may alias.
  * Errors: INVALID_ARGUMENT (null, rows < 0, vocab <= 0, temperature <= 0 or not finite).
  */
 int spexis_softmax_rows(const float* logits, float* probs, int64_t rows, int32_t vocab,
@@ -194,7 +200,7 @@ size_t spexis_accept_workspace_size(int32_t num_seqs, int32_t vocab, int32_t max
  *      a_b = number of leading accepts.
  *   3. a_b < k_b: weights w = max(0, fp32(p_a - q_a)); a_b = k_b: w = p_k (bonus).  Rows
  *      read here must be finite and >= 0, else row_status = BAD_VALUE and the token at
- *      position a_b is -1.
+ *      position a_b is -1.  (row_status = INTERNAL flags a library fault, never expected.)
  *   4. the token at position a_b is the inverse-CDF sample of w with u_sample[b], taken in
  *      exact fixed point at the scale of the target row: M = max p_a in [2^e, 2^(e+1)),
  *      W_v = floor(w_v * 2^(40-e)), S = sum W_v (if S = 0 for a residual, the weights are

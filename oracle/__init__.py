@@ -59,6 +59,8 @@ def lib():
         L.oracle_softmax.restype = None
         L.oracle_accept.argtypes = [i32, i32, i32, P, P, P, P, P, P, P, P, P, P]
         L.oracle_accept.restype = None
+        L.oracle_set_num_threads.argtypes = [ctypes.c_int]
+        L.oracle_set_num_threads.restype = None
         L.oracle_num_threads.argtypes = []
         L.oracle_num_threads.restype = ctypes.c_int
         _lib = L
@@ -76,6 +78,11 @@ def _p(a: np.ndarray):
 
 def num_threads() -> int:
     return int(lib().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops from now on."""
+    lib().oracle_set_num_threads(int(n))
 
 
 def append_kv(k_pool: np.ndarray, v_pool: np.ndarray, num_blocks: int, num_kv_heads: int, block_size: int,

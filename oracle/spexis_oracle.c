@@ -513,6 +513,15 @@ int oracle_lookahead(int32_t n, const int64_t* cur_len, const int32_t* remaining
   return 0;
 }
 
+/* Threads of the parallel loops above from now on (n >= 1; no effect without OpenMP). */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* Number of OpenMP threads the parallel loops above use (for reporting). */
 int oracle_num_threads(void) {
   int n = 1;

@@ -48,6 +48,7 @@ constexpr int kPerLane = 4 * kF4;                // vocab entries per lane (16)
 constexpr int kRoundGrid = 65536;                // workgroups of a later test round (256 per CU)
 constexpr int64_t kOneRoundBytes = 192ll << 20;  // target rows that one test round reads whole
 constexpr int64_t kRoundRowBytes = 256ll << 10;  // rows this long pay for the launches of a round
+constexpr int64_t kNarrowFirstBytes = 256ll << 20;  // a first round over {0,1} reading more starts with {0}
 
 enum Mode { kResidual = 1, kBonus = 2, kDone = 3 };
 
@@ -75,9 +76,10 @@ __device__ __forceinline__ Geom seq_geom(const AcceptParams& p, int b, int& n) {
 }
 
 // p = 2^(x*c - M) * (1/Z): the probability of a logit, the same expression in every pass
-// (R = 1/Z is rounded once per row).
+// (R = 1/Z is rounded once per row).  x*c - M is one explicit fused multiply-add, so no site
+// can contract it differently from another: every pass sees the same probabilities.
 __device__ __forceinline__ float logit_prob(float x, float c, float M, float R) {
-  return fast_exp2(x * c - M) * R;
+  return fast_exp2(__builtin_fmaf(x, c, -M)) * R;
 }
 
 __device__ __forceinline__ bool bad_value(float x) { return !(x >= 0.f) || isinf(x); }
@@ -754,6 +756,17 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
   const int s = 40 - floor_log2(M);
   const bool vec = (p.V & 3) == 0;
   const float fill = r.logits ? -INFINITY : 0.f;
+  int32_t* orow = p.out_tokens + (int64_t)b * (p.max_k + 1);
+  // Until the thread whose prefix range holds the threshold overwrites them (after the barrier
+  // below), the outputs say that no token was found.  That cannot happen while every pass
+  // computes the same weights; if it ever did, the row reports it instead of keeping the
+  // previous call's outputs.
+  if (lead) {
+    orow[a] = -1;
+    p.accepted_len[b] = a;
+    p.row_status[b] = SPEXIS_ROW_INTERNAL;
+    if (p.tok_prob) p.tok_prob[b] = 0.f;
+  }
   // a residual whose fixed-point weights are all 0 falls back to p
   const bool use_p = !residual || wave_sum_u64(own_r) == 0;
   const int which = use_p ? 1 : 0;
@@ -788,7 +801,6 @@ __global__ __launch_bounds__(kThreads) void accept_search_kernel(AcceptParams p)
   if (cstar < 0) return;   // unreachable: S > 0 (p's largest entry alone weighs >= 2^40)
   // the output row but its sampled entry: the accepted drafts, then -1 (wave 0; the id loads go
   // out with the sub-chunk's, the stores follow them)
-  int32_t* orow = p.out_tokens + (int64_t)b * (p.max_k + 1);
   static_assert(kAcceptMaxK < kWave, "one lane per accepted draft");
   int idv = -1;
   if (wave == 0 && lane < a) idv = p.ids[g.d0 + lane];   // a <= max_k <= kAcceptMaxK
@@ -938,12 +950,16 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
     // Rounds of doubling width until position max_k is covered.  A round costs a few
     // microseconds of launch and latency, a row 4V bytes: with short rows (under 256 KB) that
     // together stream in well under that many rounds' worth of time, one round reads every
-    // row; otherwise the first round is two positions wide ({0,1}, {2..5}, {6..13}, ...), since
-    // most sequences pass the first test at usual acceptance rates.  (Measured: rounds save
-    // 3.5 us at 64 sequences of 128256-entry rows, and cost 2.6 us at 128 of 32000.)
+    // row.  Otherwise the first round is two positions wide ({0,1}, {2..5}, {6..13}, ...), so
+    // that sequences passing the first test need no extra launch, unless its four rows per
+    // sequence come to more than 256 MB: then the rows a first rejection leaves unread cost
+    // more than a launch, and the rounds are {0}, {1,2}, {3..6}, ....  (Measured: rounds save
+    // 3.5 us at 64 sequences of 128256-entry rows, and cost 2.6 us at 128 of 32000; a first
+    // round of one position costs 7 us at 64 sequences of 128256 entries and saves 3 us at 256
+    // of them and 57 us at 512 of 152064.)
     const bool one_round =
         (int64_t)p.V * 4 < kRoundRowBytes && (int64_t)p.B * (p.max_k + 1) * p.V * 4 <= kOneRoundBytes;
-    int width = one_round ? p.max_k + 1 : 2;
+    int width = one_round ? p.max_k + 1 : ((int64_t)p.B * 4 * p.V * 4 > kNarrowFirstBytes ? 1 : 2);
     {
       const unsigned gs = (unsigned)((int64_t)p.B * 2 * width * p.nsub);
       hipLaunchKernelGGL(accept_stats_kernel, dim3(gs), dim3(kThreads), 0, s, p, width);

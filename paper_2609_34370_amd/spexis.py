@@ -25,7 +25,7 @@ SPEXIS_ERR_WORKSPACE_TOO_SMALL = -3
 SPEXIS_ERR_HIP = -4
 SPEXIS_INPUT_PROBS = 0
 SPEXIS_INPUT_LOGITS = 1
-SPEXIS_ROW_OK, SPEXIS_ROW_EMPTY, SPEXIS_ROW_BAD_VALUE, SPEXIS_ROW_BAD_TOKEN = 0, 1, 2, 3
+SPEXIS_ROW_OK, SPEXIS_ROW_EMPTY, SPEXIS_ROW_BAD_VALUE, SPEXIS_ROW_BAD_TOKEN, SPEXIS_ROW_INTERNAL = 0, 1, 2, 3, 4
 
 
 class SpexisError(RuntimeError):
