@@ -45,12 +45,15 @@ constexpr int kWaves = kThreads / kWave;
 constexpr int kWaveSub = kAcceptSub / kWaves;   // entries of a sub-chunk one wave takes (1024)
 constexpr int kF4 = kWaveSub / (kWave * 4);      // float4 loads per lane (4)
 constexpr int kPerLane = 4 * kF4;                // vocab entries per lane (16)
-constexpr int kRoundGrid = 65536;                // workgroups of a later test round (256 per CU)
+constexpr int kRoundGrid = 65536;                // workgroups of a later round's stream (256 per CU)
+constexpr int kTestsGrid = 4096;                 // workgroups of a later round's tests
 constexpr int64_t kOneRoundBytes = 192ll << 20;  // target rows that one test round reads whole
 constexpr int64_t kRoundRowBytes = 256ll << 10;  // rows this long pay for the launches of a round
 constexpr int64_t kNarrowFirstBytes = 256ll << 20;  // a first round over {0,1} reading more starts with {0}
 
 enum Mode { kResidual = 1, kBonus = 2, kDone = 3 };
+// the job of a listed sequence in a round's stream launch
+enum Job { kJobNone = 0, kJobResidual = 1, kJobBonus = 2, kJobNext = 3 };
 
 struct Geom {
   int t0, d0, k, valid;
@@ -503,14 +506,12 @@ __device__ __forceinline__ void store_sub_stats(const AcceptParams& p, float (&v
 
 // A round's positions [lo, hi) of sequence b over sub-chunk `sub`: statistics of target rows
 // lo..min(hi-1, k) and draft rows lo..min(hi, k)-1 (target rows first), each row's loads issued
-// before the previous row reduces; the item of sub-chunk 0 gathers the round's test inputs.
+// before the previous row reduces.
 __device__ void next_round_stats(const AcceptParams& p, int b, const Geom& g, int lo, int hi, int sub, int wave,
                                  int lane) {
   const int nt = min(hi - 1, g.k) - lo + 1;   // >= 1: lo <= k
   const int nd = max(0, min(hi, g.k) - lo);
   const int rows = nt + nd;
-  if (sub == 0 && threadIdx.x == 0)
-    for (int pos = lo; pos < min(hi, g.k); ++pos) gather_test(p, b, g, pos);
   const bool vec = (p.V & 3) == 0;
   auto row = [&](int j) {
     return j < nt ? p.target + (int64_t)(g.t0 + lo + j) * p.V : p.draft + (int64_t)(g.d0 + lo + j - nt) * p.V;
@@ -628,24 +629,29 @@ __global__ __launch_bounds__(kThreads) void accept_gather_kernel(AcceptParams p)
   gather_test(p, b, g, i);
 }
 
-// Round r, positions [lo, hi): one work item per (sequence of the list, sub-chunk).  Every item
-// of a sequence runs the tests at those positions (its waves split them) and reaches the same
-// first failure.  A failure at a: the sequence is done testing (residual at a), and the item
-// computes the fixed-point sums of the residual of row a over its sub-chunk.  No failure: the
-// same for the bonus row if the round reached position k, else the sequence joins round r+1
-// (positions [hi, hi2)) and the item computes that round's statistics over its sub-chunk.
-__global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p, int r, int lo, int hi, int hi2) {
+// Round r, positions [lo, hi), step 1 of 2: one workgroup per sequence of the round's list runs
+// the tests at those positions from the statistics (its waves split the positions) and finds
+// the first failure.  A failure at a: the sequence is done testing, and the residual of row a
+// will be sampled.  No failure: the bonus row k will be sampled if the round reached position
+// k, else the sequence joins round r+1 (positions [hi, hi2)), whose test inputs it gathers.
+// It leaves the stream launch of the round one record per list entry (the job: the fixed-point
+// sums of the sampled row at its scale, or round r+1's statistics) and the search its record.
+// So the stream launch's items start streaming after one load, instead of each repeating the
+// tests.
+__global__ __launch_bounds__(kThreads) void accept_tests_kernel(AcceptParams p, int r, int lo, int hi, int hi2) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int64_t total = (int64_t)round_count(p, r) * p.nsub;
+  const int count = round_count(p, r);
   __shared__ int sm_fail[kWaves];
-  for (int64_t item = blockIdx.x; item < total; item += gridDim.x) {
-    const int sub = (int)(item % p.nsub), li = (int)(item / p.nsub);
-    const bool lead = sub == 0 && threadIdx.x == 0;
+  for (int li = blockIdx.x; li < count; li += gridDim.x) {
     int b;
     Geom g;
     round_seq(p, r, li, b, g);
+    u32x4* rec = reinterpret_cast<u32x4*>(p.strec) + 3 * (int64_t)li;
     if (r == 0 && g.valid != 1) {   // no query token, or a draft id out of range
-      if (lead) write_invalid(p, b, g.valid == 0 ? 0 : 1);
+      if (threadIdx.x == 0) {
+        write_invalid(p, b, g.valid == 0 ? 0 : 1);
+        rec[1] = u32x4{(uint32_t)kJobNone, 0u, 0u, 0u};
+      }
       continue;
     }
     // position i fails when !(u_i q_i(x_i) < p_i(x_i)) (NaN statistics fail)
@@ -653,8 +659,6 @@ __global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p,
     const int end = min(hi, g.k);
     int fail = g.k + 1;   // none
     for (int i = lo + wave; i < end; i += kWaves) {
-      // the three floats a test uses (loading the fourth, unused, would let its register be
-      // reused at once, which waits for the load before the statistics' loads are issued)
       const f32x2 t = *reinterpret_cast<const f32x2*>(tin + 4 * i);
       const float u = tin[4 * i + 2];
       const RowCtx rc = row_ctx(p, b, g, i, true, lane);
@@ -669,20 +673,86 @@ __global__ __launch_bounds__(kThreads) void accept_decide_kernel(AcceptParams p,
     __syncthreads();
     const int a = min(min(sm_fail[0], sm_fail[1]), min(sm_fail[2], sm_fail[3]));
     __syncthreads();
+    if (wave != 0) continue;
+    const u32x4 q0 = u32x4{(uint32_t)b, (uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k};
     if (a < g.k || hi > g.k) {
       // a failure at a: the residual of row a; every test passed and the round reached k: the
-      // bonus row k.  Either way the scale is known from row a's statistics, so the sums follow.
+      // bonus row k.  Either way the scale is known from row a's statistics.
       const bool residual = a < g.k;
-      sample_sums(p, b, g, residual ? a : g.k, residual, sub, wave, lane);
+      const int pos = residual ? a : g.k;
+      const RowCtx rc = row_ctx(p, b, g, pos, residual, lane);
+      float M;
+      int bad;
+      sampled_scale(p, rc, b, residual, lane, M, bad);
+      if (lane == 0) {
+        const u32x4 stats{__float_as_uint(rc.Mp), __float_as_uint(rc.Rp), __float_as_uint(rc.Mq),
+                          __float_as_uint(rc.Rq)};
+        u32x4* srec = reinterpret_cast<u32x4*>(p.srec) + 3 * (int64_t)b;
+        srec[0] = u32x4{(uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k, (uint32_t)pos};
+        srec[1] = u32x4{(uint32_t)(residual ? kResidual : kBonus), (uint32_t)bad, __float_as_uint(M), 0u};
+        srec[2] = stats;
+        // a bad or empty row has no sums to compute (the search reports it)
+        const bool go = !bad && M > 0.f;
+        rec[0] = q0;
+        rec[1] = u32x4{(uint32_t)(go ? (residual ? kJobResidual : kJobBonus) : kJobNone), (uint32_t)pos, 0u,
+                       (uint32_t)(go ? 40 - floor_log2(M) : 0)};
+        rec[2] = stats;
+      }
     } else {
       // hi <= k <= max_k: round r+1 exists (the host passes hi2 > hi)
-      if (lead) {
+      if (lane == 0) {
         const int at = __hip_atomic_fetch_add(p.counts + r + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        *reinterpret_cast<u32x4*>(p.lists + ((int64_t)r * p.B + at) * 4) =
-            u32x4{(uint32_t)b, (uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k};
+        *reinterpret_cast<u32x4*>(p.lists + ((int64_t)r * p.B + at) * 4) = q0;
+        rec[0] = q0;
+        rec[1] = u32x4{(uint32_t)kJobNext, (uint32_t)hi, (uint32_t)hi2, 0u};
       }
-      next_round_stats(p, b, g, hi, hi2, sub, wave, lane);
+      for (int pos = hi + lane; pos < min(hi2, g.k); pos += kWave) gather_test(p, b, g, pos);
     }
+  }
+}
+
+// Round r, step 2 of 2: one work item per (sequence of the list, sub-chunk) does the job the
+// tests launch recorded for the sequence: the fixed-point sums of the sampled row(s) over its
+// sub-chunk, or the statistics of round r+1's rows over its sub-chunk.  So the sampled rows of
+// finished sequences stream together with the next round's rows.
+__global__ __launch_bounds__(kThreads) void accept_stream_kernel(AcceptParams p, int r) {
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int64_t total = (int64_t)round_count(p, r) * p.nsub;
+  const bool vec = (p.V & 3) == 0;
+  for (int64_t item = blockIdx.x; item < total; item += gridDim.x) {
+    const int sub = (int)(item % p.nsub), li = (int)(item / p.nsub);
+    const u32x4* rec = reinterpret_cast<const u32x4*>(p.strec) + 3 * (int64_t)li;
+    const u32x4 q0 = rec[0], q1 = rec[1], q2 = rec[2];
+    const int job = (int)q1[0];
+    if (job != kJobResidual && job != kJobBonus && job != kJobNext) continue;
+    const int b = (int)q0[0];
+    const Geom g{(int)q0[1], (int)q0[2], (int)q0[3], 1};
+    if (job == kJobNext) {
+      next_round_stats(p, b, g, (int)q1[1], (int)q1[2], sub, wave, lane);
+      continue;
+    }
+    const bool residual = job == kJobResidual;
+    const int a = (int)q1[1];
+    RowCtx rc;
+    rc.P = p.target + (int64_t)(g.t0 + a) * p.V;
+    rc.Q = residual ? p.draft + (int64_t)(g.d0 + a) * p.V : nullptr;
+    rc.logits = p.kind == 1;
+    rc.Mp = __uint_as_float(q2[0]);
+    rc.Rp = __uint_as_float(q2[1]);
+    rc.Mq = __uint_as_float(q2[2]);
+    rc.Rq = __uint_as_float(q2[3]);
+    // non-temporal: the search reads back one sub-chunk of these rows at most (measured: the
+    // acceptance of 512 sequences of 152064-entry rows 6 us faster, a whole verification step
+    // about 2 us, and no slower at 64 sequences of 128256)
+    float pv[kPerLane], qv[kPerLane];
+    load_sub<true>(rc.P, sub, wave, p.V, vec, -INFINITY, lane, pv);
+    if (residual) {
+      load_sub<true>(rc.Q, sub, wave, p.V, vec, -INFINITY, lane, qv);
+    } else {
+#pragma unroll
+      for (int e = 0; e < kPerLane; ++e) qv[e] = 0.f;
+    }
+    sub_sums(p, rc, residual, b, sub, (int)q1[3], wave, lane, pv, qv);
   }
 }
 
@@ -909,6 +979,19 @@ hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V
   return hipGetLastError();
 }
 
+// Tests, then stream, of round r.  Later rounds, whose size the host does not know, have
+// capped grids.
+static hipError_t launch_round(const AcceptParams& p, int r, int lo, int hi, int hi2, hipStream_t s) {
+  const unsigned items = (unsigned)((int64_t)p.B * p.nsub);
+  const unsigned gt = r == 0 || p.B < kTestsGrid ? (unsigned)p.B : (unsigned)kTestsGrid;
+  hipLaunchKernelGGL(accept_tests_kernel, dim3(gt), dim3(kThreads), 0, s, p, r, lo, hi, hi2);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const unsigned gs = r == 0 || items < (unsigned)kRoundGrid ? items : (unsigned)kRoundGrid;
+  hipLaunchKernelGGL(accept_stream_kernel, dim3(gs), dim3(kThreads), 0, s, p, r);
+  return hipGetLastError();
+}
+
 static hipError_t launch_search(const AcceptParams& p, hipStream_t s) {
   hipLaunchKernelGGL(accept_search_kernel, dim3(p.B), dim3(kThreads), 0, s, p);
   return hipGetLastError();
@@ -942,8 +1025,7 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
                          s, q);
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(accept_decide_kernel, dim3(items), dim3(kThreads), 0, s, q, 0, 0, q.max_k + 1, 0);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_round(q, 0, 0, q.max_k + 1, 0, s)) != hipSuccess) return e;
     return launch_search(q, s);
   }
   if (p.kind == 1) {
@@ -966,13 +1048,10 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     for (int r = 0, lo = 0; lo <= p.max_k; ++r, lo += width, width *= 2) {
-      // decide round r; a sequence passing all of it computes round r+1's statistics.  Later
-      // rounds, whose size the host does not know, have a capped grid.
+      // round r; a sequence passing all of it computes round r+1's statistics
       const int hi = lo + width;
       const int hi2 = hi <= p.max_k ? hi + 2 * width : 0;
-      const unsigned gd = r == 0 || items < (unsigned)kRoundGrid ? items : (unsigned)kRoundGrid;
-      hipLaunchKernelGGL(accept_decide_kernel, dim3(gd), dim3(kThreads), 0, s, p, r, lo, hi, hi2);
-      if ((e = hipGetLastError()) != hipSuccess) return e;
+      if ((e = launch_round(p, r, lo, hi, hi2, s)) != hipSuccess) return e;
     }
   } else {
     hipLaunchKernelGGL(accept_init_kernel, dim3((p.B + kThreads - 1) / kThreads), dim3(kThreads), 0, s, p);

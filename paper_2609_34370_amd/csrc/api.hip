@@ -88,7 +88,7 @@ bool attn_waves(int32_t num_seqs, int32_t num_kv_heads, int32_t max_seq_len, int
 }
 
 struct AcceptLayout {
-  size_t geo, st_a, st_mode, counts, lists, lse, tin, max_part, bad_part, sum_part, srec, total;
+  size_t geo, st_a, st_mode, counts, lists, lse, tin, max_part, bad_part, sum_part, srec, strec, total;
 };
 
 int64_t accept_nsub(int64_t V) { return (V + spexis::kAcceptSub - 1) / spexis::kAcceptSub; }
@@ -113,6 +113,7 @@ AcceptLayout accept_layout(int64_t B, int64_t V, int64_t max_k) {
   l.bad_part = take(B * ns * 4);
   l.sum_part = take(B * ns * 2 * 8);
   l.srec = take(B * 48);
+  l.strec = take(B * 48);
   l.total = off;
   return l;
 }
@@ -340,6 +341,7 @@ int accept_impl(const char* who, int32_t kind, int32_t num_seqs, int32_t vocab, 
   p.bad_part = reinterpret_cast<int32_t*>(ws + lay.bad_part);
   p.sum_part = reinterpret_cast<uint64_t*>(ws + lay.sum_part);
   p.srec = reinterpret_cast<int32_t*>(ws + lay.srec);
+  p.strec = reinterpret_cast<int32_t*>(ws + lay.strec);
   p.ext_tstats = target_stats;
   p.ext_dstats = draft_stats;
   p.ext_parts = stats_parts;

@@ -140,7 +140,10 @@ struct AcceptParams {
   int32_t* bad_part;     // [B][nsub] the sampled row(s) hold a bad value (probability inputs)
   uint64_t* sum_part;    // [B][nsub][2] fixed-point sums of the residual and of p
   int32_t* srec;         // [B][12] the search's record of b: t0, d0, k, a | mode, bad, scale, 0 |
-                         // Mp, Rp, Mq, Rq (written with the sums of sub-chunk 0, or by write_invalid)
+                         // Mp, Rp, Mq, Rq (written by the tests launch that ends its testing, or
+                         // by write_invalid)
+  int32_t* strec;        // [B][12] a round's job per list entry (logits mode): b, t0, d0, k | job,
+                         // position or next round's lo, next round's hi, shift | Mp, Rp, Mq, Rq
 };
 
 constexpr int kAcceptMaxK = 32;      // drafts per sequence the boundary takes (below one wave's lanes)
