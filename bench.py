@@ -211,6 +211,9 @@ def main():
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--kv-chunk", type=int, default=0)
+    ap.add_argument("--graph", action="store_true",
+                    help="replay each input copy's step from a HIP graph (captured before timing) in the timed "
+                         "loops, instead of launching its calls one by one")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="first copy BYTES device-to-device 3 times (a known-size kernel for counter calibration); "
@@ -279,8 +282,12 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    if args.graph:
+        for st in steps:
+            st.capture()
+    go = [st.replay if args.graph else st.run for st in steps]
     for i in range(args.warmup):
-        steps[i % R].run()
+        go[i % R]()
     torch.cuda.synchronize()
 
     K = args.steps
@@ -288,14 +295,14 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(K):
-        steps[i % R].run()
+        go[i % R]()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     # The same K steps warm (one copy of the inputs, back to back), beside the headline.
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(K):
-        step.run()
+        go[0]()
     torch.cuda.synchronize()
     elapsed_warm = time.perf_counter() - t0
 
@@ -358,7 +365,8 @@ def main():
         "config": {"workload": spec.name, "batch": batch.B, "q_heads": spec.num_q_heads,
                    "kv_heads": spec.num_kv_heads, "head_dim": spec.head_dim, "block_size": spec.block_size,
                    "context": list(spec.ctx), "draft_tokens": list(spec.k), "vocab": spec.vocab,
-                   "temperature": spec.temperature, "accept_input": "logits", "parallelism": "none"},
+                   "temperature": spec.temperature, "accept_input": "logits", "parallelism": "none",
+                   "launch": "hip_graph" if args.graph else "eager"},
         "protocol": f"cold (headline): {R} copies of the inputs used in turn, {(R - 1) * abytes / 2**30:.2f} GiB "
                     f"of other steps' attention reads between two uses of one copy; warm: one copy back to back; "
                     f"flushed: one copy, a 1 GiB read before each step (phase times only)",
