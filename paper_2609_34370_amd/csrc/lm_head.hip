@@ -309,6 +309,210 @@ void lm_head_kernel(LmParams p) {
   }
 }
 
+// 129 to 320 rows of a wide projection (an LM head's vocabulary): one workgroup of eight waves
+// (two per SIMD) per 256-column tile takes every row, so each K-slice of W is read from HBM and
+// through L2 once, by one workgroup.  Both operands go through LDS: every K-step of 64 the
+// workgroup's threads copy h (320 rows, 40 KB) and W (eight packed 32-column tiles, 32 KB) into
+// one of two stages, loaded one step ahead into registers, and the waves read their fragments
+// from the stage.  Wave (wr, wc) of a 2 x 4 grid computes rows 160 wr .. +160 (five row tiles)
+// by columns 64 wc .. +64 (two column tiles): 160 accumulators, within the 256 registers a wave
+// has at two waves per SIMD.  Against four waves per 160-row x 256-column workgroup (two row
+// groups, each reading W), the L2 serves about 2.35 GB instead of 3.4 GB at 320 x 4096 @ 128256.
+// Epilogue as lm_head_kernel's: logits or bf16 outputs, then each row's statistics per
+// 128-column tile.
+__global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
+  constexpr int RT = 5, CT = 2, WR = 2, WC = 4;
+  constexpr int NRT = WR * RT;        // row tiles of the workgroup
+  constexpr int kRows = 32 * NRT;     // 320
+  constexpr int kCols = 32 * WC * CT; // 256
+  constexpr int kStatTiles = kCols / kLmCols;
+  constexpr int kHChunks = kRows * 8 / 512;   // 16-byte h chunks each thread copies per step (5)
+  constexpr int kWChunks = 8 * 256 / 512;     // 16-byte W chunks each thread copies per step (4)
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 31, half = lane >> 5;
+  const int wr = wave / WC, wc = wave % WC;
+  const int wgcols = (p.V + kCols - 1) / kCols;
+  int nt, mg;
+  tile_of(blockIdx.x, wgcols, 1, nt, mg);
+  if (nt >= wgcols) return;
+  const int n0 = nt * kCols;
+  const int rows = min(kRows, p.M);
+  const int nsteps = p.d / kLmK;
+  const int wtiles = (p.V + 31) / 32;
+  const uint16_t* hbase = reinterpret_cast<const uint16_t*>(p.h);
+  const uint16_t* wbase = reinterpret_cast<const uint16_t*>(p.w);
+
+  // stage x of h: row r, chunk kc (8 K values) at r * 8 + (kc ^ ((r >> 1) & 7)) (the 16 rows of
+  // one ds_read_b128 pass hit distinct bank groups); stage x of W: packed tile c (columns
+  // n0 + 32 c ..), its 256 chunks in packed order
+  __shared__ u32x4 sm_h[2][kRows * 8];
+  __shared__ u32x4 sm_w[2][8 * 256];
+  u32x4 hreg[kHChunks], wreg[kWChunks];
+  auto load_step = [&](int j) {
+    j = min(j, nsteps - 1);   // past the end: re-read the last step (kept unconditional)
+#pragma unroll
+    for (int u = 0; u < kHChunks; ++u) {
+      const int q = threadIdx.x + 512 * u;
+      const int r = min(q >> 3, rows - 1), kc = q & 7;
+      hreg[u] = *reinterpret_cast<const u32x4*>(hbase + (int64_t)r * p.d + j * kLmK + 8 * kc);
+    }
+#pragma unroll
+    for (int u = 0; u < kWChunks; ++u) {
+      const int q = threadIdx.x + 512 * u;
+      const int wt = min(n0 / 32 + (q >> 8), wtiles - 1);
+      wreg[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(
+          wbase + ((int64_t)wt * (p.d / kLmK) + j) * kPackTile + 8 * (q & 255)));
+    }
+  };
+  auto store_step = [&](int stage) {
+#pragma unroll
+    for (int u = 0; u < kHChunks; ++u) {
+      const int q = threadIdx.x + 512 * u;
+      const int r = q >> 3, kc = q & 7;
+      sm_h[stage][r * 8 + (kc ^ ((r >> 1) & 7))] = hreg[u];
+    }
+#pragma unroll
+    for (int u = 0; u < kWChunks; ++u) sm_w[stage][threadIdx.x + 512 * u] = wreg[u];
+  };
+
+  f32x16 acc[RT][CT];
+#pragma unroll
+  for (int t = 0; t < RT; ++t)
+#pragma unroll
+    for (int c = 0; c < CT; ++c)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[t][c][e] = 0.f;
+
+  auto compute = [&](int stage) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      u32x4 b[CT], a[RT];
+#pragma unroll
+      for (int c = 0; c < CT; ++c) b[c] = sm_w[stage][(CT * wc + c) * 256 + s * 64 + lane];
+#pragma unroll
+      for (int t = 0; t < RT; ++t) {
+        const int m = 32 * (wr * RT + t) + col;
+        a[t] = sm_h[stage][m * 8 + ((4 * half + s) ^ ((m >> 1) & 7))];
+      }
+#pragma unroll
+      for (int t = 0; t < RT; ++t)
+#pragma unroll
+        for (int c = 0; c < CT; ++c)
+          acc[t][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a[t]), as_bf16x8(b[c]), acc[t][c], 0, 0, 0);
+    }
+  };
+
+  // step j: compute from stage j % 2 while step j+1's copies (loaded during step j-1) go into the
+  // other stage, then load step j+2
+  load_step(0);
+  store_step(0);
+  load_step(1);
+  __syncthreads();
+  for (int j = 0; j < nsteps; ++j) {
+    compute(j & 1);
+    store_step((j + 1) & 1);
+    load_step(j + 2);
+    __syncthreads();
+  }
+
+  // ---- epilogue (accumulator value i of lane l in tile (t, c): row 32 (wr RT + t) + 8 (i / 4)
+  // + 4 (l / 32) + i % 4, column 32 (CT wc + c) + l % 32)
+  auto out_row = [&](int t, int i) { return 32 * (wr * RT + t) + 8 * (i >> 2) + 4 * half + (i & 3); };
+  auto out_col = [&](int c) { return n0 + 32 * (CT * wc + c) + col; };
+  if (p.logits) {
+#pragma unroll
+    for (int c = 0; c < CT; ++c) {
+      const int v = out_col(c);
+      if (v >= p.V) continue;
+#pragma unroll
+      for (int t = 0; t < RT; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int r = out_row(t, i);
+          if (r < rows) __builtin_nontemporal_store(acc[t][c][i], p.logits + (int64_t)r * p.V + v);
+        }
+    }
+  }
+  if (p.y) {
+    const uint16_t* res = reinterpret_cast<const uint16_t*>(p.res);
+    uint16_t* y = reinterpret_cast<uint16_t*>(p.y);
+#pragma unroll
+    for (int c = 0; c < CT; ++c) {
+      const int v = out_col(c);
+      if (v >= p.V) continue;
+#pragma unroll
+      for (int t = 0; t < RT; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int r = out_row(t, i);
+          if (r < rows) {
+            const int64_t at = (int64_t)r * p.V + v;
+            y[at] = bf16_rne(res ? acc[t][c][i] + bf16_float(res[at]) : acc[t][c][i]);
+          }
+        }
+    }
+  }
+  if (!p.stats) return;
+  // Row statistics: each wave transposes one 32x32 tile at a time through its part of the (now
+  // free) h stages; lane r < 32 reduces row r over the tile's 32 columns, then over the wave's CT
+  // tiles in order; the two waves of a row and 128-column statistics tile combine in order.
+  __shared__ float sm_m[WC][kRows], sm_z[WC][kRows];
+  constexpr int kTS = 36;   // floats per transposed row (16-byte aligned, padded)
+  float* tile = reinterpret_cast<float*>(&sm_h[0][0]) + wave * 32 * kTS;
+#pragma unroll
+  for (int t = 0; t < RT; ++t) {
+    float wm = -INFINITY, wz = 0.f;
+#pragma unroll
+    for (int c = 0; c < CT; ++c) {
+      const bool live = out_col(c) < p.V;
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        tile[(8 * (i >> 2) + 4 * half + (i & 3)) * kTS + col] = live ? acc[t][c][i] * p.c : -INFINITY;
+      if (lane < 32) {
+        f32x4 x[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) x[q] = *reinterpret_cast<const f32x4*>(tile + lane * kTS + 4 * q);
+        float mx = -INFINITY;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) mx = fmaxf(fmaxf(mx, fmaxf(x[q][0], x[q][1])), fmaxf(x[q][2], x[q][3]));
+        float e = 0.f;
+        if (mx != -INFINITY) {
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+#pragma unroll
+            for (int u = 0; u < 4; ++u) e += fast_exp2(x[q][u] - mx);
+        }
+        if (c == 0) {
+          wm = mx;
+          wz = e;
+        } else {
+          const float M = fmaxf(wm, mx);
+          wz = (wm != -INFINITY ? wz * fast_exp2(wm - M) : 0.f) + (mx != -INFINITY ? e * fast_exp2(mx - M) : 0.f);
+          wm = M;
+        }
+      }
+    }
+    if (lane < 32) {
+      sm_m[wc][32 * (wr * RT + t) + lane] = wm;
+      sm_z[wc][32 * (wr * RT + t) + lane] = wz;
+    }
+  }
+  __syncthreads();
+  constexpr int kWavesPerStat = WC / kStatTiles;
+  for (int q = threadIdx.x; q < rows * kStatTiles; q += 512) {
+    const int r = q % rows, st = q / rows, w0 = st * kWavesPerStat;
+    const int stile = nt * kStatTiles + st;
+    if (stile >= p.ntiles) continue;
+    float M = sm_m[w0][r];
+#pragma unroll
+    for (int w = 1; w < kWavesPerStat; ++w) M = fmaxf(M, sm_m[w0 + w][r]);
+    float Z = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWavesPerStat; ++w)
+      if (sm_m[w0 + w][r] != -INFINITY) Z += sm_z[w0 + w][r] * fast_exp2(sm_m[w0 + w][r] - M);
+    *reinterpret_cast<f32x2*>(p.stats + ((int64_t)r * p.ntiles + stile) * 2) = f32x2{M, Z};
+  }
+}
+
 template <int RT, int CT, int WR, int NA, int DEPTH, int WPE>
 static hipError_t launch_lm_nrt(const LmParams& q, hipStream_t s) {
   // grid: tiles of 8 vocabulary tiles (one per XCD) x row groups of 32 WR RT rows, row groups
@@ -367,6 +571,14 @@ hipError_t launch_projection(const LmParams& p, hipStream_t s) {
   if (need <= 1) return launch_lm_nrt<1, 2, 1, 2, 4, 2>(p, s);
   if (need <= 2) return launch_lm_nrt<2, 2, 1, 2, 4, 2>(p, s);
   if (need <= 4) return launch_lm_nrt<4, 2, 1, 2, 4, 1>(p, s);
+  if (need >= 6 && need <= 10 && p.ksplit == 1) {
+    // every row in one workgroup per 256-column tile (lm_head_wide_kernel)
+    LmParams q = p;
+    q.mgroups = 1;
+    const int wgcols = (p.V + 255) / 256;
+    hipLaunchKernelGGL(lm_head_wide_kernel, dim3((unsigned)((wgcols + 7) / 8 * 8)), dim3(512), 0, s, q);
+    return hipGetLastError();
+  }
   if (group_rows(p.M) == 192) return launch_lm_nrt<6, 2, 1, 2, 4, 1>(p, s);
   return launch_lm_nrt<5, 2, 1, 2, 4, 1>(p, s);
 }
