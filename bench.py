@@ -457,6 +457,20 @@ def bench_lm_head(args):
     a_own = step.accepted_len.cpu().numpy().copy()
     us_acc_stats = timed(run_fused, args.steps, args.warmup)
     a_fused = step.accepted_len.cpu().numpy()
+    # the LM head also gathering the logits at the drafts, and acceptance from those
+    tg = torch.empty(T, dtype=torch.float32, device="cuda")
+    dg = torch.empty(len(rows_d), dtype=torch.float32, device="cuda")
+    cols = torch.empty(T, dtype=torch.int32, device="cuda")
+    sx.spexis_verify_gather_columns(step.qsl, ids, cols)
+    us_lm_gather = timed(lambda: sx.spexis_lm_head_gather(h, w, stats, cols, tg, logits=logits, temperature=temp),
+                         args.steps, args.warmup)
+    sx.spexis_lm_head_gather(hd, w, dstats, ids, dg, logits=dlogits, temperature=temp)
+    run_gathered = lambda: sx.spexis_accept_with_stats(step.qsl, logits, dlogits, stats, dstats, ids, acc.u_accept,
+                                                       acc.u_sample, batch.max_k, step.accepted_len,
+                                                       step.out_tokens, step.row_status, step.acc_ws,
+                                                       temperature=temp, target_gathered=tg, draft_gathered=dg)
+    us_acc_gathered = timed(run_gathered, args.steps, args.warmup)
+    assert np.array_equal(step.accepted_len.cpu().numpy(), a_fused)
     log(f"[lm_head] accepted mean {a_own.mean():.3f} (own statistics) / {a_fused.mean():.3f} (fused); "
         f"decisions differ on {int((a_own != a_fused).sum())} of {batch.B} sequences")
     wbytes, hbytes, lbytes, sbytes = V * d * 2, T * d * 2, T * V * 4, T * tiles * 8
@@ -471,11 +485,13 @@ def bench_lm_head(args):
         "mfma": {"achieved": round(tfl, 1), "peak": MFMA_BF16_TFLOPS, "unit": "TFLOP/s",
                  "frac": round(tfl / MFMA_BF16_TFLOPS, 4), "flops": flops},
         "accept_us": round(us_acc, 2), "accept_with_stats_us": round(us_acc_stats, 2),
+        "us_with_gathers": round(us_lm_gather, 2), "accept_with_stats_gathered_us": round(us_acc_gathered, 2),
         "dtype": "bf16", "data": "synthetic",
     }
     log(f"[lm_head] {T}x{d} @ {V}x{d}: {us_lm:.1f} us ({us_lm_stats:.1f} us without logits) -> {gbs:.0f} GB/s "
         f"({gbs / HBM_PEAK_GBS:.1%}), {tfl:.0f} TFLOP/s ({tfl / MFMA_BF16_TFLOPS:.1%}); accept {us_acc:.1f} us, "
-        f"with given statistics {us_acc_stats:.1f} us")
+        f"with given statistics {us_acc_stats:.1f} us; with the gathers fused: LM head {us_lm_gather:.1f} us, "
+        f"accept {us_acc_gathered:.1f} us")
     print(json.dumps(line), flush=True)
 
 

@@ -12,6 +12,8 @@
  *   spexis_verify_attention  causal grouped-query attention of those rows over the cache
  *   spexis_accept            ratio tests, residual / bonus sampling, outputs
  *   spexis_lm_head           logits = h W^T with fused softmax statistics (next to accept)
+ *   spexis_lm_head_gather    the same, also gathering each row's logit at a given column
+ *   spexis_verify_gather_columns  those columns for the target rows: the drafts they verify
  *   spexis_accept_with_stats acceptance from logits whose statistics are known
  *   spexis_accept_noalloc    spexis_accept in a static scratch array (callers that cannot allocate)
  *   spexis_select_drafts     selective speculation: drop the least confident drafts first
@@ -270,6 +272,32 @@ int spexis_lm_head(const void* hidden, const void* weight, int32_t rows, int32_t
                    int32_t hidden_dim, float temperature, float* logits, float* stats,
                    void* stream);
 
+/*
+ * spexis_lm_head_gather -- spexis_lm_head that also gathers, in its epilogue, the logit each row
+ * contributes to an acceptance test: the target and draft logits at the drafted token x_i (the
+ * gathers at x_i fused into the LM head of the verifying stage, Implementation; the tests of
+ * [sd], Related Work).  Arguments as spexis_lm_head (stats must not be NULL), plus
+ *   gather_cols  [rows] int32: the column row m gathers, or -1 (any value outside [0, vocab)
+ *                gathers nothing).  For draft rows these are the draft ids themselves; for target
+ *                rows spexis_verify_gather_columns builds them.
+ *   gathered     [rows] fp32 output: gathered[m] = logits[m][gather_cols[m]], the same fp32 value
+ *                the logits output holds; rows that gather nothing are not written
+ * Errors: as spexis_lm_head; INVALID_ARGUMENT for a NULL gather_cols or gathered.
+ */
+int spexis_lm_head_gather(const void* hidden, const void* weight, int32_t rows, int32_t vocab,
+                          int32_t hidden_dim, float temperature, float* logits, float* stats,
+                          const int32_t* gather_cols, float* gathered, void* stream);
+
+/*
+ * spexis_verify_gather_columns -- the target rows' gather columns of a verification batch: row
+ * qsl[b]+i verifies draft x_i = draft_ids[qsl[b]-b+i] (i < k_b) and gathers at it; each
+ * sequence's last row (its bonus position) gets -1.
+ *   total_tokens  host: T = qsl[B];  draft_ids [T-B] int32;  cols [T] int32 output
+ * Errors: INVALID_ARGUMENT (bad sizes, NULL pointers), HIP.
+ */
+int spexis_verify_gather_columns(int32_t num_seqs, int32_t total_tokens, const int32_t* query_start_loc,
+                                 const int32_t* draft_ids, int32_t* cols, void* stream);
+
 /* Column tiles per row of spexis_lm_head's statistics: ceil(vocab / 128). */
 int32_t spexis_lm_head_tiles(int32_t vocab);
 
@@ -284,7 +312,10 @@ size_t spexis_lm_head_stats_size(int32_t rows, int32_t vocab);
  *   target_stats  [T][stats_tiles][2] fp32, draft_stats [T-B][stats_tiles][2] fp32: for
  *                 every row, (max y*c, sum 2^(y*c - max)) over each of stats_tiles disjoint
  *                 column ranges that together cover the row, c = log2(e) / temperature
- * Errors: as spexis_accept.
+ *   target_gathered, draft_gathered  both NULL, or [T] and [T-B] fp32: the logits at the drafts,
+ *                 target row qsl[b]+i and draft row qsl[b]-b+i at x_i (i < k_b), as
+ *                 spexis_lm_head_gather writes them; then the tests read no logit row
+ * Errors: as spexis_accept; INVALID_ARGUMENT if only one gathered array is given.
  */
 int spexis_accept_with_stats(int32_t num_seqs, int32_t vocab, int32_t max_k, float temperature,
                              int32_t total_tokens, const int32_t* query_start_loc,
@@ -292,6 +323,7 @@ int spexis_accept_with_stats(int32_t num_seqs, int32_t vocab, int32_t max_k, flo
                              const float* target_stats, const float* draft_stats,
                              int32_t stats_tiles, const int32_t* draft_ids,
                              const float* u_accept, const float* u_sample,
+                             const float* target_gathered, const float* draft_gathered,
                              int32_t* accepted_len, int32_t* out_tokens, int32_t* row_status,
                              int32_t* seq_lens_inout, void* workspace, size_t workspace_bytes,
                              void* stream);

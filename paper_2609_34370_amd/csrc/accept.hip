@@ -468,8 +468,13 @@ __device__ __forceinline__ void gather_test(const AcceptParams& p, int b, const 
   const int x = p.ids[g.d0 + pos];
   const bool ok = x >= 0 && x < p.V;
   f32x4 t;
-  t[0] = ok ? p.target[(int64_t)(g.t0 + pos) * p.V + x] : 0.f;
-  t[1] = ok ? p.draft[(int64_t)(g.d0 + pos) * p.V + x] : 0.f;
+  if (p.tg_given) {   // gathered by the LM head (the same fp32 values)
+    t[0] = ok ? p.tg_given[g.t0 + pos] : 0.f;
+    t[1] = ok ? p.dg_given[g.d0 + pos] : 0.f;
+  } else {
+    t[0] = ok ? p.target[(int64_t)(g.t0 + pos) * p.V + x] : 0.f;
+    t[1] = ok ? p.draft[(int64_t)(g.d0 + pos) * p.V + x] : 0.f;
+  }
   t[2] = p.u_accept[g.d0 + pos];
   t[3] = ok ? 1.f : 0.f;
   *reinterpret_cast<f32x4*>(p.tin + ((int64_t)b * p.max_k + pos) * 4) = t;
@@ -989,6 +994,31 @@ static hipError_t launch_round(const AcceptParams& p, int r, int lo, int hi, int
   if (e != hipSuccess) return e;
   const unsigned gs = r == 0 || items < (unsigned)kRoundGrid ? items : (unsigned)kRoundGrid;
   hipLaunchKernelGGL(accept_stream_kernel, dim3(gs), dim3(kThreads), 0, s, p, r);
+  return hipGetLastError();
+}
+
+// The target rows' gather columns for the LM head: row qsl[b]+i verifies draft x_i of sequence b
+// (i < k_b) and gathers at it; the sequence's last row (its bonus position) gathers nothing.
+// Thread (b, i) takes rows i, i + 33, ... of sequence b (one row each when k_b <= 32).  Indices
+// are clamped into the buffers.
+__global__ __launch_bounds__(kThreads) void gather_columns_kernel(const int32_t* qsl, const int32_t* ids, int B, int T,
+                                                                  int32_t* cols) {
+  constexpr int kPer = kAcceptMaxK + 1;
+  const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (idx >= (int64_t)B * kPer) return;
+  const int b = (int)(idx / kPer), i = (int)(idx % kPer);
+  const int a0 = clampi(qsl[b], 0, T), a1 = clampi(qsl[b + 1], a0, T);
+  const int n = a1 - a0;
+  for (int j = i; j < n; j += kPer) {
+    const int d = a0 - b + j;   // the draft this row verifies
+    cols[a0 + j] = j < n - 1 && d >= 0 && d < T - B ? ids[d] : -1;
+  }
+}
+
+hipError_t launch_gather_columns(const int32_t* qsl, const int32_t* ids, int B, int T, int32_t* cols, hipStream_t s) {
+  const int64_t n = (int64_t)B * (kAcceptMaxK + 1);
+  hipLaunchKernelGGL(gather_columns_kernel, dim3((unsigned)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, s,
+                     qsl, ids, B, T, cols);
   return hipGetLastError();
 }
 

@@ -279,7 +279,8 @@ int accept_impl(const char* who, int32_t kind, int32_t num_seqs, int32_t vocab, 
                 const float* target_stats, const float* draft_stats, int32_t stats_parts,
                 const int32_t* draft_ids, const float* u_accept, const float* u_sample, int32_t* accepted_len,
                 int32_t* out_tokens, int32_t* row_status, int32_t* seq_lens_inout, void* workspace,
-                size_t workspace_bytes, void* stream, float* tok_prob = nullptr, bool static_scratch = false) {
+                size_t workspace_bytes, void* stream, float* tok_prob = nullptr, bool static_scratch = false,
+                const float* target_gathered = nullptr, const float* draft_gathered = nullptr) {
   // query_start_loc == nullptr (internal callers only): every sequence is one row, no drafts
   if (kind != SPEXIS_INPUT_PROBS && kind != SPEXIS_INPUT_LOGITS)
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: kind %d is neither PROBS nor LOGITS", who, kind);
@@ -345,6 +346,8 @@ int accept_impl(const char* who, int32_t kind, int32_t num_seqs, int32_t vocab, 
   p.ext_tstats = target_stats;
   p.ext_dstats = draft_stats;
   p.ext_parts = stats_parts;
+  p.tg_given = target_gathered;
+  p.dg_given = draft_gathered;
   return hip_result(spexis::launch_accept(p, (hipStream_t)stream), who);
 }
 
@@ -378,12 +381,14 @@ int spexis_accept_with_stats(int32_t num_seqs, int32_t vocab, int32_t max_k, flo
                              int32_t total_tokens, const int32_t* query_start_loc, const float* target_logits,
                              const float* draft_logits, const float* target_stats, const float* draft_stats,
                              int32_t stats_tiles, const int32_t* draft_ids, const float* u_accept,
-                             const float* u_sample, int32_t* accepted_len, int32_t* out_tokens,
-                             int32_t* row_status, int32_t* seq_lens_inout, void* workspace, size_t workspace_bytes,
-                             void* stream) {
+                             const float* u_sample, const float* target_gathered, const float* draft_gathered,
+                             int32_t* accepted_len, int32_t* out_tokens, int32_t* row_status,
+                             int32_t* seq_lens_inout, void* workspace, size_t workspace_bytes, void* stream) {
   const bool has_drafts = total_tokens > num_seqs;
   if (num_seqs > 0 && (!target_stats || (has_drafts && !draft_stats)))
     return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept_with_stats: null statistics");
+  if ((target_gathered == nullptr) != (draft_gathered == nullptr))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept_with_stats: give both gathered arrays or neither");
   if (stats_tiles <= 0) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_accept_with_stats: stats_tiles <= 0");
   // the per-row reductions of the statistics live in the workspace's statistics area
   if (num_seqs > 0 && max_k >= 0 && total_tokens > (int64_t)num_seqs * (max_k + 1))
@@ -392,7 +397,8 @@ int spexis_accept_with_stats(int32_t num_seqs, int32_t vocab, int32_t max_k, flo
   return accept_impl("spexis_accept_with_stats", SPEXIS_INPUT_LOGITS, num_seqs, vocab, max_k, temperature,
                      total_tokens, query_start_loc, target_logits, draft_logits, target_stats,
                      has_drafts ? draft_stats : target_stats, stats_tiles, draft_ids, u_accept, u_sample,
-                     accepted_len, out_tokens, row_status, seq_lens_inout, workspace, workspace_bytes, stream);
+                     accepted_len, out_tokens, row_status, seq_lens_inout, workspace, workspace_bytes, stream,
+                     nullptr, false, has_drafts ? target_gathered : nullptr, has_drafts ? draft_gathered : nullptr);
 }
 
 size_t spexis_sample_workspace_size(int32_t rows, int32_t vocab) {
@@ -600,19 +606,25 @@ size_t spexis_lm_head_stats_size(int32_t rows, int32_t vocab) {
   return (size_t)rows * spexis_lm_head_tiles(vocab) * 2 * sizeof(float);
 }
 
-int spexis_lm_head(const void* hidden, const void* weight, int32_t rows, int32_t vocab, int32_t hidden_dim,
-                   float temperature, float* logits, float* stats, void* stream) {
-  if (rows < 0 || vocab <= 0 || hidden_dim <= 0)
-    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lm_head: bad size");
+}  // extern "C"
+
+namespace {
+
+int lm_head_impl(const char* who, const void* hidden, const void* weight, int32_t rows, int32_t vocab,
+                 int32_t hidden_dim, float temperature, float* logits, float* stats, const int32_t* gather_cols,
+                 float* gathered, void* stream) {
+  if (rows < 0 || vocab <= 0 || hidden_dim <= 0) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: bad size", who);
   if (!(temperature > 0.f) || !std::isfinite(temperature))
-    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lm_head: temperature must be finite and > 0");
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: temperature must be finite and > 0", who);
   if (hidden_dim % 256 != 0)
-    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_lm_head: hidden_dim %d is not a multiple of 256", hidden_dim);
+    return fail(SPEXIS_ERR_UNSUPPORTED, "%s: hidden_dim %d is not a multiple of 256", who, hidden_dim);
   if (rows == 0) return ok();
-  if (!hidden || !weight || !stats) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lm_head: null pointer");
+  if (!hidden || !weight || !stats) return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: null pointer", who);
+  if ((gather_cols == nullptr) != (gathered == nullptr))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "%s: give gather_cols and gathered together", who);
   const int64_t tiles = spexis_lm_head_tiles(vocab);
   if (spexis::projection_workgroups(rows, vocab) + 8 * rows >= (1ll << 31) || (int64_t)rows * vocab >= (1ll << 40))
-    return fail(SPEXIS_ERR_UNSUPPORTED, "spexis_lm_head: problem too large");
+    return fail(SPEXIS_ERR_UNSUPPORTED, "%s: problem too large", who);
   spexis::LmParams p{};
   p.h = hidden;
   p.w = weight;
@@ -624,7 +636,40 @@ int spexis_lm_head(const void* hidden, const void* weight, int32_t rows, int32_t
   p.ntiles = (int)tiles;
   p.ksplit = 1;
   p.c = (float)(1.4426950408889634 / (double)temperature);
-  return hip_result(spexis::launch_projection(p, (hipStream_t)stream), "spexis_lm_head");
+  p.gcols = gather_cols;
+  p.gout = gathered;
+  return hip_result(spexis::launch_projection(p, (hipStream_t)stream), who);
+}
+
+}  // namespace
+
+extern "C" {
+
+int spexis_lm_head(const void* hidden, const void* weight, int32_t rows, int32_t vocab, int32_t hidden_dim,
+                   float temperature, float* logits, float* stats, void* stream) {
+  return lm_head_impl("spexis_lm_head", hidden, weight, rows, vocab, hidden_dim, temperature, logits, stats,
+                      nullptr, nullptr, stream);
+}
+
+int spexis_lm_head_gather(const void* hidden, const void* weight, int32_t rows, int32_t vocab, int32_t hidden_dim,
+                          float temperature, float* logits, float* stats, const int32_t* gather_cols,
+                          float* gathered, void* stream) {
+  if (rows > 0 && (!gather_cols || !gathered))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_lm_head_gather: null gather_cols or gathered");
+  return lm_head_impl("spexis_lm_head_gather", hidden, weight, rows, vocab, hidden_dim, temperature, logits, stats,
+                      gather_cols, gathered, stream);
+}
+
+int spexis_verify_gather_columns(int32_t num_seqs, int32_t total_tokens, const int32_t* query_start_loc,
+                                 const int32_t* draft_ids, int32_t* cols, void* stream) {
+  if (num_seqs < 0 || total_tokens < num_seqs)
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_gather_columns: bad size");
+  if (num_seqs == 0) return ok();
+  if (!query_start_loc || !cols || (total_tokens > num_seqs && !draft_ids))
+    return fail(SPEXIS_ERR_INVALID_ARGUMENT, "spexis_verify_gather_columns: null pointer");
+  return hip_result(spexis::launch_gather_columns(query_start_loc, draft_ids, num_seqs, total_tokens, cols,
+                                                  (hipStream_t)stream),
+                    "spexis_verify_gather_columns");
 }
 
 }  // extern "C"

@@ -62,6 +62,10 @@ struct LmParams {
   int M, V, d, ntiles, mgroups;   // ntiles: 128-column statistics tiles; mgroups: set by the launcher
   int ksplit;            // K split over workgroups (grid y); each takes d / ksplit
   float c;               // log2(e) / temperature
+  // Fused gathers (gout null: none; needs stats): gout[m] = logits[m][gcols[m]] for every row
+  // whose gcols[m] lies in [0, V).
+  const int32_t* gcols;
+  float* gout;
 };
 
 constexpr int kLmCols = 128;   // columns of a statistics tile, and of a narrow projection's workgroup
@@ -144,6 +148,8 @@ struct AcceptParams {
                          // by write_invalid)
   int32_t* strec;        // [B][12] a round's job per list entry (logits mode): b, t0, d0, k | job,
                          // position or next round's lo, next round's hi, shift | Mp, Rp, Mq, Rq
+  const float* tg_given; // with given statistics, optionally the logits at the drafts: target row
+  const float* dg_given; // t0+i at x_i ([T]) and draft row d0+i at x_i ([T-B]); null: read them
 };
 
 constexpr int kAcceptMaxK = 32;      // drafts per sequence the boundary takes (below one wave's lanes)
@@ -166,5 +172,6 @@ hipError_t launch_projection(const LmParams& p, hipStream_t s);
 int64_t projection_workgroups(int64_t M, int64_t N);
 hipError_t launch_softmax(const float* logits, float* probs, int64_t rows, int V, float c, hipStream_t s);
 hipError_t launch_accept(const AcceptParams& p, hipStream_t s);
+hipError_t launch_gather_columns(const int32_t* qsl, const int32_t* ids, int B, int T, int32_t* cols, hipStream_t s);
 
 }  // namespace spexis

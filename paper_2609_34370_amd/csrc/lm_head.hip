@@ -39,6 +39,7 @@ __device__ __forceinline__ uint16_t bf16_rne(float f) {
 
 __device__ __forceinline__ float bf16_float(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
+
 // W rows are read once: non-temporal loads keep them from evicting h out of L2.
 template <bool kStream>
 __device__ __forceinline__ u32x4 ldw(const uint16_t* p) {
@@ -212,6 +213,14 @@ void lm_head_kernel(LmParams p) {
   // stores keep them from evicting the h and W lines the other workgroups still read through L2
   // (measured at 320 x 4096 @ 128256: 469 against 480 us; at 4608 x 3584 @ 152064: 5332 against
   // 5684 us).
+  // the gather columns of the rows lanes below 32 reduce in the statistics (loaded first: their
+  // latency passes under the logits stores)
+  int gcol[RT];
+#pragma unroll
+  for (int t = 0; t < RT; ++t) {
+    const int grow = 32 * (wr * RT + t) + lane;
+    gcol[t] = p.gout && p.stats && lane < 32 && grow < rows ? p.gcols[m0 + grow] : -1;
+  }
   if (p.logits) {
     float* out = p.logits + (int64_t)ks * p.M * p.V;
 #pragma unroll
@@ -257,16 +266,22 @@ void lm_head_kernel(LmParams p) {
 #pragma unroll
   for (int t = 0; t < RT; ++t) {
     float wm = -INFINITY, wz = 0.f;
+    const int grow = 32 * (wr * RT + t) + lane;
+    const int gc = gcol[t];
 #pragma unroll
     for (int c = 0; c < CT; ++c) {
       const bool live = out_col(c) < p.V;
 #pragma unroll
       for (int i = 0; i < 16; ++i)
-        tile[(8 * (i >> 2) + 4 * half + (i & 3)) * kTS + col] = live ? acc[t][c][i] * p.c : -INFINITY;
+        tile[(8 * (i >> 2) + 4 * half + (i & 3)) * kTS + col] = live ? acc[t][c][i] : -INFINITY;
       if (lane < 32) {
+        // x c rounded once, then x c - max: no contraction into one fused operation
+#pragma clang fp contract(off)
         f32x4 x[8];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) x[q] = *reinterpret_cast<const f32x4*>(tile + lane * kTS + 4 * q);
+        for (int q = 0; q < 8; ++q) x[q] = *reinterpret_cast<const f32x4*>(tile + lane * kTS + 4 * q) * p.c;
+        const int cb = out_col(c) - col;   // the tile's first column
+        if (gc >= cb && gc < cb + 32 && gc < p.V) p.gout[m0 + grow] = tile[lane * kTS + (gc - cb)];
         float mx = -INFINITY;
 #pragma unroll
         for (int q = 0; q < 8; ++q) mx = fmaxf(fmaxf(mx, fmaxf(x[q][0], x[q][1])), fmaxf(x[q][2], x[q][3]));
@@ -334,7 +349,7 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
   int nt, mg;
   tile_of(blockIdx.x, wgcols, 1, nt, mg);
   if (nt >= wgcols) return;
-  const int n0 = nt * kCols;
+  const int n0 = nt * kCols, m0 = 0;
   const int rows = min(kRows, p.M);
   const int nsteps = p.d / kLmK;
   const int wtiles = (p.V + 31) / 32;
@@ -418,6 +433,14 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
   // + 4 (l / 32) + i % 4, column 32 (CT wc + c) + l % 32)
   auto out_row = [&](int t, int i) { return 32 * (wr * RT + t) + 8 * (i >> 2) + 4 * half + (i & 3); };
   auto out_col = [&](int c) { return n0 + 32 * (CT * wc + c) + col; };
+  // the gather columns of the rows lanes below 32 reduce in the statistics (loaded first: their
+  // latency passes under the logits stores)
+  int gcol[RT];
+#pragma unroll
+  for (int t = 0; t < RT; ++t) {
+    const int grow = 32 * (wr * RT + t) + lane;
+    gcol[t] = p.gout && p.stats && lane < 32 && grow < rows ? p.gcols[m0 + grow] : -1;
+  }
   if (p.logits) {
 #pragma unroll
     for (int c = 0; c < CT; ++c) {
@@ -461,16 +484,22 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
 #pragma unroll
   for (int t = 0; t < RT; ++t) {
     float wm = -INFINITY, wz = 0.f;
+    const int grow = 32 * (wr * RT + t) + lane;
+    const int gc = gcol[t];
 #pragma unroll
     for (int c = 0; c < CT; ++c) {
       const bool live = out_col(c) < p.V;
 #pragma unroll
       for (int i = 0; i < 16; ++i)
-        tile[(8 * (i >> 2) + 4 * half + (i & 3)) * kTS + col] = live ? acc[t][c][i] * p.c : -INFINITY;
+        tile[(8 * (i >> 2) + 4 * half + (i & 3)) * kTS + col] = live ? acc[t][c][i] : -INFINITY;
       if (lane < 32) {
+        // x c rounded once, then x c - max: no contraction into one fused operation
+#pragma clang fp contract(off)
         f32x4 x[8];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) x[q] = *reinterpret_cast<const f32x4*>(tile + lane * kTS + 4 * q);
+        for (int q = 0; q < 8; ++q) x[q] = *reinterpret_cast<const f32x4*>(tile + lane * kTS + 4 * q) * p.c;
+        const int cb = out_col(c) - col;   // the tile's first column
+        if (gc >= cb && gc < cb + 32 && gc < p.V) p.gout[m0 + grow] = tile[lane * kTS + (gc - cb)];
         float mx = -INFINITY;
 #pragma unroll
         for (int q = 0; q < 8; ++q) mx = fmaxf(fmaxf(mx, fmaxf(x[q][0], x[q][1])), fmaxf(x[q][2], x[q][3]));

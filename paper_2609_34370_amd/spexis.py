@@ -74,8 +74,12 @@ def lib():
     L.spexis_lm_head.restype = ctypes.c_int
     L.spexis_lm_head_tiles.argtypes, L.spexis_lm_head_tiles.restype = [i32], i32
     L.spexis_lm_head_stats_size.argtypes, L.spexis_lm_head_stats_size.restype = [i32, i32], sz
-    L.spexis_accept_with_stats.argtypes = [i32, i32, i32, f32, i32, P, P, P, P, P, i32, P, P, P, P, P, P, P, P, sz,
-                                           P]
+    L.spexis_accept_with_stats.argtypes = [i32, i32, i32, f32, i32, P, P, P, P, P, i32, P, P, P, P, P, P, P, P, P,
+                                           P, sz, P]
+    L.spexis_lm_head_gather.argtypes = [P, P, i32, i32, i32, f32, P, P, P, P, P]
+    L.spexis_lm_head_gather.restype = ctypes.c_int
+    L.spexis_verify_gather_columns.argtypes = [i32, i32, P, P, P, P]
+    L.spexis_verify_gather_columns.restype = ctypes.c_int
     L.spexis_accept_with_stats.restype = ctypes.c_int
     L.spexis_select_drafts.argtypes = [i32, i32, P, P, f32, P, P, P, P]
     L.spexis_select_drafts.restype = ctypes.c_int
@@ -217,9 +221,35 @@ def spexis_lm_head(hidden, weight, stats, logits=None, temperature=1.0, vocab=No
                                 _ptr(stats, torch.float32), _stream(stream)))
 
 
+def spexis_lm_head_gather(hidden, weight, stats, gather_cols, gathered, logits=None, temperature=1.0, vocab=None,
+                          stream=None) -> None:
+    """spexis_lm_head that also writes gathered[m] = logits[m][gather_cols[m]] (for columns in
+    [0, V))."""
+    rows, hidden_dim = hidden.shape
+    if vocab is None:
+        vocab = logits.shape[1] if logits is not None else None
+    if vocab is None:
+        raise ValueError("vocab is needed when logits is None")
+    assert weight.numel() * 2 == spexis_packed_weight_size(vocab, hidden_dim), "weight must be packed"
+    _check(lib().spexis_lm_head_gather(
+        _ptr(hidden, torch.bfloat16), _ptr(weight, torch.bfloat16), rows, vocab, hidden_dim,
+        ctypes.c_float(temperature), _ptr(logits, torch.float32), _ptr(stats, torch.float32),
+        _ptr(gather_cols, torch.int32), _ptr(gathered, torch.float32), _stream(stream)))
+
+
+def spexis_verify_gather_columns(query_start_loc, draft_ids, cols, stream=None) -> None:
+    """cols[qsl[b]+i] = the draft id row qsl[b]+i verifies (i < k_b), -1 for bonus rows."""
+    num_seqs = query_start_loc.shape[0] - 1
+    total = cols.shape[0]
+    _check(lib().spexis_verify_gather_columns(num_seqs, total, _ptr(query_start_loc, torch.int32),
+                                              _ptr(draft_ids, torch.int32) if draft_ids.numel() else None,
+                                              _ptr(cols, torch.int32), _stream(stream)))
+
+
 def spexis_accept_with_stats(query_start_loc, target_logits, draft_logits, target_stats, draft_stats, draft_ids,
                              u_accept, u_sample, max_k, accepted_len, out_tokens, row_status, workspace,
-                             temperature=1.0, seq_lens_inout=None, stream=None) -> None:
+                             temperature=1.0, seq_lens_inout=None, target_gathered=None, draft_gathered=None,
+                             stream=None) -> None:
     num_seqs = query_start_loc.shape[0] - 1
     total_tokens, vocab = target_logits.shape
     tiles = target_stats.shape[1]
@@ -230,7 +260,8 @@ def spexis_accept_with_stats(query_start_loc, target_logits, draft_logits, targe
         _ptr(target_logits, torch.float32), _ptr(draft_logits, torch.float32) if nd > 0 else None,
         _ptr(target_stats, torch.float32), _ptr(draft_stats, torch.float32) if nd > 0 else None, tiles,
         _ptr(draft_ids, torch.int32) if nd > 0 else None, _ptr(u_accept, torch.float32) if nd > 0 else None,
-        _ptr(u_sample, torch.float32), _ptr(accepted_len, torch.int32), _ptr(out_tokens, torch.int32),
+        _ptr(u_sample, torch.float32), _ptr(target_gathered, torch.float32), _ptr(draft_gathered, torch.float32),
+        _ptr(accepted_len, torch.int32), _ptr(out_tokens, torch.int32),
         _ptr(row_status, torch.int32), _ptr(seq_lens_inout, torch.int32), _ptr(workspace), ws_bytes,
         _stream(stream)))
 

@@ -141,6 +141,26 @@ def test_accept_noalloc_validation():
 
 
 @no_gpu
+def test_lm_head_gather_validation():
+    L = sx.lib()
+    # a NULL gathered output or column array, and a hidden size the projection does not take
+    assert L.spexis_lm_head_gather(FAKE, FAKE, 8, 1000, 256, ctypes.c_float(1.0), None, FAKE, FAKE, None,
+                                   None) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert L.spexis_lm_head_gather(FAKE, FAKE, 8, 1000, 256, ctypes.c_float(1.0), None, FAKE, None, FAKE,
+                                   None) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert L.spexis_lm_head_gather(FAKE, FAKE, 8, 1000, 300, ctypes.c_float(1.0), None, FAKE, FAKE, FAKE,
+                                   None) == sx.SPEXIS_ERR_UNSUPPORTED
+    assert L.spexis_verify_gather_columns(3, 2, FAKE, FAKE, FAKE, None) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert L.spexis_verify_gather_columns(3, 7, None, FAKE, FAKE, None) == sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert L.spexis_verify_gather_columns(0, 0, None, None, None, None) == sx.SPEXIS_OK
+    # acceptance takes both gathered arrays or neither
+    a = [2, 100, 2, ctypes.c_float(1.0), 6, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE, FAKE]
+    assert L.spexis_accept_with_stats(*a, FAKE, None, FAKE, FAKE, FAKE, None, FAKE, 1 << 20, None) == \
+        sx.SPEXIS_ERR_INVALID_ARGUMENT
+    assert b"gathered" in L.spexis_last_error()
+
+
+@no_gpu
 def test_softmax_validation():
     L = sx.lib()
     assert L.spexis_softmax_rows(FAKE, FAKE, 4, 10, ctypes.c_float(0.0), None) == sx.SPEXIS_ERR_INVALID_ARGUMENT

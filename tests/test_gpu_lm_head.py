@@ -242,3 +242,79 @@ def test_accept_with_fused_statistics_flags_bad_draft_ids():
         np.testing.assert_array_equal(t1[keep], t0[keep])
         np.testing.assert_array_equal(s1[keep], 0)
 
+
+
+@pytest.mark.parametrize("B,K,d", [(20, 5, 256), (64, 4, 512), (90, 4, 256)])
+def test_lm_head_gathers_the_draft_logits(B, K, d):
+    # target rows gather at the draft of the position they verify (spexis_verify_gather_columns), draft
+    # rows at their own draft; the gathered values are the logits output bit for bit, rows with no
+    # gather (bonus rows) or an id outside [0, V) are left alone, and acceptance from the fused
+    # statistics gives the same outputs with or without them.  B sequences of 0..K drafts: about
+    # 70, 290 and 400 target rows, so all three workgroup shapes of the projection run.
+    rng = np.random.default_rng(B + d)
+    V, T_ = 3000, 0.8
+    k = rng.integers(0, K + 1, B)
+    qsl = np.concatenate([[0], np.cumsum(k + 1)]).astype(np.int32)
+    Tt, Td = int(qsl[-1]), int(qsl[-1]) - B
+    w, _ = bf16_pair((V, d), 31, 0.1)
+    ht, _ = bf16_pair((Tt, d), 32, 1.0)
+    hd, _ = bf16_pair((Td, d), 33, 1.0)
+    ids = rng.integers(0, V, Td).astype(np.int32)
+    if Td > 2:
+        ids[1] = V + 5                       # out of range: gathered nowhere
+    tiles = sx.spexis_lm_head_tiles(V)
+    dev = lambda x: torch.as_tensor(x, device="cuda")
+    wp = sx.spexis_pack_weight(w.cuda())
+    tl = torch.empty((Tt, V), dtype=torch.float32, device="cuda")
+    dl = torch.empty((Td, V), dtype=torch.float32, device="cuda")
+    ts = torch.empty((Tt, tiles, 2), dtype=torch.float32, device="cuda")
+    ds = torch.empty((Td, tiles, 2), dtype=torch.float32, device="cuda")
+    tg = torch.full((Tt,), float("nan"), device="cuda")
+    dg = torch.full((Td,), float("nan"), device="cuda")
+    cols = torch.full((Tt,), -9, dtype=torch.int32, device="cuda")
+    sx.spexis_verify_gather_columns(dev(qsl), dev(ids), cols)
+    torch.cuda.synchronize()
+    expect = np.concatenate([np.append(ids[qsl[b] - b:qsl[b] - b + k[b]], -1) for b in range(B)])
+    np.testing.assert_array_equal(cols.cpu().numpy(), expect)
+    sx.spexis_lm_head_gather(ht.cuda(), wp, ts, cols, tg, logits=tl, temperature=T_)
+    sx.spexis_lm_head_gather(hd.cuda(), wp, ds, dev(ids), dg, logits=dl, temperature=T_)
+    ts2, ds2 = torch.empty_like(ts), torch.empty_like(ds)
+    sx.spexis_lm_head(ht.cuda(), wp, ts2, temperature=T_, vocab=V)
+    sx.spexis_lm_head(hd.cuda(), wp, ds2, temperature=T_, vocab=V)
+    torch.cuda.synchronize()
+    # the gathering pass writes the same statistics as the plain one
+    assert torch.equal(ts, ts2) and torch.equal(ds, ds2)
+    tln, dln, tgn, dgn = tl.cpu().numpy(), dl.cpu().numpy(), tg.cpu().numpy(), dg.cpu().numpy()
+    for m in range(Td):
+        x = ids[m]
+        if 0 <= x < V:
+            assert dgn[m].view(np.uint32) == dln[m, x].view(np.uint32), m
+        else:
+            assert np.isnan(dgn[m])
+    for b in range(B):
+        for i in range(k[b] + 1):
+            m = qsl[b] + i
+            x = ids[qsl[b] - b + i] if i < k[b] else -1
+            if 0 <= x < V:
+                assert tgn[m].view(np.uint32) == tln[m, x].view(np.uint32), (b, i)
+            else:
+                assert np.isnan(tgn[m]), (b, i)
+    say(f"[lm_head gather] B={B} rows {Tt}/{Td}: gathered values equal the logits")
+    ua = dev(rng.random(Td, dtype=np.float32))
+    us = dev(rng.random(B, dtype=np.float32))
+    ws = torch.empty(sx.spexis_accept_workspace_size(B, V, K), dtype=torch.uint8, device="cuda")
+    outs = []
+    for gathered in ((None, None), (tg, dg)):
+        acc = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+        tok = torch.full((B, K + 1), -7, dtype=torch.int32, device="cuda")
+        st = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+        sx.spexis_accept_with_stats(dev(qsl), tl, dl, ts, ds, dev(ids), ua, us, K, acc, tok, st, ws, temperature=T_,
+                                    target_gathered=gathered[0], draft_gathered=gathered[1])
+        torch.cuda.synchronize()
+        outs.append((acc.clone(), tok.clone(), st.clone()))
+    for a, b_ in zip(*outs):
+        assert torch.equal(a, b_)
+    if Td > 2:   # the sequence holding the out-of-range draft id reports it
+        d0 = qsl[:-1] - np.arange(B)
+        bad = [b for b in range(B) if d0[b] <= 1 < d0[b] + k[b]][0]
+        assert outs[1][2].cpu().numpy()[bad] == sx.SPEXIS_ROW_BAD_TOKEN
