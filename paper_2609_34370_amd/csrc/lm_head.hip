@@ -324,9 +324,9 @@ void lm_head_kernel(LmParams p) {
   }
 }
 
-// 129 to 320 rows of a wide projection (an LM head's vocabulary): one workgroup of eight waves
-// (two per SIMD) per 256-column tile takes every row, so each K-slice of W is read from HBM and
-// through L2 once, by one workgroup.  Both operands go through LDS: every K-step of 64 the
+// More than 160 rows of a wide projection (an LM head's vocabulary): one workgroup of eight waves
+// (two per SIMD) per (256-column tile, group of 320 rows), so that each K-slice of W crosses L2
+// once per 320 rows.  Both operands go through LDS: every K-step of 64 the
 // workgroup's threads copy h (320 rows, 40 KB) and W (eight packed 32-column tiles, 32 KB) into
 // one of two stages, loaded one step ahead into registers, and the waves read their fragments
 // from the stage.  Wave (wr, wc) of a 2 x 4 grid computes rows 160 wr .. +160 (five row tiles)
@@ -347,13 +347,13 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
   const int wr = wave / WC, wc = wave % WC;
   const int wgcols = (p.V + kCols - 1) / kCols;
   int nt, mg;
-  tile_of(blockIdx.x, wgcols, 1, nt, mg);
+  tile_of(blockIdx.x, wgcols, p.mgroups, nt, mg);
   if (nt >= wgcols) return;
-  const int n0 = nt * kCols, m0 = 0;
-  const int rows = min(kRows, p.M);
+  const int n0 = nt * kCols, m0 = mg * kRows;
+  const int rows = min(kRows, p.M - m0);
   const int nsteps = p.d / kLmK;
   const int wtiles = (p.V + 31) / 32;
-  const uint16_t* hbase = reinterpret_cast<const uint16_t*>(p.h);
+  const uint16_t* hbase = reinterpret_cast<const uint16_t*>(p.h) + (int64_t)m0 * p.d;
   const uint16_t* wbase = reinterpret_cast<const uint16_t*>(p.w);
 
   // stage x of h: row r, chunk kc (8 K values) at r * 8 + (kc ^ ((r >> 1) & 7)) (the 16 rows of
@@ -451,7 +451,7 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int r = out_row(t, i);
-          if (r < rows) __builtin_nontemporal_store(acc[t][c][i], p.logits + (int64_t)r * p.V + v);
+          if (r < rows) __builtin_nontemporal_store(acc[t][c][i], p.logits + (int64_t)(m0 + r) * p.V + v);
         }
     }
   }
@@ -468,7 +468,7 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
         for (int i = 0; i < 16; ++i) {
           const int r = out_row(t, i);
           if (r < rows) {
-            const int64_t at = (int64_t)r * p.V + v;
+            const int64_t at = (int64_t)(m0 + r) * p.V + v;
             y[at] = bf16_rne(res ? acc[t][c][i] + bf16_float(res[at]) : acc[t][c][i]);
           }
         }
@@ -538,7 +538,7 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
 #pragma unroll
     for (int w = 0; w < kWavesPerStat; ++w)
       if (sm_m[w0 + w][r] != -INFINITY) Z += sm_z[w0 + w][r] * fast_exp2(sm_m[w0 + w][r] - M);
-    *reinterpret_cast<f32x2*>(p.stats + ((int64_t)r * p.ntiles + stile) * 2) = f32x2{M, Z};
+    *reinterpret_cast<f32x2*>(p.stats + ((int64_t)(m0 + r) * p.ntiles + stile) * 2) = f32x2{M, Z};
   }
 }
 
@@ -562,6 +562,11 @@ static hipError_t launch_lm_nrt(const LmParams& q, hipStream_t s) {
 // than groups of 160 (five tiles), else 160.  The larger group makes about 10% fewer L2 requests
 // per output (measured 4.73 against 4.98 ms at 4608 x 3584 @ 152064); 320 rows keep two groups
 // of 160 rather than two of 192.
+// The eight-wave kernel takes 161 to 320 rows: one group.  Beyond, in groups of 320 rows, it was
+// slower than the four-wave groups of 192 (4608 x 3584 @ 152064: 5280 against 5100 us without
+// logits), whose waves keep more MFMAs per LDS fragment read.
+static bool wide_rows(int64_t M) { return M <= 320; }
+
 static int64_t group_rows(int64_t M) {
   const int64_t p160 = (M + 159) / 160 * 160, p192 = (M + 191) / 192 * 192;
   return p192 * 20 <= p160 * 21 ? 192 : 160;
@@ -577,6 +582,7 @@ int64_t projection_workgroups(int64_t M, int64_t N) {
   // beyond
   const int64_t cols = wide_columns(M, N) ? (N + 255) / 256 : (N + kLmCols - 1) / kLmCols;
   if (M <= 128) return cols;
+  if (M > 160 && wide_rows(M)) return cols * ((M + 319) / 320);
   return cols * ((M + group_rows(M) - 1) / group_rows(M));
 }
 
@@ -600,12 +606,12 @@ hipError_t launch_projection(const LmParams& p, hipStream_t s) {
   if (need <= 1) return launch_lm_nrt<1, 2, 1, 2, 4, 2>(p, s);
   if (need <= 2) return launch_lm_nrt<2, 2, 1, 2, 4, 2>(p, s);
   if (need <= 4) return launch_lm_nrt<4, 2, 1, 2, 4, 1>(p, s);
-  if (need >= 6 && need <= 10 && p.ksplit == 1) {
-    // every row in one workgroup per 256-column tile (lm_head_wide_kernel)
+  if (need >= 6 && p.ksplit == 1 && wide_rows(p.M)) {
+    // groups of 320 rows, one eight-wave workgroup per (256-column tile, group): lm_head_wide_kernel
     LmParams q = p;
-    q.mgroups = 1;
+    q.mgroups = (p.M + 319) / 320;
     const int wgcols = (p.V + 255) / 256;
-    hipLaunchKernelGGL(lm_head_wide_kernel, dim3((unsigned)((wgcols + 7) / 8 * 8)), dim3(512), 0, s, q);
+    hipLaunchKernelGGL(lm_head_wide_kernel, dim3((unsigned)((wgcols + 7) / 8 * 8 * q.mgroups)), dim3(512), 0, s, q);
     return hipGetLastError();
   }
   if (group_rows(p.M) == 192) return launch_lm_nrt<6, 2, 1, 2, 4, 1>(p, s);

@@ -122,7 +122,7 @@ def test_lm_head_large_row_count_sampled_rows():
     rows, V, d = 4608, 152064, 3584
     h, hb = bf16_pair((rows, d), 7, 1.0)
     w, wb = bf16_pair((V, d), 8, 0.02)
-    sel = [0, 319, 320, 2301, 4607]
+    sel = [0, 159, 160, 191, 192, 319, 320, 2301, 4479, 4480, 4607]
     say(f"[lm head] rows={rows} V={V} d={d} (rows {sel} checked)")
     check(h, hb, w, wb, 0.7, rows_idx=sel)
 
