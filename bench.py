@@ -133,16 +133,42 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def stream_peaks(torch, nbytes=4 << 30, reps=5):
-    """Measured HBM rates on this GPU: the read probe of libspexis_probe.so (plain coalesced
-    16-byte loads over a 4 GiB buffer, best grid and repetition) and torch's device copy (bytes
-    read plus bytes written per second)."""
+def _read_probe():
+    """spexis_probe_stream_read of libspexis_probe.so (plain coalesced 16-byte loads)."""
     import ctypes
     from paper_2609_34370_amd import build as _b
     probe = ctypes.CDLL(_b.PROBE_LIB_PATH)
     probe.spexis_probe_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
                                                ctypes.c_void_p]
     probe.spexis_probe_stream_read.restype = ctypes.c_int
+    return probe
+
+
+SETTLE_MS = 60.0
+
+
+def settle(torch, fn, ms=SETTLE_MS):
+    """Runs `fn` back to back for `ms` milliseconds before it is timed.  After input generation or
+    an idle spell this GPU takes some 40 ms of load to reach its clocks: the first 20 calls of a
+    compute-bound kernel ran up to 15% slower than later ones (an LM head at 320 x 4096 @ 128256:
+    431 us, then 400, 394, 379, 371, and 368-370 us from then on), while the verification step,
+    memory-bound, settled within its warmup and ran slower after a longer sustained load (phase
+    times 149 against 145 us of attention after 200 ms of load).  So the component timings settle
+    on their own call for this long, and the step bench keeps its W warmup steps only."""
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < ms * 1e-3:
+        for _ in range(4):
+            fn()
+        torch.cuda.synchronize()
+
+
+def stream_peaks(torch, nbytes=4 << 30, reps=5):
+    """Measured HBM rates on this GPU: the read probe of libspexis_probe.so (plain coalesced
+    16-byte loads over a 4 GiB buffer, best grid and repetition) and torch's device copy (bytes
+    read plus bytes written per second)."""
+    import ctypes
+    probe = _read_probe()
     src = torch.zeros(nbytes // 4, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
     sink = torch.empty(8192 * 256, dtype=torch.int32, device="cuda")
@@ -313,13 +339,13 @@ def main():
     cold = phase_pass(torch, steps, K, stream)
     warm = phase_pass(torch, [step], K, stream)
     flushed = None
-    peaks = None
     if args.copy_probe == 0:
         fa = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
         flushed = phase_pass(torch, [step], K, stream, flush=lambda: fa.sum())
         del fa
         torch.cuda.empty_cache()
-        peaks = stream_peaks(torch)
+    # the read-rate probe (not in counter runs: its copies would be taken for the calibration's)
+    peaks = stream_peaks(torch) if args.copy_probe == 0 else None
 
     a, toks, status = step.accept_outputs()
     for other in steps[1:]:
@@ -420,6 +446,7 @@ def bench_lm_head(args):
     temp = acc.temperature
 
     def timed(fn, steps, warmup):
+        settle(torch, fn)
         for _ in range(warmup):
             fn()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -431,9 +458,16 @@ def bench_lm_head(args):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / steps   # us
 
+    w_plain = w
     w = sx.spexis_pack_weight(w)   # once per weight, outside the timed region
     us_lm = timed(lambda: sx.spexis_lm_head(h, w, stats, logits=logits, temperature=temp), args.steps, args.warmup)
     us_lm_stats = timed(lambda: sx.spexis_lm_head(h, w, stats, temperature=temp, vocab=V), args.steps, args.warmup)
+    # context: torch's bf16 GEMM of the same product (bf16 output, no statistics), both as
+    # h W^T and as W h^T (the transposed logits), whose library kernels differ
+    us_torch = timed(lambda: torch.nn.functional.linear(h, w_plain), args.steps, args.warmup)
+    ht = h.t()
+    us_torch_t = timed(lambda: torch.mm(w_plain, ht), args.steps, args.warmup)
+    del w_plain, ht
     # Acceptance on logits this LM head produced: target rows from h, draft rows from h plus
     # noise (a draft model sharing the head), drafts drawn from the draft rows (input generation,
     # untimed).  Timed: acceptance computing its own statistics, and from the fused ones.
@@ -486,12 +520,15 @@ def bench_lm_head(args):
                  "frac": round(tfl / MFMA_BF16_TFLOPS, 4), "flops": flops},
         "accept_us": round(us_acc, 2), "accept_with_stats_us": round(us_acc_stats, 2),
         "us_with_gathers": round(us_lm_gather, 2), "accept_with_stats_gathered_us": round(us_acc_gathered, 2),
+        "torch_bf16_us": {"h_wT": round(us_torch, 2), "w_hT": round(us_torch_t, 2)},
+        "protocol": f"each figure: {SETTLE_MS:.0f} ms of the same call, {args.warmup} warmup calls, then the "
+                    f"mean of {args.steps} calls",
         "dtype": "bf16", "data": "synthetic",
     }
     log(f"[lm_head] {T}x{d} @ {V}x{d}: {us_lm:.1f} us ({us_lm_stats:.1f} us without logits) -> {gbs:.0f} GB/s "
         f"({gbs / HBM_PEAK_GBS:.1%}), {tfl:.0f} TFLOP/s ({tfl / MFMA_BF16_TFLOPS:.1%}); accept {us_acc:.1f} us, "
         f"with given statistics {us_acc_stats:.1f} us; with the gathers fused: LM head {us_lm_gather:.1f} us, "
-        f"accept {us_acc_gathered:.1f} us")
+        f"accept {us_acc_gathered:.1f} us; torch bf16 GEMM {us_torch:.1f} us (h W^T), {us_torch_t:.1f} us (W h^T)")
     print(json.dumps(line), flush=True)
 
 
@@ -529,6 +566,7 @@ def bench_select(args):
     theta = float(np.minimum(a, k).sum() / max(k.sum(), 1))
 
     def timed(fn):
+        settle(torch, fn)
         for _ in range(args.warmup):
             fn()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -588,6 +626,7 @@ def bench_lookahead(args):
         prec = torch.where(tau < (1 << 30), 0.83, 0.0).to(torch.float64)
         mem = torch.empty(64, dtype=torch.float64, device="cuda")
         call = lambda: sx.spexis_lookahead_memory(ell, tau, prec, 4, 0.7, mem)
+        settle(torch, call)
         for _ in range(args.warmup):
             call()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -622,6 +661,7 @@ def bench_draft(args):
     ad = wl.make_adapter_inputs(spec, batch, device="cuda", seed=args.seed)
     step = DraftStep(batch, cache, ad)
     stream = torch.cuda.current_stream()
+    settle(torch, step.run)
     for _ in range(args.warmup):
         step.run()
     torch.cuda.synchronize()
@@ -632,6 +672,7 @@ def bench_draft(args):
     ms = (time.perf_counter() - t0) * 1e3 / args.steps
     # the same step replayed from a HIP graph: no host work between its kernels
     step.capture()
+    settle(torch, step.replay)
     for _ in range(args.warmup):
         step.replay()
     torch.cuda.synchronize()
@@ -643,7 +684,7 @@ def bench_draft(args):
     phases = (("adapter_in", step.adapter_in), ("attention", step.attention), ("adapter_out", step.adapter_out),
               ("lm_head", step.lm_head), ("sample", step.sample))
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(phases) + 1)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
+    settle(torch, step.run)
     for i in range(args.steps):
         ev[i][0].record(stream)
         for j, (_, fn) in enumerate(phases):
