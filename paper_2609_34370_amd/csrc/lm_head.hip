@@ -327,9 +327,10 @@ void lm_head_kernel(LmParams p) {
 // More than 160 rows of a wide projection (an LM head's vocabulary): one workgroup of eight waves
 // (two per SIMD) per (256-column tile, group of 320 rows), so that each K-slice of W crosses L2
 // once per 320 rows.  Both operands go through LDS: every K-step of 64 the
-// workgroup's threads copy h (320 rows, 40 KB) and W (eight packed 32-column tiles, 32 KB) into
-// one of two stages, loaded one step ahead into registers, and the waves read their fragments
-// from the stage.  Wave (wr, wc) of a 2 x 4 grid computes rows 160 wr .. +160 (five row tiles)
+// workgroup copies h (320 rows, 40 KB) and W (eight packed 32-column tiles, 32 KB) from memory
+// straight into one of two stages, a step ahead, and the waves read their fragments from the
+// stage, those of the next MFMA step while the current step's MFMAs run.  Wave (wr, wc) of a
+// 2 x 4 grid computes rows 160 wr .. +160 (five row tiles)
 // by columns 64 wc .. +64 (two column tiles): 160 accumulators, within the 256 registers a wave
 // has at two waves per SIMD.  Against four waves per 160-row x 256-column workgroup (two row
 // groups, each reading W), the L2 serves about 2.35 GB instead of 3.4 GB at 320 x 4096 @ 128256.
@@ -341,9 +342,9 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
   constexpr int kRows = 32 * NRT;     // 320
   constexpr int kCols = 32 * WC * CT; // 256
   constexpr int kStatTiles = kCols / kLmCols;
-  constexpr int kHChunks = kRows * 8 / 512;   // 16-byte h chunks each thread copies per step (5)
-  constexpr int kWChunks = 8 * 256 / 512;     // 16-byte W chunks each thread copies per step (4)
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 31, half = lane >> 5;
+  // the wave index wave-uniform (scalar), so the copies' LDS destinations are scalar sums
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int lane = threadIdx.x & 63, col = lane & 31, half = lane >> 5;
   const int wr = wave / WC, wc = wave % WC;
   const int wgcols = (p.V + kCols - 1) / kCols;
   int nt, mg;
@@ -358,35 +359,49 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
 
   // stage x of h: row r, chunk kc (8 K values) at r * 8 + (kc ^ ((r >> 1) & 7)) (the 16 rows of
   // one ds_read_b128 pass hit distinct bank groups); stage x of W: packed tile c (columns
-  // n0 + 32 c ..), its 256 chunks in packed order
-  __shared__ u32x4 sm_h[2][kRows * 8];
-  __shared__ u32x4 sm_w[2][8 * 256];
-  u32x4 hreg[kHChunks], wreg[kWChunks];
-  auto load_step = [&](int j) {
-    j = min(j, nsteps - 1);   // past the end: re-read the last step (kept unconditional)
+  // n0 + 32 c ..), its 256 chunks in packed order.  One array: h stages 0 and 1, then W stages
+  // 0 and 1.
+  constexpr int kHStage = kRows * 8, kWStage = 8 * 256;
+  __shared__ u32x4 sm[2 * kHStage + 2 * kWStage];
+  // Copies go from memory straight into a stage (buffer loads to LDS, 1 KB per wave and
+  // instruction, lane l's 16 bytes at slot 64 u + l): no staging registers, which leaves room
+  // for two sets of operand fragments.  Buffer resources span the group's rows of h and the
+  // workgroup's packed W tiles: loads past them (rows past M, columns past V) return zeros,
+  // whose results are dropped.
+  constexpr int kWaves = WR * WC;
+  constexpr int kHCopies = kHStage / 64 / kWaves;   // copy instructions per wave and step
+  constexpr int kWCopies = kWStage / 64 / kWaves;
+  static_assert(kHStage % (64 * kWaves) == 0 && kWStage % (64 * kWaves) == 0, "copy split");
+  const int wt0 = n0 / 32, wtn = min(8, wtiles - wt0);
+  const __amdgpu_buffer_rsrc_t hrs =
+      __builtin_amdgcn_make_buffer_rsrc((void*)hbase, (short)0, rows * p.d * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(wbase + (int64_t)wt0 * (p.d / kLmK) * kPackTile), (short)0, wtn * (p.d / kLmK) * kPackTile * 2,
+      0x00020000);
+  int hoff[kHCopies], woff[kWCopies];   // byte offsets of the lane's chunks at step 0
 #pragma unroll
-    for (int u = 0; u < kHChunks; ++u) {
-      const int q = threadIdx.x + 512 * u;
-      const int r = min(q >> 3, rows - 1), kc = q & 7;
-      hreg[u] = *reinterpret_cast<const u32x4*>(hbase + (int64_t)r * p.d + j * kLmK + 8 * kc);
-    }
+  for (int u = 0; u < kHCopies; ++u) {
+    const int q = (wave * kHCopies + u) * 64 + lane;
+    const int r = q >> 3, kc = (q & 7) ^ ((r >> 1) & 7);
+    hoff[u] = (r * p.d + 8 * kc) * 2;
+  }
 #pragma unroll
-    for (int u = 0; u < kWChunks; ++u) {
-      const int q = threadIdx.x + 512 * u;
-      const int wt = min(n0 / 32 + (q >> 8), wtiles - 1);
-      wreg[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(
-          wbase + ((int64_t)wt * (p.d / kLmK) + j) * kPackTile + 8 * (q & 255)));
-    }
-  };
-  auto store_step = [&](int stage) {
+  for (int u = 0; u < kWCopies; ++u) {
+    const int q = (wave * kWCopies + u) * 64 + lane;
+    woff[u] = ((q >> 8) * (p.d / kLmK) * kPackTile + 8 * (q & 255)) * 2;
+  }
+  auto copy_step = [&](int j, int stage) {
 #pragma unroll
-    for (int u = 0; u < kHChunks; ++u) {
-      const int q = threadIdx.x + 512 * u;
-      const int r = q >> 3, kc = q & 7;
-      sm_h[stage][r * 8 + (kc ^ ((r >> 1) & 7))] = hreg[u];
-    }
+    for (int u = 0; u < kHCopies; ++u)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          hrs, (__attribute__((address_space(3))) void*)(sm + stage * kHStage + (wave * kHCopies + u) * 64), 16,
+          hoff[u], j * kLmK * 2, 0, 0);
 #pragma unroll
-    for (int u = 0; u < kWChunks; ++u) sm_w[stage][threadIdx.x + 512 * u] = wreg[u];
+    for (int u = 0; u < kWCopies; ++u)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          wrs,
+          (__attribute__((address_space(3))) void*)(sm + 2 * kHStage + stage * kWStage + (wave * kWCopies + u) * 64),
+          16, woff[u], j * kPackTile * 2, 0, 0);
   };
 
   f32x16 acc[RT][CT];
@@ -397,37 +412,71 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[t][c][e] = 0.f;
 
+  // Fragment reads are written as instructions: the compiler would make every LDS read wait for
+  // all copies to LDS in flight (into either stage), which cancels the copies' prefetch.  The
+  // reads of MFMA step s + 1 go out before step s's MFMAs, and each step waits for its own
+  // fragments by count (LDS reads return in order).  Byte addresses: A fragment of row tile t at
+  // step s, h stage + (32 (wr RT + t) + col) * 128 + ((4 half + s) ^ ((col >> 1) & 7)) * 16 (row
+  // m's swizzle (m >> 1) & 7 is col's, 32 (wr RT + t) being a multiple of 16); B fragment of
+  // column tile c, W stage + ((CT wc + c) * 256 + 64 s + lane) * 16.
+  static_assert(RT == 5 && CT == 2, "the waits below name five A and two B fragments");
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) u32x4*)sm;   // LDS byte address
+  uint32_t aaddr[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    aaddr[s] = lds0 + (32 * wr * RT + col) * 128 + (((4 * half + s) ^ ((col >> 1) & 7)) << 4);
+  const uint32_t baddr = lds0 + 2 * kHStage * 16 + (CT * wc * 256 + lane) * 16;
+  auto lds_read = [](uint32_t addr) {
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+    return v;
+  };
   auto compute = [&](int stage) {
+    u32x4 a[2][RT], b[2][CT];
+    auto frags = [&](int s, int x) {
+#pragma unroll
+      for (int t = 0; t < RT; ++t) a[x][t] = lds_read(aaddr[s] + stage * kHStage * 16 + t * 4096);
+#pragma unroll
+      for (int c = 0; c < CT; ++c) b[x][c] = lds_read(baddr + stage * kWStage * 16 + c * 4096 + s * 1024);
+    };
+    frags(0, 0);
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      u32x4 b[CT], a[RT];
-#pragma unroll
-      for (int c = 0; c < CT; ++c) b[c] = sm_w[stage][(CT * wc + c) * 256 + s * 64 + lane];
-#pragma unroll
-      for (int t = 0; t < RT; ++t) {
-        const int m = 32 * (wr * RT + t) + col;
-        a[t] = sm_h[stage][m * 8 + ((4 * half + s) ^ ((m >> 1) & 7))];
+      const int x = s & 1;
+      if (s < 3) {
+        frags(s + 1, x ^ 1);
+        asm volatile("s_waitcnt lgkmcnt(7)"
+                     : "+v"(a[x][0]), "+v"(a[x][1]), "+v"(a[x][2]), "+v"(a[x][3]), "+v"(a[x][4]), "+v"(b[x][0]),
+                       "+v"(b[x][1])
+                     :
+                     : "memory");
+      } else {
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(a[x][0]), "+v"(a[x][1]), "+v"(a[x][2]), "+v"(a[x][3]), "+v"(a[x][4]), "+v"(b[x][0]),
+                       "+v"(b[x][1])
+                     :
+                     : "memory");
       }
 #pragma unroll
       for (int t = 0; t < RT; ++t)
 #pragma unroll
         for (int c = 0; c < CT; ++c)
-          acc[t][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a[t]), as_bf16x8(b[c]), acc[t][c], 0, 0, 0);
+          acc[t][c] =
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a[x][t]), as_bf16x8(b[x][c]), acc[t][c], 0, 0, 0);
     }
   };
 
-  // step j: compute from stage j % 2 while step j+1's copies (loaded during step j-1) go into the
-  // other stage, then load step j+2
-  load_step(0);
-  store_step(0);
-  load_step(1);
-  __syncthreads();
+  // step j: wait for this wave's copies of step j, then the barrier makes every wave's copies
+  // visible and tells that all have finished step j - 1, whose stage step j + 1 now fills while
+  // step j is computed
+  copy_step(0, 0);
   for (int j = 0; j < nsteps; ++j) {
-    compute(j & 1);
-    store_step((j + 1) & 1);
-    load_step(j + 2);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+    if (j + 1 < nsteps) copy_step(j + 1, (j + 1) & 1);
+    compute(j & 1);
   }
+  __syncthreads();   // the epilogue's transposes reuse h stage 0
 
   // ---- epilogue (accumulator value i of lane l in tile (t, c): row 32 (wr RT + t) + 8 (i / 4)
   // + 4 (l / 32) + i % 4, column 32 (CT wc + c) + l % 32)
@@ -480,7 +529,7 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
   // tiles in order; the two waves of a row and 128-column statistics tile combine in order.
   __shared__ float sm_m[WC][kRows], sm_z[WC][kRows];
   constexpr int kTS = 36;   // floats per transposed row (16-byte aligned, padded)
-  float* tile = reinterpret_cast<float*>(&sm_h[0][0]) + wave * 32 * kTS;
+  float* tile = reinterpret_cast<float*>(&sm[0]) + wave * 32 * kTS;
 #pragma unroll
   for (int t = 0; t < RT; ++t) {
     float wm = -INFINITY, wz = 0.f;
@@ -562,14 +611,18 @@ static hipError_t launch_lm_nrt(const LmParams& q, hipStream_t s) {
 // than groups of 160 (five tiles), else 160.  The larger group makes about 10% fewer L2 requests
 // per output (measured 4.73 against 4.98 ms at 4608 x 3584 @ 152064); 320 rows keep two groups
 // of 160 rather than two of 192.
-// The eight-wave kernel takes 161 to 320 rows: one group.  Beyond, in groups of 320 rows, it was
-// slower than the four-wave groups of 192 (4608 x 3584 @ 152064: 5280 against 5100 us without
-// logits), whose waves keep more MFMAs per LDS fragment read.
-static bool wide_rows(int64_t M) { return M <= 320; }
-
 static int64_t group_rows(int64_t M) {
   const int64_t p160 = (M + 159) / 160 * 160, p192 = (M + 191) / 192 * 192;
   return p192 * 20 <= p160 * 21 ? 192 : 160;
+}
+
+// The eight-wave kernel takes 161 to 320 rows (one group), and more rows in groups of 320 when
+// those pad M by no more than its speed per row makes up for: it ran 12% faster than the
+// four-wave groups of 192 at 4608 x 3584 @ 152064 (4273 against 4885 us without logits), so it
+// is taken while its padded rows stay within 1.12 times theirs.
+static bool wide_rows(int64_t M) {
+  const int64_t g = group_rows(M);
+  return M <= 320 || (M + 319) / 320 * 320 * 100 <= (M + g - 1) / g * g * 112;
 }
 
 // Up to 128 rows, 256-column workgroups when the columns alone give at least one workgroup per
