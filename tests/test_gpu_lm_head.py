@@ -69,8 +69,11 @@ def check(h, hb, w, wb, T, rows_idx=None):
     return logits, stats
 
 
+# (320, 2048), (200, 70001), (961, 4099) and (1500, 9000) run the eight-wave kernel: one group,
+# a vocabulary whose last packed tile is part zeros, a last group of one row, a last group of
+# 220 rows with a 40-column last tile; (333, 3000) and (700, 130) the four-wave groups
 @pytest.mark.parametrize("rows,V,d", [(1, 1000, 256), (37, 4101, 512), (320, 2048, 256), (333, 3000, 256),
-                                      (700, 130, 512), (1500, 9000, 256)])
+                                      (700, 130, 512), (1500, 9000, 256), (200, 70001, 256), (961, 4099, 512)])
 def test_lm_head_small_shapes(rows, V, d):
     h, hb = bf16_pair((rows, d), 1, 1.0)
     w, wb = bf16_pair((V, d), 2, 0.05)
