@@ -12,8 +12,9 @@
 // boundaries, and block ids fetched one tile ahead with scalar loads (their wait counter is
 // not the one the tile loads use).  An item a wave covers whole is normalised and written as
 // bf16; an item cut between shares leaves fp32 partials (reference maximum, sum,
-// unnormalised output) that a second kernel combines.  Balance is exact to one tile, whatever
-// the mix of sequence lengths.
+// unnormalised output) that a second kernel combines -- the partial of a share's first item
+// held in LDS until the wave ends.  Balance is exact to one tile, whatever the mix of sequence
+// lengths.
 //
 // Per 32-key tile and 32-row tile, with v_mfma_f32_32x32x16_bf16 (operand A: lane l holds row
 // l%32, k-slice 8*(l/32)..+7; B: column l%32, same k-slice; C: lane l, value i holds row
@@ -261,12 +262,22 @@ void verify_attn_kernel(AttnParams p) {
   bool starts_before = false;
   int head_b = 0, head_f = 0, head_nt = 0, head_q0 = 0, head_n = 0, head_flag = 0;
   int lim[NT];
-  // Q, the score product's B operand, in operand order.  Two row tiles keep it in this wave's
-  // part of LDS (registers would not hold it next to two tiles' accumulators); one in registers.
+  // Q, the score product's B operand, in operand order: with two row tiles, row tile 0 in this
+  // wave's part of LDS and row tile 1 in registers (both in registers would not fit next to two
+  // tiles' accumulators); one row tile in registers.
   constexpr bool kQinLds = NT == 2;
   u32x4 qr[kQinLds ? 1 : NT][KS];
-  __shared__ u32x4 sm_q[kQinLds ? 4 : 1][NT][KS][kWave];
+  __shared__ u32x4 sm_q[kQinLds ? 4 : 1][KS][kWave];
   const int wave = threadIdx.x >> 6;
+  // The partial of the share's first item (its later part, which ends inside the share) waits in
+  // this wave's LDS, its maxima and sums in registers, and goes to memory when the wave ends:
+  // stores issued in the middle of a share cost far more than their bytes (a timing-only copy
+  // without them ran 9% faster at 20 and at 63 rows per item).  With two row tiles of 128-wide
+  // heads the four waves' stashes and row tile 0 of Q fill the 160 KB of LDS exactly.
+  __shared__ f32x4 sm_stash[4][NT * 32 * D / 4];
+  float st_m[NT], st_l[NT];
+  bool stashed = false;
+  int stash_rows = 0;
   float m[NT], l[NT];
   f32x16 acc[NT][MT];
 
@@ -286,12 +297,12 @@ void verify_attn_kernel(AttnParams p) {
       lim[nt] = L + j;   // keys 0..L+j are visible
       const uint16_t* qrow = reinterpret_cast<const uint16_t*>(p.q) +
                              ((int64_t)(q0 + j) * p.hq + h * p.group + gq) * D + 8 * half;
-      if (kQinLds) {
+      if (kQinLds && nt == 0) {
         u32x4 t[KS];
 #pragma unroll
         for (int s = 0; s < KS; ++s) t[s] = ld16(qrow + 16 * s);
 #pragma unroll
-        for (int s = 0; s < KS; ++s) sm_q[kQinLds ? wave : 0][nt][s][lane] = t[s];
+        for (int s = 0; s < KS; ++s) sm_q[kQinLds ? wave : 0][s][lane] = t[s];
       } else {
 #pragma unroll
         for (int s = 0; s < KS; ++s) qr[kQinLds ? 0 : nt][s] = ld16(qrow + 16 * s);
@@ -338,6 +349,15 @@ void verify_attn_kernel(AttnParams p) {
             w[1] = pack_bf16x2(acc[nt][mt][4 * a + 2] * inv, acc[nt][mt][4 * a + 3] * inv);
             *reinterpret_cast<u32x2*>(orow + 32 * mt + 8 * a + 4 * half) = w;
           }
+      } else if (starts_before) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int a = 0; a < 4; ++a)
+            sm_stash[wave][(r * D + 32 * mt + 8 * a + 4 * half) / 4] =
+                f32x4{acc[nt][mt][4 * a], acc[nt][mt][4 * a + 1], acc[nt][mt][4 * a + 2], acc[nt][mt][4 * a + 3]};
+        st_m[nt] = m[nt];
+        st_l[nt] = lt;
       } else {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
@@ -352,6 +372,10 @@ void verify_attn_kernel(AttnParams p) {
           slot[(int64_t)p.rmax * D + p.rmax + r] = lt;
         }
       }
+    }
+    if (starts_before) {
+      stashed = true;
+      stash_rows = R;
     }
   };
 
@@ -384,7 +408,8 @@ void verify_attn_kernel(AttnParams p) {
 #pragma unroll
       for (int s = 0; s < KS; ++s)
         sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            as_bf16x8(B.k[s]), as_bf16x8(kQinLds ? sm_q[kQinLds ? wave : 0][nt][s][lane] : qr[kQinLds ? 0 : nt][s]),
+            as_bf16x8(B.k[s]),
+            as_bf16x8(kQinLds && nt == 0 ? sm_q[kQinLds ? wave : 0][s][lane] : qr[kQinLds ? 0 : nt][s]),
             sc, 0, 0, 0);
       float x[16];
 #pragma unroll
@@ -445,6 +470,23 @@ void verify_attn_kernel(AttnParams p) {
     for (int d = 0; d < DEPTH; ++d) {
       process(buf[d], i + d);
       load_tile(buf[d], i + d + DEPTH);
+    }
+  }
+
+  // the stashed partial to slot 0, 16 bytes per lane and step (the wave's own LDS writes are
+  // complete before its reads).  (Issued instead right after the share's last tile load, so that
+  // the stores drain under the last tiles' compute, it needed the loop split in two, and the
+  // kernel ran slower.)
+  if (stashed) {
+    for (int idx = lane; idx < stash_rows * D / 4; idx += kWave)
+      *reinterpret_cast<f32x4*>(slots + 4 * (int64_t)idx) = sm_stash[wave][idx];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int r = nt * 32 + col;
+      if (half == 0 && r < stash_rows) {
+        slots[(int64_t)p.rmax * D + r] = st_m[nt];
+        slots[(int64_t)p.rmax * D + p.rmax + r] = st_l[nt];
+      }
     }
   }
 
