@@ -46,6 +46,29 @@ __device__ __forceinline__ float halves_sum(float v) {
 }
 
 constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" of the running maxima
+
+// acc[mt] *= alpha (alpha per lane: the lane's query row), in place on the registers that hold the
+// accumulators.  Written out because otherwise the compiler keeps a second copy of every
+// accumulator in vector registers, refreshed by one v_accvgpr_read per accumulator on every tile,
+// for the rare tiles that take this path.  The hazard checks do not look inside inline assembly:
+// the leading s_nops give an accumulator's last MFMA its 18+ wait states before the first read
+// (this is its own basic block, so no MFMA is scheduled in between), the trailing one covers the
+// last write before the next MFMA reads it as its C operand.
+template <int MT>
+__device__ __forceinline__ void scale_acc(f32x16 (&acc)[MT], float alpha) {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      float v = acc[mt][e], t;
+      asm volatile("v_accvgpr_read_b32 %1, %0\n\tv_mul_f32 %1, %1, %2\n\tv_accvgpr_write_b32 %0, %1"
+                   : "+a"(v), "=&v"(t)
+                   : "v"(alpha));
+      acc[mt][e] = v;
+    }
+  asm volatile("s_nop 4");
+}
 constexpr float kLazy = 8.0f;         // base-2 headroom before the running maximum moves
 constexpr int kWaitVmcnt0 = 0x0F70;   // s_waitcnt operand: vmcnt(0), expcnt and lgkmcnt not waited
 
@@ -428,14 +451,14 @@ void verify_attn_kernel(AttnParams p) {
       // Lazy rescaling: the reference maximum moves only when a score exceeds it by more than
       // 2^kLazy, so 2^(x - m) stays <= 2^kLazy and the accumulators are rescaled rarely.
       if (__builtin_amdgcn_ballot_w64(mx > m[nt] + kLazy) != 0) {
-        const float mnew = fmaxf(m[nt], mx);
-        const float alpha = fast_exp2(m[nt] - mnew);
+        const float mold = m[nt];
+        const float mnew = fmaxf(mold, mx);
+        const float alpha = fast_exp2(mold - mnew);
         m[nt] = mnew;
         l[nt] *= alpha;
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) acc[nt][mt][e] *= alpha;
+        // a row still at kNegBig has added nothing yet (its accumulators are zero): the first tile
+        // of an item moves every row's maximum and scales nothing
+        if (__builtin_amdgcn_ballot_w64(mold > kNegBig) != 0) scale_acc<MT>(acc[nt], alpha);
       }
       float ps = 0.f;
 #pragma unroll
