@@ -14,19 +14,19 @@
 // reads the same partials.  Kernels, in order on the caller's stream (kernel boundaries are
 // the only synchronisation):
 //   rounds    (logit inputs) the tests run in rounds of doubling width, positions {0,1},
-//             {2..5}, {6..13}, ... (one round for small batches); a round takes only the
-//             sequences that passed every test before it (a device-side list), so rows past a
-//             rejection are rarely read.
+//             {2..5}, {6..13}, ... (or {0}, {1,2}, ... when a first round over {0,1} would read
+//             a lot; one round for short rows); a round takes only the sequences that passed
+//             every test before it (a device-side list), so rows past a rejection are rarely read.
 //     stats   round 0: the statistics (max, sum of 2^(y - max)) of its target and draft rows,
 //             per (row, sub-chunk), and the inputs of its tests.  The tests of a round are
 //             independent of each other, so nothing here waits for a decision.
-//     decide  round r, one work item per (sequence, sub-chunk): every item of a sequence runs
-//             the round's tests from those statistics (its waves split the positions) and
-//             reaches the same first failure a; then it computes the fixed-point sums of the
-//             residual of row a (or of the bonus row) over its sub-chunk, or, for a sequence
-//             that passed every test, the statistics of round r+1's rows over its sub-chunk
-//             (and puts the sequence on round r+1's list).  So the sampled rows of finished
-//             sequences stream together with the next round's rows, one launch per round.
+//     tests   round r, one workgroup per sequence of the round's list: the round's tests from
+//             those statistics, the first failure a, and the sequence's job in the stream
+//             launch: the residual of row a (or the bonus row) to sum, or, for a sequence that
+//             passed every test of the round, round r+1's statistics (it joins that list).
+//     stream  round r, one work item per (sequence of the list, sub-chunk): the job, after one
+//             load of its record.  So the sampled rows of finished sequences stream together
+//             with the next round's rows.
 //   init      (probability inputs) one thread per sequence: geometry, draft-id check, tests.
 //   max pass  (probability inputs) per sub-chunk: max of p, bad flag.
 //   sum pass  (probability inputs) per sub-chunk: the sums of W_v.
@@ -50,6 +50,7 @@ constexpr int kTestsGrid = 4096;                 // workgroups of a later round'
 constexpr int64_t kOneRoundBytes = 192ll << 20;  // target rows that one test round reads whole
 constexpr int64_t kRoundRowBytes = 256ll << 10;  // rows this long pay for the launches of a round
 constexpr int64_t kNarrowFirstBytes = 256ll << 20;  // a first round over {0,1} reading more starts with {0}
+constexpr int64_t kStatPairItems = 16384;        // statistics passes of more (row, sub-chunk) items pair them
 
 enum Mode { kResidual = 1, kBonus = 2, kDone = 3 };
 // the job of a listed sequence in a round's stream launch
@@ -432,10 +433,10 @@ __device__ __forceinline__ void wave_stats(float (&v)[kPerLane], float c, float&
   if (bad) z = NAN;
 }
 
-// Sequence b's rows and state for the decide launches (valid: 1 valid, 0 no query token, -1 a
-// draft id outside [0, V)), written once per sequence by the pass before the first decide launch
-// (the statistics or the gather pass).  That launch then reads one record per item instead of
-// query_start_loc and every draft id: a dependent round trip less for each of its items.
+// Sequence b's rows and state for the tests launches (valid: 1 valid, 0 no query token, -1 a
+// draft id outside [0, V)), written once per sequence by the pass before the first tests launch
+// (the statistics or the gather pass).  That launch then reads one record per sequence instead
+// of query_start_loc and every draft id: a dependent round trip less.
 __device__ __forceinline__ void store_geom_state(const AcceptParams& p, int b, const Geom& g, int bad_id) {
   const int state = !g.valid ? 0 : bad_id ? -1 : 1;
   *reinterpret_cast<u32x4*>(p.geo + 4 * (int64_t)b) = u32x4{(uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k, (uint32_t)state};
@@ -535,30 +536,36 @@ __device__ void next_round_stats(const AcceptParams& p, int b, const Geom& g, in
 }
 
 // Round 0, positions [0, hi): statistics of target rows 0..min(hi-1, k) and draft rows
-// 0..min(hi, k)-1 of every sequence, one work item per (row, sub-chunk), and the inputs of the
-// tests at those positions.  (Items of one row each keep more loads in flight than items that
-// stream a sequence's rows one after another.)
+// 0..min(hi, k)-1 of every sequence, one work item per (row, SUBS consecutive sub-chunks), and
+// the inputs of the tests at those positions.  An item issues the loads of all its sub-chunks
+// before it reduces the first.  (Items of one row each keep more loads in flight than items
+// that stream a sequence's rows one after another.)
+template <int SUBS>
 __global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p, int hi) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   if (blockIdx.x == 0 && threadIdx.x <= kAcceptMaxRounds) p.counts[threadIdx.x] = 0;
   const int rows = 2 * hi;
-  const int64_t total = (int64_t)p.B * rows * p.nsub;
+  const int ngrp = (p.nsub + SUBS - 1) / SUBS;
+  const int64_t total = (int64_t)p.B * rows * ngrp;
   for (int64_t item = blockIdx.x; item < total; item += gridDim.x) {
-    const int sub = (int)(item % p.nsub);
-    const int64_t rest = item / p.nsub;
+    const int grp = (int)(item % ngrp);
+    const int64_t rest = item / ngrp;
     const int rr = (int)(rest % rows), b = (int)(rest / rows);
     const int pos = rr >> 1, which = rr & 1;
     int n;
     const Geom g = seq_geom(p, b, n);
     const bool skip = !g.valid || pos > g.k || (which == 1 && pos == g.k);
-    float v[kPerLane];
+    const int sub0 = grp * SUBS, nsubs = min(SUBS, p.nsub - sub0);
+    float v[SUBS][kPerLane];
     if (!skip) {
       const float* row = which ? p.draft + (int64_t)(g.d0 + pos) * p.V : p.target + (int64_t)(g.t0 + pos) * p.V;
-      load_sub<true>(row, sub, wave, p.V, (p.V & 3) == 0, -INFINITY, lane, v);
+#pragma unroll
+      for (int u = 0; u < SUBS; ++u)
+        if (u < nsubs) load_sub<true>(row, sub0 + u, wave, p.V, (p.V & 3) == 0, -INFINITY, lane, v[u]);
     }
-    // the first item of each sequence records it for the decide launches (its id loads follow the
+    // the first item of each sequence records it for the tests launches (its id loads follow the
     // row's, so they add no round trip)
-    if (rr == 0 && sub == 0 && wave == 0) {
+    if (rr == 0 && grp == 0 && wave == 0) {
       int bad = 0;
       for (int i = lane; i < g.k; i += kWave) {
         const int x = p.ids[g.d0 + i];
@@ -569,8 +576,10 @@ __global__ __launch_bounds__(kThreads) void accept_stats_kernel(AcceptParams p, 
     }
     if (skip) continue;
     // the inputs of test pos, gathered here so that the decision needs no dependent gather
-    if (which == 0 && pos < g.k && sub == 0 && threadIdx.x == 0) gather_test(p, b, g, pos);
-    store_sub_stats(p, v, lse_slot(p, b, pos, which), sub, wave, lane);
+    if (which == 0 && pos < g.k && grp == 0 && threadIdx.x == 0) gather_test(p, b, g, pos);
+#pragma unroll
+    for (int u = 0; u < SUBS; ++u)   // nsubs is the same for the whole workgroup
+      if (u < nsubs) store_sub_stats(p, v[u], lse_slot(p, b, pos, which), sub0 + u, wave, lane);
   }
 }
 
@@ -1073,8 +1082,15 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
         (int64_t)p.V * 4 < kRoundRowBytes && (int64_t)p.B * (p.max_k + 1) * p.V * 4 <= kOneRoundBytes;
     int width = one_round ? p.max_k + 1 : ((int64_t)p.B * 4 * p.V * 4 > kNarrowFirstBytes ? 1 : 2);
     {
-      const unsigned gs = (unsigned)((int64_t)p.B * 2 * width * p.nsub);
-      hipLaunchKernelGGL(accept_stats_kernel, dim3(gs), dim3(kThreads), 0, s, p, width);
+      // Large passes take two sub-chunks per work item (measured: 6 us faster at 512 sequences
+      // of 152064 entries and 2 us at 256 of 128256; 1 us slower at 64 of 128256).
+      const int64_t items = (int64_t)p.B * 2 * width * p.nsub;
+      if (items > kStatPairItems) {
+        hipLaunchKernelGGL(accept_stats_kernel<2>, dim3((unsigned)((int64_t)p.B * 2 * width * ((p.nsub + 1) / 2))),
+                           dim3(kThreads), 0, s, p, width);
+      } else {
+        hipLaunchKernelGGL(accept_stats_kernel<1>, dim3((unsigned)items), dim3(kThreads), 0, s, p, width);
+      }
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     for (int r = 0, lo = 0; lo <= p.max_k; ++r, lo += width, width *= 2) {
