@@ -72,6 +72,23 @@ def test_append_bit_exact(wid):
     assert np.array_equal(bf16_to_u16(attn.v_pool), vp)
 
 
+@pytest.mark.parametrize("bs,D", [(16, 128), (32, 128), (16, 64), (32, 64)])
+def test_append_long_queries_bit_exact(bs, D):
+    # up to 150 new rows per sequence (more than the 64 V rows the kernel stages in LDS at a
+    # time, so a 16-slot unit can be written by two chunks), empty caches and one-row queries
+    say(f"[append] long queries bs={bs} D={D}")
+    spec, batch, attn, _ = case(1, seed=50 + bs + D, accept=False, batch=9, block_size=bs, head_dim=D,
+                                ctx=("uniform", 0, 70), k=("uniform", 0, 149))
+    k0, v0 = bf16_to_u16(attn.k_pool), bf16_to_u16(attn.v_pool)
+    step = VerifyStep(batch, attn, None)
+    step.append()
+    torch.cuda.synchronize()
+    kp, vp = oracle_pools_after_append(spec, batch, k0, v0, attn)
+    assert int(batch.k.max()) + 1 > 64
+    assert np.array_equal(bf16_to_u16(attn.k_pool), kp)
+    assert np.array_equal(bf16_to_u16(attn.v_pool), vp)
+
+
 # ------------------------------------------------------------------------- attention
 
 def check_attention(wid, nseq=None, seed=None, kv_chunk_tokens=0, **over):
