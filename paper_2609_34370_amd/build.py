@@ -38,7 +38,9 @@ def _compile(src: str) -> str:
 
 def _link(objs, path: str) -> None:
     tmp = path + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
+    # --no-undefined: a symbol no object defines (e.g. a kernel stub the host side failed to
+    # instantiate) fails the build instead of the first load
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-Wl,--no-undefined", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")

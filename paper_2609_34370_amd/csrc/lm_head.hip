@@ -40,6 +40,26 @@ __device__ __forceinline__ uint16_t bf16_rne(float f) {
 __device__ __forceinline__ float bf16_float(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
 
+// Waits until at most N LDS reads (or scalar loads) of the wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_lgkm() {
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
+// One 16-byte LDS read, written as an instruction (byte address addr).
+__device__ __forceinline__ u32x4 lds_read_b128(uint32_t addr) {
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+  return v;
+}
+// Ties a register to the wait before it: no use of v moves above that wait.
+__device__ __forceinline__ void tie(u32x4& v) { asm volatile("" : "+v"(v)); }
+// A 16-byte-per-lane buffer load into LDS (lane l's bytes at lds + 16 l).  Kept out of the
+// kernel templates: the host side of a template kernel cannot instantiate this builtin.
+__device__ __forceinline__ void buffer_load_lds16(__amdgpu_buffer_rsrc_t rs, __attribute__((address_space(3))) void* lds,
+                                                  int voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, lds, 16, voff, soff, 0, 0);
+}
+
 // W rows are read once: non-temporal loads keep them from evicting h out of L2.
 template <bool kStream>
 __device__ __forceinline__ u32x4 ldw(const uint16_t* p) {
@@ -336,12 +356,14 @@ void lm_head_kernel(LmParams p) {
 // groups, each reading W), the L2 serves about 2.35 GB instead of 3.4 GB at 320 x 4096 @ 128256.
 // Epilogue as lm_head_kernel's: logits or bf16 outputs, then each row's statistics per
 // 128-column tile.
-__global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
-  constexpr int RT = 5, CT = 2, WR = 2, WC = 4;
+template <int RT, int CT, int WR, int WC>
+__global__ __launch_bounds__(64 * WR * WC) __attribute__((amdgpu_waves_per_eu(WR * WC / 4)))
+void lm_head_wide_kernel(LmParams p) {
   constexpr int NRT = WR * RT;        // row tiles of the workgroup
-  constexpr int kRows = 32 * NRT;     // 320
-  constexpr int kCols = 32 * WC * CT; // 256
+  constexpr int kRows = 32 * NRT;     // rows of the group
+  constexpr int kCols = 32 * WC * CT; // columns of the workgroup
   constexpr int kStatTiles = kCols / kLmCols;
+  static_assert(kCols == 256 && WC % kStatTiles == 0, "two 128-column statistics tiles, whole waves each");
   // the wave index wave-uniform (scalar), so the copies' LDS destinations are scalar sums
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int lane = threadIdx.x & 63, col = lane & 31, half = lane >> 5;
@@ -361,7 +383,7 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
   // one ds_read_b128 pass hit distinct bank groups); stage x of W: packed tile c (columns
   // n0 + 32 c ..), its 256 chunks in packed order.  One array: h stages 0 and 1, then W stages
   // 0 and 1.
-  constexpr int kHStage = kRows * 8, kWStage = 8 * 256;
+  constexpr int kHStage = kRows * 8, kWStage = kCols / 32 * 256;
   __shared__ u32x4 sm[2 * kHStage + 2 * kWStage];
   // Copies go from memory straight into a stage (buffer loads to LDS, 1 KB per wave and
   // instruction, lane l's 16 bytes at slot 64 u + l): no staging registers, which leaves room
@@ -372,7 +394,7 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
   constexpr int kHCopies = kHStage / 64 / kWaves;   // copy instructions per wave and step
   constexpr int kWCopies = kWStage / 64 / kWaves;
   static_assert(kHStage % (64 * kWaves) == 0 && kWStage % (64 * kWaves) == 0, "copy split");
-  const int wt0 = n0 / 32, wtn = min(8, wtiles - wt0);
+  const int wt0 = n0 / 32, wtn = min(kCols / 32, wtiles - wt0);
   const __amdgpu_buffer_rsrc_t hrs =
       __builtin_amdgcn_make_buffer_rsrc((void*)hbase, (short)0, rows * p.d * 2, 0x00020000);
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
@@ -393,15 +415,13 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
   auto copy_step = [&](int j, int stage) {
 #pragma unroll
     for (int u = 0; u < kHCopies; ++u)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          hrs, (__attribute__((address_space(3))) void*)(sm + stage * kHStage + (wave * kHCopies + u) * 64), 16,
-          hoff[u], j * kLmK * 2, 0, 0);
+      buffer_load_lds16(hrs, (__attribute__((address_space(3))) void*)(sm + stage * kHStage + (wave * kHCopies + u) * 64),
+                        hoff[u], j * kLmK * 2);
 #pragma unroll
     for (int u = 0; u < kWCopies; ++u)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          wrs,
-          (__attribute__((address_space(3))) void*)(sm + 2 * kHStage + stage * kWStage + (wave * kWCopies + u) * 64),
-          16, woff[u], j * kPackTile * 2, 0, 0);
+      buffer_load_lds16(
+          wrs, (__attribute__((address_space(3))) void*)(sm + 2 * kHStage + stage * kWStage + (wave * kWCopies + u) * 64),
+          woff[u], j * kPackTile * 2);
   };
 
   f32x16 acc[RT][CT];
@@ -419,18 +439,14 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
   // step s, h stage + (32 (wr RT + t) + col) * 128 + ((4 half + s) ^ ((col >> 1) & 7)) * 16 (row
   // m's swizzle (m >> 1) & 7 is col's, 32 (wr RT + t) being a multiple of 16); B fragment of
   // column tile c, W stage + ((CT wc + c) * 256 + 64 s + lane) * 16.
-  static_assert(RT == 5 && CT == 2, "the waits below name five A and two B fragments");
+  static_assert(RT + CT <= 15, "one lgkmcnt covers a step's fragment reads");
   const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) u32x4*)sm;   // LDS byte address
   uint32_t aaddr[4];
 #pragma unroll
   for (int s = 0; s < 4; ++s)
     aaddr[s] = lds0 + (32 * wr * RT + col) * 128 + (((4 * half + s) ^ ((col >> 1) & 7)) << 4);
   const uint32_t baddr = lds0 + 2 * kHStage * 16 + (CT * wc * 256 + lane) * 16;
-  auto lds_read = [](uint32_t addr) {
-    u32x4 v;
-    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr) : "memory");
-    return v;
-  };
+  auto lds_read = [](uint32_t addr) { return lds_read_b128(addr); };
   auto compute = [&](int stage) {
     u32x4 a[2][RT], b[2][CT];
     auto frags = [&](int s, int x) {
@@ -445,18 +461,15 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
       const int x = s & 1;
       if (s < 3) {
         frags(s + 1, x ^ 1);
-        asm volatile("s_waitcnt lgkmcnt(7)"
-                     : "+v"(a[x][0]), "+v"(a[x][1]), "+v"(a[x][2]), "+v"(a[x][3]), "+v"(a[x][4]), "+v"(b[x][0]),
-                       "+v"(b[x][1])
-                     :
-                     : "memory");
+        wait_lgkm<RT + CT>();   // this step's reads done; the next step's stay in flight
       } else {
-        asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(a[x][0]), "+v"(a[x][1]), "+v"(a[x][2]), "+v"(a[x][3]), "+v"(a[x][4]), "+v"(b[x][0]),
-                       "+v"(b[x][1])
-                     :
-                     : "memory");
+        wait_lgkm<0>();
       }
+      // tie the fragments to the wait, so that no use of them moves above it
+#pragma unroll
+      for (int t = 0; t < RT; ++t) tie(a[x][t]);
+#pragma unroll
+      for (int c = 0; c < CT; ++c) tie(b[x][c]);
 #pragma unroll
       for (int t = 0; t < RT; ++t)
 #pragma unroll
@@ -576,7 +589,7 @@ __global__ __launch_bounds__(512) void lm_head_wide_kernel(LmParams p) {
   }
   __syncthreads();
   constexpr int kWavesPerStat = WC / kStatTiles;
-  for (int q = threadIdx.x; q < rows * kStatTiles; q += 512) {
+  for (int q = threadIdx.x; q < rows * kStatTiles; q += 64 * kWaves) {
     const int r = q % rows, st = q / rows, w0 = st * kWavesPerStat;
     const int stile = nt * kStatTiles + st;
     if (stile >= p.ntiles) continue;
@@ -664,7 +677,8 @@ hipError_t launch_projection(const LmParams& p, hipStream_t s) {
     LmParams q = p;
     q.mgroups = (p.M + 319) / 320;
     const int wgcols = (p.V + 255) / 256;
-    hipLaunchKernelGGL(lm_head_wide_kernel, dim3((unsigned)((wgcols + 7) / 8 * 8 * q.mgroups)), dim3(512), 0, s, q);
+    hipLaunchKernelGGL((lm_head_wide_kernel<5, 2, 2, 4>), dim3((unsigned)((wgcols + 7) / 8 * 8 * q.mgroups)),
+                       dim3(512), 0, s, q);
     return hipGetLastError();
   }
   if (group_rows(p.M) == 192) return launch_lm_nrt<6, 2, 1, 2, 4, 1>(p, s);

@@ -69,11 +69,13 @@ def check(h, hb, w, wb, T, rows_idx=None):
     return logits, stats
 
 
-# (320, 2048), (200, 70001), (961, 4099) and (1500, 9000) run the eight-wave kernel: one group,
-# a vocabulary whose last packed tile is part zeros, a last group of one row, a last group of
-# 220 rows with a 40-column last tile; (333, 3000) and (700, 130) the four-wave groups
+# (320, 2048), (200, 70001), (961, 4099), (1500, 9000) and (1100, 70001) run the eight-wave
+# kernel: one group, a vocabulary whose last packed tile is part zeros, a last group of one row,
+# a last group of 220 rows with a 40-column last tile, a last group of 140 rows with a
+# part-zero last packed tile; (333, 3000) and (700, 130) the four-wave groups of 160 or 192 rows
 @pytest.mark.parametrize("rows,V,d", [(1, 1000, 256), (37, 4101, 512), (320, 2048, 256), (333, 3000, 256),
-                                      (700, 130, 512), (1500, 9000, 256), (200, 70001, 256), (961, 4099, 512)])
+                                      (700, 130, 512), (1500, 9000, 256), (200, 70001, 256), (961, 4099, 512),
+                                      (1100, 70001, 512)])
 def test_lm_head_small_shapes(rows, V, d):
     h, hb = bf16_pair((rows, d), 1, 1.0)
     w, wb = bf16_pair((V, d), 2, 0.05)
@@ -125,7 +127,7 @@ def test_lm_head_large_row_count_sampled_rows():
     rows, V, d = 4608, 152064, 3584
     h, hb = bf16_pair((rows, d), 7, 1.0)
     w, wb = bf16_pair((V, d), 8, 0.02)
-    sel = [0, 159, 160, 191, 192, 319, 320, 2301, 4479, 4480, 4607]
+    sel = [0, 159, 160, 191, 192, 255, 256, 319, 320, 2301, 4351, 4352, 4479, 4480, 4607]
     say(f"[lm head] rows={rows} V={V} d={d} (rows {sel} checked)")
     check(h, hb, w, wb, 0.7, rows_idx=sel)
 
