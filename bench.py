@@ -26,6 +26,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+PHASE_STEPS = 100           # event-timed steps per phase pass (at least; more when --steps is larger)
 MFMA_BF16_TFLOPS = 2500.0   # dense bf16 matrix-core peak of the MI355X
 METRIC = "verified tokens/sec (verify-attn + accept) at 1 GPU; achieved HBM GB/s"
 
@@ -333,16 +334,17 @@ def main():
     torch.cuda.synchronize()
     elapsed_warm = time.perf_counter() - t0
 
-    # Per-phase durations: K more steps with HIP events on the launch stream around each call
+    # Per-phase durations: max(K, 100) more steps with HIP events on the launch stream around each call
     # (an event record idles the stream for a few microseconds, so these steps are not the ones
     # `value` is computed from): cold as in the timed region, warm, and after a 1 GiB read
     # (a reduction over a scratch buffer: it leaves no dirty lines to write back) before every step.
-    cold = phase_pass(torch, steps, K, stream)
-    warm = phase_pass(torch, [step], K, stream)
+    KP = max(K, PHASE_STEPS)
+    cold = phase_pass(torch, steps, KP, stream)
+    warm = phase_pass(torch, [step], KP, stream)
     flushed = None
     if args.copy_probe == 0:
         fa = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
-        flushed = phase_pass(torch, [step], K, stream, flush=lambda: fa.sum())
+        flushed = phase_pass(torch, [step], KP, stream, flush=lambda: fa.sum())
         del fa
         torch.cuda.empty_cache()
     # the read-rate probe (not in counter runs: its copies would be taken for the calibration's)
@@ -398,7 +400,8 @@ def main():
                    "launch": "hip_graph" if args.graph else "eager"},
         "protocol": f"cold (headline): {R} copies of the inputs used in turn, {(R - 1) * abytes / 2**30:.2f} GiB "
                     f"of other steps' attention reads between two uses of one copy; warm: one copy back to back; "
-                    f"flushed: one copy, a 1 GiB read before each step (phase times only)",
+                    f"flushed: one copy, a 1 GiB read before each step (phase times only); phase statistics "
+                    f"over {KP} event-timed steps per pass",
         "warm": {"value": round(emitted / (ms_step_warm * 1e-3), 1), "ms_per_step": round(ms_step_warm, 4)},
         "phases_us": {"append": round(ms_append * 1e3, 2), "verify_attention": round(ms_attn * 1e3, 2),
                       "accept": round(ms_accept * 1e3, 2)},
