@@ -348,7 +348,6 @@ void verify_attn_kernel(AttnParams p) {
   auto end_item = [&](int i) {
     const bool ends_after = pc.t < pc.nt - 1;
     const bool whole = !starts_before && !ends_after;
-    float* slot = slots + (starts_before ? 0 : slot_f);
     if (!whole && !starts_before) {   // this wave holds the item's first tiles
       head_flag = 1;
       head_b = pc.b;
@@ -357,14 +356,12 @@ void verify_attn_kernel(AttnParams p) {
       head_q0 = q0;
       head_n = n;
     }
-    // Outputs (and, with one row tile, partials) leave through the wave's LDS scratch, transposed,
-    // so that each store writes whole 16-byte chunks of consecutive rows: stored straight from
-    // the accumulators, an instruction writes 8 or 16 bytes into each of 32 rows, and a timing-
-    // only copy without the output stores ran 29 us (10%) faster at 63 rows per item.  The scratch
-    // holds Q's row tile 0 during the item, no longer needed here; a wave's LDS operations run in
-    // order.
+    // Outputs leave through the wave's LDS scratch, transposed, so that each store writes whole
+    // 16-byte chunks of consecutive rows: stored straight from the accumulators, an instruction
+    // writes 8 bytes into each of 32 rows, and a timing-only copy without the output stores ran
+    // 29 us (10%) faster at 63 rows per item.  The scratch holds Q's row tile 0 during the item,
+    // no longer needed here; a wave's LDS operations run in order.
     constexpr int kOc = D / 8;   // 16-byte chunks of a bf16 output row
-    constexpr int kPc = D / 4;   // 16-byte chunks of an fp32 partial row
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const float lt = halves_sum(l[nt]);
@@ -406,46 +403,9 @@ void verify_attn_kernel(AttnParams p) {
         }
         st_m[nt] = m[nt];
         st_l[nt] = lt;
-      } else if (NT == 2) {
-        // With two row tiles the partials go straight from the accumulators: a transpose here
-        // (any loop over the scratch) made the compiler spill registers in the tile loop.
-        if (lr < R) {
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int a = 0; a < 4; ++a) {
-              const f32x4 v = {acc[nt][mt][4 * a], acc[nt][mt][4 * a + 1], acc[nt][mt][4 * a + 2], acc[nt][mt][4 * a + 3]};
-              *reinterpret_cast<f32x4*>(slot + (int64_t)lr * D + 32 * mt + 8 * a + 4 * half) = v;
-            }
-        }
-      } else {
-        // fp32 rows, 16 at a time: chunk c of row rl at chunk c ^ rl of the scratch row
-#pragma unroll 1
-        for (int p2 = 0; p2 < 2; ++p2) {
-          if ((col >> 4) == p2) {
-            const int rl = col & 15;
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-              for (int a = 0; a < 4; ++a) {
-                scr[rl * kPc + ((8 * mt + 2 * a + half) ^ (rl & (kPc - 1)))] =
-                    u32x4{__float_as_uint(acc[nt][mt][4 * a]), __float_as_uint(acc[nt][mt][4 * a + 1]),
-                          __float_as_uint(acc[nt][mt][4 * a + 2]), __float_as_uint(acc[nt][mt][4 * a + 3])};
-                __builtin_amdgcn_sched_barrier(0);
-              }
-          }
-#pragma unroll 1
-          for (int q = lane; q < 16 * kPc; q += kWave) {
-            const int rl = q / kPc, c = q % kPc, r = nt * 32 + 16 * p2 + rl;
-            const u32x4 v = scr[rl * kPc + (c ^ (rl & (kPc - 1)))];
-            if (r < R) *reinterpret_cast<u32x4*>(slot + (int64_t)r * D + 4 * c) = v;
-          }
-        }
       }
-      if (!whole && !starts_before && half == 0 && lr < R) {
-        slot[(int64_t)p.rmax * D + lr] = m[nt];
-        slot[(int64_t)p.rmax * D + p.rmax + lr] = lt;
-      }
+      // (an item this wave starts and a later share finishes is the share's last: its partial
+      // is stored after the tile loop, from the accumulators it leaves behind)
     }
     if (starts_before) {
       stashed = true;
@@ -544,6 +504,41 @@ void verify_attn_kernel(AttnParams p) {
     for (int d = 0; d < DEPTH; ++d) {
       process(buf[d], i + d);
       load_tile(buf[d], i + d + DEPTH);
+    }
+  }
+
+  // The share's last item, if a later share finishes it: its partial to slot 1, through the LDS
+  // scratch in two halves of the head dimension (32 rows x D/2 columns each), so that each store
+  // writes 16-byte chunks of consecutive rows.  Here, past the tile loop, the transpose costs no
+  // registers the loop needs (inside it, it spilled).
+  if (head_flag) {
+    constexpr int kHc = D / 8;   // 16-byte chunks of half an fp32 row
+    float* slot1 = slots + slot_f;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const float lt = halves_sum(l[nt]);
+      const int lr = nt * 32 + col;
+#pragma unroll
+      for (int hm = 0; hm < 2; ++hm) {
+#pragma unroll
+        for (int mt = hm * MT / 2; mt < (hm + 1) * MT / 2; ++mt)
+#pragma unroll
+          for (int a = 0; a < 4; ++a) {
+            const int c = 8 * (mt - hm * MT / 2) + 2 * a + half;
+            scr[col * kHc + (c ^ (col & (kHc - 1)))] =
+                u32x4{__float_as_uint(acc[nt][mt][4 * a]), __float_as_uint(acc[nt][mt][4 * a + 1]),
+                      __float_as_uint(acc[nt][mt][4 * a + 2]), __float_as_uint(acc[nt][mt][4 * a + 3])};
+          }
+        for (int q = lane; q < 32 * kHc; q += kWave) {
+          const int row = q / kHc, c = q % kHc, r = nt * 32 + row;
+          const u32x4 v = scr[row * kHc + (c ^ (row & (kHc - 1)))];
+          if (r < R) *reinterpret_cast<u32x4*>(slot1 + (int64_t)r * D + hm * (D / 2) + 4 * c) = v;
+        }
+      }
+      if (half == 0 && lr < R) {
+        slot1[(int64_t)p.rmax * D + lr] = m[nt];
+        slot1[(int64_t)p.rmax * D + p.rmax + lr] = lt;
+      }
     }
   }
 
