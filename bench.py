@@ -136,13 +136,16 @@ def cpu_model() -> str:
 
 
 def _read_probe():
-    """spexis_probe_stream_read of libspexis_probe.so (plain coalesced 16-byte loads)."""
+    """The read probes of libspexis_probe.so (coalesced 16-byte loads, strided or in chunks)."""
     import ctypes
     from paper_2609_34370_amd import build as _b
     probe = ctypes.CDLL(_b.PROBE_LIB_PATH)
     probe.spexis_probe_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
                                                ctypes.c_void_p]
     probe.spexis_probe_stream_read.restype = ctypes.c_int
+    probe.spexis_probe_chunk_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int64,
+                                              ctypes.c_void_p, ctypes.c_void_p]
+    probe.spexis_probe_chunk_read.restype = ctypes.c_int
     return probe
 
 
@@ -166,9 +169,10 @@ def settle(torch, fn, ms=SETTLE_MS):
 
 
 def stream_peaks(torch, nbytes=4 << 30, reps=5):
-    """Measured HBM rates on this GPU: the read probe of libspexis_probe.so (plain coalesced
-    16-byte loads over a 4 GiB buffer, best grid and repetition) and torch's device copy (bytes
-    read plus bytes written per second)."""
+    """Measured HBM rates on this GPU: the read probes of libspexis_probe.so over a 4 GiB
+    buffer (coalesced 16-byte non-temporal loads, grid-strided or in contiguous chunks per
+    workgroup; the best pattern, grid and repetition is `read`, each pattern's best is reported
+    too) and torch's device copy (bytes read plus bytes written per second)."""
     import ctypes
     probe = _read_probe()
     src = torch.zeros(nbytes // 4, dtype=torch.float32, device="cuda")
@@ -194,8 +198,17 @@ def stream_peaks(torch, nbytes=4 << 30, reps=5):
         if rc != 0:
             raise RuntimeError(f"stream probe failed: {rc}")
 
-    out = {"read": round(max(nbytes / best(lambda g=g: read(g)) / 1e9 for g in (1024, 2048, 4096, 8192)), 1),
-           "copy": round(2 * nbytes / best(lambda: dst.copy_(src)) / 1e9, 1)}
+    def chunks(grid, chunk):
+        rc = probe.spexis_probe_chunk_read(ctypes.c_void_p(src.data_ptr()), nbytes, grid, chunk,
+                                           ctypes.c_void_p(sink.data_ptr()), s)
+        if rc != 0:
+            raise RuntimeError(f"stream probe failed: {rc}")
+
+    strided = max(nbytes / best(lambda g=g: read(g)) / 1e9 for g in (1024, 2048, 4096, 8192))
+    chunked = max(nbytes / best(lambda g=g, c=c: chunks(g, c)) / 1e9
+                  for g in (2048, 4096) for c in (64 << 10, 1 << 20))
+    out = {"read": round(max(strided, chunked), 1), "read_strided": round(strided, 1),
+           "read_chunked": round(chunked, 1), "copy": round(2 * nbytes / best(lambda: dst.copy_(src)) / 1e9, 1)}
     del src, dst, sink
     torch.cuda.empty_cache()
     return out
