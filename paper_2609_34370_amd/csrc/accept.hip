@@ -1069,16 +1069,17 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
     return launch_search(q, s);
   }
   if (p.kind == 1) {
-    // Rounds of doubling width, at most three.  A round costs a few
-    // microseconds of launch and latency, a row 4V bytes: with short rows (under 256 KB) that
-    // together stream in well under that many rounds' worth of time, one round reads every
-    // row.  Otherwise the first round is two positions wide ({0,1}, {2..5}, {6..13}, ...), so
-    // that sequences passing the first test need no extra launch, unless its four rows per
-    // sequence come to more than 256 MB: then the rows a first rejection leaves unread cost
-    // more than a launch, and the rounds are {0}, {1,2}, {3..6}, ....  (Measured: rounds save
-    // 3.5 us at 64 sequences of 128256-entry rows, and cost 2.6 us at 128 of 32000; a first
-    // round of one position costs 7 us at 64 sequences of 128256 entries and saves 3 us at 256
-    // of them and 57 us at 512 of 152064.)
+    // Rounds of doubling width, at most three.  A round costs a few microseconds of launch and
+    // latency, a row 4V bytes: with short rows (under 256 KB) that together stream in well
+    // under that many rounds' worth of time, one round reads every row.  Otherwise the first
+    // round is two positions wide ({0,1}, {2..5}, the rest), so that sequences passing the
+    // first test need no extra launch, unless its four rows per sequence come to more than
+    // 256 MB: then the rows a first rejection leaves unread cost more than a launch, and the
+    // rounds are {0}, {1,2}, the rest.  (Measured: rounds save 3.5 us at 64 sequences of
+    // 128256-entry rows, and cost 2.6 us at 128 of 32000; a first round of one position costs
+    // 7 us at 64 sequences of 128256 entries and saves 3 us at 256 of them and 57 us at 512 of
+    // 152064; one round over every position is 4.5 us slower at 64 of 128256, its 0.295 GB
+    // statistics pass at 5.9 TB/s.)
     const bool one_round =
         (int64_t)p.V * 4 < kRoundRowBytes && (int64_t)p.B * (p.max_k + 1) * p.V * 4 <= kOneRoundBytes;
     int width = one_round ? p.max_k + 1 : ((int64_t)p.B * 4 * p.V * 4 > kNarrowFirstBytes ? 1 : 2);
