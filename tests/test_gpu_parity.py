@@ -153,6 +153,34 @@ def test_attention_skewed_share_pairs_odd_head_count():
                     ctx=("uniform", 9000, 11000), k=("fixed", 4))
 
 
+def random_attention_geometry(seed):
+    """One random attention geometry (seeded; the test's own draw): head size, block size, KV
+    heads, group size and draft counts within the boundary's limits (G (k+1) <= 64 rows), batch,
+    context range and KV split setting."""
+    r = np.random.default_rng(1000 + seed)
+    D = int(r.choice([64, 128]))
+    bs = int(r.choice([16, 32]))
+    hkv = int(r.choice([1, 2, 3, 4, 8]))
+    G = int(r.choice([1, 2, 4, 7, 8]))
+    kmax = int(r.integers(0, 64 // G))           # rows G (k+1) <= 64
+    klo = int(r.integers(0, kmax + 1))
+    lo = int(r.integers(0, 2000))
+    hi = lo + int(r.integers(0, 2500))
+    over = dict(batch=int(r.integers(1, 41)), num_q_heads=G * hkv, num_kv_heads=hkv, head_dim=D, block_size=bs,
+                ctx=("uniform", lo, hi), k=("uniform", klo, kmax))
+    return over, int(r.choice([0, 0, 32, 64, 160, 1024]))
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_attention_random_geometry(seed):
+    # every row of every sequence against the oracle, over random mixes of the kernel's paths:
+    # one or two row tiles, head sizes 64 and 128, block sizes 16 and 32, items whole or cut
+    # between shares at random points, empty caches and k = 0 rows
+    over, chunk = random_attention_geometry(seed)
+    say(f"[attention random] seed {seed}: {over} kv_chunk_tokens={chunk}")
+    check_attention(1, seed=2000 + seed, kv_chunk_tokens=chunk, **over)
+
+
 def test_attention_block_permutation_invariance():
     spec, batch, attn, _ = case(1, seed=9, accept=False, batch=5, ctx=("uniform", 40, 200))
     step = VerifyStep(batch, attn, None)
@@ -348,8 +376,8 @@ def test_accept_logits_agrees_with_oracle(wid):
 
 def test_accept_logits_rounds_with_ragged_drafts():
     # 128 sequences, k_b in 0..8, V = 128256: 590 MB of target rows, so the tests run in rounds,
-    # and a first round over {0,1} would read 263 MB, so they are {0}, {1,2}, {3..6}, {7,8};
-    # draft noise spread U[0.1, 3] sends some sequences through all four
+    # and a first round over {0,1} would read 263 MB, so they are {0}, {1,2}, {3..8}; draft
+    # noise spread U[0.1, 3] sends some sequences through all three
     spec, batch, attn, acc = case(4, vocab=128256)
     assert batch.B * (batch.max_k + 1) * spec.vocab * 4 > (192 << 20)
     say(f"[accept logits rounds] B={batch.B} V={spec.vocab} k in [{batch.k.min()}, {batch.k.max()}]")
@@ -364,6 +392,41 @@ def test_accept_logits_rounds_with_ragged_drafts():
     assert (a >= 3).sum() > 0 and (a >= 7).sum() > 0, "some sequences must reach the later rounds"
     diff = [b for b in range(batch.B) if a[b] != ra[b] or not np.array_equal(t[b], rt[b])]
     say(f"  accepted histogram={np.bincount(a, minlength=9).tolist()} disagreements={len(diff)}")
+    for b in diff:
+        assert borderline(p, q, ids, ua, us, batch.qsl, b, ra[b], rt[b], a[b], t[b]), b
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_accept_random_geometry(seed):
+    # random batch, vocabulary (not a multiple of 4 or of a sub-chunk), ragged draft counts up
+    # to the boundary's 32, draft noise and temperature: probabilities bit-exact, logits equal
+    # to the oracle's exact rule on its fp64 softmax (within 1e-5 of a decision boundary)
+    r = np.random.default_rng(3000 + seed)
+    V = int(r.integers(1000, 200000))
+    kmax = int(r.integers(0, 33))
+    over = dict(batch=int(r.integers(1, 41)), vocab=V, k=("uniform", int(r.integers(0, kmax + 1)), kmax),
+                draft_noise=("uniform", 0.05, float(r.uniform(0.5, 4.0))), temperature=float(r.choice([0.5, 1.0, 1.7])),
+                target_std=float(r.uniform(1.0, 4.0)), ctx=("uniform", 1, 64))
+    spec, batch, attn, acc = case(1, seed=4000 + seed, **over)
+    say(f"[accept random] seed {seed}: B={batch.B} V={V} k in [{batch.k.min()}, {batch.k.max()}] "
+        f"T={spec.temperature}")
+    p, q = oracle_probs(acc)
+    ids, ua, us = acc.draft_ids.cpu().numpy(), acc.u_accept.cpu().numpy(), acc.u_sample.cpu().numpy()
+    ra, rt, rs, _ = oracle.accept(batch.qsl, p, q, ids, ua, us, max_k=batch.max_k)
+    step = VerifyStep(batch, attn, acc)
+    step.accept(target=torch.as_tensor(p, device="cuda"), draft=torch.as_tensor(q, device="cuda"),
+                kind=sx.SPEXIS_INPUT_PROBS)
+    torch.cuda.synchronize()
+    a, t, s_ = step.accept_outputs()
+    np.testing.assert_array_equal(a, ra)   # the oracle's rule on these same fp32 probabilities
+    np.testing.assert_array_equal(t, rt)
+    np.testing.assert_array_equal(s_, rs)
+    step.accept()
+    torch.cuda.synchronize()
+    a, t, s_ = step.accept_outputs()
+    assert (s_ == 0).all() and (rs == 0).all()
+    diff = [b for b in range(batch.B) if a[b] != ra[b] or not np.array_equal(t[b], rt[b])]
+    say(f"  mean accepted={a.mean():.3f} disagreements={len(diff)}")
     for b in diff:
         assert borderline(p, q, ids, ua, us, batch.qsl, b, ra[b], rt[b], a[b], t[b]), b
 
