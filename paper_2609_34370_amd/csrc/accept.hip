@@ -14,10 +14,11 @@
 // reads the same partials.  Kernels, in order on the caller's stream (kernel boundaries are
 // the only synchronisation):
 //   rounds    (logit inputs) the tests run in rounds of doubling width, positions {0,1},
-//             {2..5}, then all the rest (or {0}, {1,2}, the rest, when a first round over {0,1}
-//             would read a lot; one round for short rows); a round takes only the sequences
-//             that passed every test before it (a device-side list), so rows past a rejection
-//             are rarely read.
+//             {2..5}, {6..13}, ... (or {0}, {1,2}, {3..6}, ... when a first round over {0,1}
+//             would read a lot; one round for short rows), a round from the third on taking
+//             every remaining position when they are at most twice its width; a round takes
+//             only the sequences that passed every test before it (a device-side list), so rows
+//             past a rejection are rarely read.
 //     stats   round 0: the statistics (max, sum of 2^(y - max)) of its target and draft rows,
 //             per (row, sub-chunk), and the inputs of its tests.  The tests of a round are
 //             independent of each other, so nothing here waits for a decision.
@@ -1069,7 +1070,7 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
     return launch_search(q, s);
   }
   if (p.kind == 1) {
-    // Rounds of doubling width, at most three.  A round costs a few microseconds of launch and
+    // Rounds of doubling width.  A round costs a few microseconds of launch and
     // latency, a row 4V bytes: with short rows (under 256 KB) that together stream in well
     // under that many rounds' worth of time, one round reads every row.  Otherwise the first
     // round is two positions wide ({0,1}, {2..5}, the rest), so that sequences passing the
@@ -1095,19 +1096,19 @@ hipError_t launch_accept(const AcceptParams& p, hipStream_t s) {
       }
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    // The third round takes every remaining position: few sequences get that far, and a
-    // round's two launches cost more than the rows a later rejection would have left unread
-    // (measured: 4 us faster at 512 sequences of 152064 entries with k = 8, level at 128 and
-    // 256 sequences of 128256).
-    for (int r = 0, lo = 0, w = width; lo <= p.max_k; ++r) {
+    // From the third round on, a round takes every remaining position when they are at most
+    // twice its width: few sequences get that far, and a round's two launches cost more than
+    // the rows a later rejection would have left unread (measured: 4 us faster at 512
+    // sequences of 152064 entries with k = 8, level at 128 and 256 sequences of 128256).
+    // Longer remainders keep doubling, so a sequence never reads more than about twice the rows
+    // its tests need.
+    const auto round_end = [&](int r, int lo, int w) { return r >= 2 && p.max_k + 1 - lo <= 2 * w ? p.max_k + 1 : lo + w; };
+    for (int r = 0, lo = 0, w = width, hi; lo <= p.max_k; ++r, lo = hi, w *= 2) {
       // round r, positions [lo, hi); a sequence passing all of it computes round r+1's
       // statistics, positions [hi, hi2)
-      const int hi = r >= 2 ? p.max_k + 1 : lo + w;
-      const int nw = r >= 1 ? p.max_k + 1 - hi : 2 * w;
-      const int hi2 = hi <= p.max_k ? hi + nw : 0;
+      hi = round_end(r, lo, w);
+      const int hi2 = hi <= p.max_k ? round_end(r + 1, hi, 2 * w) : 0;
       if ((e = launch_round(p, r, lo, hi, hi2, s)) != hipSuccess) return e;
-      lo = hi;
-      w = nw;
     }
   } else {
     hipLaunchKernelGGL(accept_init_kernel, dim3((p.B + kThreads - 1) / kThreads), dim3(kThreads), 0, s, p);

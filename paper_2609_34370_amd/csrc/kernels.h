@@ -153,7 +153,7 @@ struct AcceptParams {
 };
 
 constexpr int kAcceptMaxK = 32;      // drafts per sequence the boundary takes (below one wave's lanes)
-constexpr int kAcceptMaxRounds = 3;  // test rounds (the third takes every remaining position)
+constexpr int kAcceptMaxRounds = 8;  // test rounds: widths 2, 4, 8, ... cover max_k <= 509
 constexpr int kAcceptSub = 4096;     // vocab entries per partial result (one workgroup's share)
 
 hipError_t launch_append(const AppendParams& p, hipStream_t s);

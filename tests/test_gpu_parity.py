@@ -491,8 +491,8 @@ def test_accept_logits_edge_rows_across_rounds():
 @pytest.mark.parametrize("V", [70001, 1100001])
 def test_accept_most_drafts_every_round_odd_vocab(V):
     # max_k = 32 (the largest the boundary takes).  V = 70001: rows of 280 KB, logits-mode rounds
-    # {0,1}, {2..5}, {6..32}; V = 1100001: a first round over {0,1} would read 282 MB, so the
-    # rounds are {0}, {1,2}, {3..32}.  Sequence b has
+    # {0,1}, {2..5}, {6..13}, {14..32}; V = 1100001: a first round over {0,1} would read 282 MB,
+    # so the rounds are {0}, {1,2}, {3..6}, {7..14}, {15..32}.  Sequence b has
     # k_b drafts and a draft row equal to the target row at positions below m_b (those tests
     # always pass), a noisy one after; the m_b sit on both sides of every round boundary of both
     # schedules.  Neither vocabulary is a multiple of 4 entries.
