@@ -510,10 +510,20 @@ void verify_attn_kernel(AttnParams p) {
   // The share's last item, if a later share finishes it: its partial to slot 1, through the LDS
   // scratch in two halves of the head dimension (32 rows x D/2 columns each), so that each store
   // writes 16-byte chunks of consecutive rows.  Here, past the tile loop, the transpose costs no
-  // registers the loop needs (inside it, it spilled).  Partials are written once and read by the
-  // merge launch: non-temporal, like the outputs, so that the end of this launch does not wait
-  // for them to be written back from the caches (the call 11.6 us faster at 63 rows per item and
-  // 99 MB of partials, level at 20 rows per item).
+  // registers the loop needs (inside it, it spilled).
+  // Partials are written once and read by the merge launch.  With two row tiles (33 to 64 rows:
+  // large partials) they are stored non-temporally, like the outputs, so that the end of this
+  // launch does not wait for them to be written back from the caches (the call 11.6 us faster at
+  // 63 rows per item, 99 MB of partials); with one row tile plain stores leave the merge's reads
+  // to the caches (at 20 rows per item the merge ran 6.0 against 7.6 us, the call 1 us faster).
+  auto put4 = [](float* a, u32x4 v) {
+    if (NT == 2) __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(a));
+    else *reinterpret_cast<u32x4*>(a) = v;
+  };
+  auto put1 = [](float* a, float v) {
+    if (NT == 2) __builtin_nontemporal_store(v, a);
+    else *a = v;
+  };
   if (head_flag) {
     constexpr int kHc = D / 8;   // 16-byte chunks of half an fp32 row
     float* slot1 = slots + slot_f;
@@ -535,29 +545,29 @@ void verify_attn_kernel(AttnParams p) {
         for (int q = lane; q < 32 * kHc; q += kWave) {
           const int row = q / kHc, c = q % kHc, r = nt * 32 + row;
           const u32x4 v = scr[row * kHc + (c ^ (row & (kHc - 1)))];
-          if (r < R) __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(slot1 + (int64_t)r * D + hm * (D / 2) + 4 * c));
+          if (r < R) put4(slot1 + (int64_t)r * D + hm * (D / 2) + 4 * c, v);
         }
       }
       if (half == 0 && lr < R) {
-        __builtin_nontemporal_store(m[nt], slot1 + (int64_t)p.rmax * D + lr);
-        __builtin_nontemporal_store(lt, slot1 + (int64_t)p.rmax * D + p.rmax + lr);
+        put1(slot1 + (int64_t)p.rmax * D + lr, m[nt]);
+        put1(slot1 + (int64_t)p.rmax * D + p.rmax + lr, lt);
       }
     }
   }
 
-  // the stashed partial to slot 0, 16 bytes per lane and step, non-temporal as above (the wave's
-  // own LDS writes are complete before its reads).  (Issued instead right after the share's last tile load, so that
+  // the stashed partial to slot 0, 16 bytes per lane and step, stored as above (the wave's own
+  // LDS writes are complete before its reads).  (Issued instead right after the share's last tile load, so that
   // the stores drain under the last tiles' compute, it needed the loop split in two, and the
   // kernel ran slower.)
   if (stashed) {
     for (int idx = lane; idx < stash_rows * D / 4; idx += kWave)
-      __builtin_nontemporal_store(sm_stash[wave][idx], reinterpret_cast<f32x4*>(slots + 4 * (int64_t)idx));
+      put4(slots + 4 * (int64_t)idx, __builtin_bit_cast(u32x4, sm_stash[wave][idx]));
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int r = nt * 32 + col;
       if (half == 0 && r < stash_rows) {
-        __builtin_nontemporal_store(st_m[nt], slots + (int64_t)p.rmax * D + r);
-        __builtin_nontemporal_store(st_l[nt], slots + (int64_t)p.rmax * D + p.rmax + r);
+        put1(slots + (int64_t)p.rmax * D + r, st_m[nt]);
+        put1(slots + (int64_t)p.rmax * D + p.rmax + r, st_l[nt]);
       }
     }
   }
