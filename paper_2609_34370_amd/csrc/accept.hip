@@ -658,6 +658,7 @@ __global__ __launch_bounds__(kThreads) void accept_tests_kernel(AcceptParams p, 
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int count = round_count(p, r);
   __shared__ int sm_fail[kWaves];
+  __shared__ f32x4 sm_rc[kWaves];   // row statistics (Mp, Rp, Mq, Rq) a wave computed
   for (int li = blockIdx.x; li < count; li += gridDim.x) {
     int b;
     Geom g;
@@ -673,6 +674,9 @@ __global__ __launch_bounds__(kThreads) void accept_tests_kernel(AcceptParams p, 
     // position i fails when !(u_i q_i(x_i) < p_i(x_i)) (NaN statistics fail)
     const float* tin = p.tin + (int64_t)b * p.max_k * 4;
     const int end = min(hi, g.k);
+    // a wave the round's tests leave idle computes the bonus row's statistics meanwhile, in case
+    // every test passes
+    const int wbonus = hi > g.k && end - lo < kWaves ? max(end - lo, 0) : -1;
     int fail = g.k + 1;   // none
     for (int i = lo + wave; i < end; i += kWaves) {
       const f32x2 t = *reinterpret_cast<const f32x2*>(tin + 4 * i);
@@ -682,8 +686,13 @@ __global__ __launch_bounds__(kThreads) void accept_tests_kernel(AcceptParams p, 
       const float qq = logit_prob(t[1], p.c, rc.Mq, rc.Rq);
       if (!((double)u * (double)qq < (double)pp)) {
         fail = i;
+        if (lane == 0) sm_rc[wave] = f32x4{rc.Mp, rc.Rp, rc.Mq, rc.Rq};   // the sampled row's, if first
         break;
       }
+    }
+    if (wave == wbonus) {
+      const RowCtx rc = row_ctx(p, b, g, g.k, false, lane);
+      if (lane == 0) sm_rc[wave] = f32x4{rc.Mp, rc.Rp, rc.Mq, rc.Rq};
     }
     if (lane == 0) sm_fail[wave] = fail;
     __syncthreads();
@@ -693,10 +702,25 @@ __global__ __launch_bounds__(kThreads) void accept_tests_kernel(AcceptParams p, 
     const u32x4 q0 = u32x4{(uint32_t)b, (uint32_t)g.t0, (uint32_t)g.d0, (uint32_t)g.k};
     if (a < g.k || hi > g.k) {
       // a failure at a: the residual of row a; every test passed and the round reached k: the
-      // bonus row k.  Either way the scale is known from row a's statistics.
+      // bonus row k.  Either way the scale is known from row a's statistics, which the wave that
+      // tested position a (or the one that took the bonus row) computed: the same values row_ctx
+      // gives here.
       const bool residual = a < g.k;
       const int pos = residual ? a : g.k;
-      const RowCtx rc = row_ctx(p, b, g, pos, residual, lane);
+      const int from = residual ? (a - lo) % kWaves : wbonus;
+      RowCtx rc;
+      if (from >= 0) {
+        const f32x4 st = sm_rc[from];
+        rc.P = p.target + (int64_t)(g.t0 + pos) * p.V;
+        rc.Q = residual ? p.draft + (int64_t)(g.d0 + pos) * p.V : nullptr;
+        rc.logits = true;
+        rc.Mp = st[0];
+        rc.Rp = st[1];
+        rc.Mq = residual ? st[2] : 1.f;
+        rc.Rq = residual ? st[3] : 1.f;
+      } else {
+        rc = row_ctx(p, b, g, pos, residual, lane);
+      }
       float M;
       int bad;
       sampled_scale(p, rc, b, residual, lane, M, bad);
