@@ -265,8 +265,8 @@ void verify_attn_kernel(AttnParams p) {
     const int tk = min(t0 + col, lc.S - 1);   // past the end: any valid slot, masked later
     const int kblk = (BS == 16 && (tk >> 4) != 2 * lc.t) ? lb : la;
     const uint16_t* kp = kc + ((int64_t)kblk * p.hkv + h) * head_stride + (tk % BS) * 8 + half * BS * 8;
-    // K tiles are read once: non-temporal loads (measured faster than plain loads of K, or than
-    // non-temporal loads of both K and V, on every workload)
+    // K tiles are read once: non-temporal loads (measured faster than plain loads of K on every
+    // workload, the call alone timed)
 #pragma unroll
     for (int s = 0; s < KS; ++s) B.k[s] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kp + s * (2 * BS * 8)));
 #pragma unroll
@@ -275,7 +275,15 @@ void verify_attn_kernel(AttnParams p) {
       const uint16_t* vp = vc + ((int64_t)vblk * p.hkv + h) * head_stride + (BS == 32 ? 16 * s2 : 0) +
                            8 * half + (int64_t)col * BS;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) B.v[mt][s2] = ld16(vp + (int64_t)(32 * mt) * BS);
+      for (int mt = 0; mt < MT; ++mt) {
+        // V is read once too: non-temporal at block size 16 (the call as fast or faster, and
+        // the acceptance launched after it 2-4 us faster: workload 2 2.7 us faster per step,
+        // workload 3 8.3 us, workload 4 3.1 us); plain at block size 32, where a lane's 16
+        // bytes are half of a 64-byte head-dim row (non-temporal: the call 8 us slower at 512
+        // sequences)
+        const u32x4* a = reinterpret_cast<const u32x4*>(vp + (int64_t)(32 * mt) * BS);
+        B.v[mt][s2] = BS == 16 ? __builtin_nontemporal_load(a) : *a;
+      }
     }
   };
 
